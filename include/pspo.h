@@ -1,0 +1,199 @@
+/*
+ * pspo.h -- C ABI of libpspo: the hot path of a PS-PPO policy update on one
+ * AMD Instinct MI355X (gfx950).
+ *
+ * PS-PPO (prefix-sampling PPO) backpropagates only through a random prefix
+ * t <= H of each completion and reweights every kept token by 1/xi_t, where
+ * xi_t = Pr(H >= t | x) is a per-prompt survival table, so the truncated
+ * update stays an unbiased estimate of the full one (Sec. 3.2, "Unbiased
+ * Stochastic Truncation", the truncated estimator G-hat; App. B).  The three
+ * calls below are the three steps of the update pass that Algorithm 1 lists
+ * after the cutoff design: draw one cutoff per completion, keep the prefixes
+ * (with their weights), and compute the reweighted clipped-ratio PPO loss
+ * (Sec. 3.1) through the LM head together with its gradient.
+ *
+ * Conventions shared by every call
+ *  - Pointers marked "device" must be device memory on the current HIP
+ *    device; "host" pointers are host memory.  Sizes and scalars are by value.
+ *  - The caller allocates and owns every buffer; the library never allocates
+ *    or frees memory and keeps no mutable global state, so calls on distinct
+ *    streams are independent.  Outputs must not alias inputs.
+ *  - Every call is asynchronous on `stream` (0 = the null stream) and returns
+ *    a pspo_status.  Errors detectable from the arguments alone are returned
+ *    before anything is enqueued (the thread-local pspo_last_error() says
+ *    which argument).  Errors only the device can see (a target id outside
+ *    [0, V), an invalid xi table, a capacity overflow) are OR-ed into the
+ *    optional device word `err_flag` (PSPO_DEVERR_* bits); the call does not
+ *    synchronise to report them.
+ *  - bf16 tensors are passed as their raw 16-bit patterns (uint16_t).
+ *  - Rollouts are prompt-major: completion k of prompt p is r = p*K + k.
+ */
+#ifndef PSPO_H_
+#define PSPO_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  PSPO_OK = 0,
+  PSPO_ERR_INVALID_ARG = 1,   /* null / misaligned pointer, negative size, bad scalar */
+  PSPO_ERR_BAD_XI = 2,        /* survival table not in (0,1] or not non-increasing (host check) */
+  PSPO_ERR_WORKSPACE = 3,     /* workspace smaller than pspo_loss_workspace_bytes() */
+  PSPO_ERR_UNSUPPORTED = 4,   /* shape or device the kernels do not handle */
+  PSPO_ERR_HIP = 5            /* a HIP runtime call failed */
+} pspo_status;
+
+/* Bits OR-ed into the optional device word err_flag. */
+#define PSPO_DEVERR_TARGET   1  /* a target id outside [0, V); that token's loss and gradient are 0 */
+#define PSPO_DEVERR_BAD_XI   2  /* a xi value outside (0,1] or an increase along t */
+#define PSPO_DEVERR_CAPACITY 4  /* sum of cutoffs exceeds `capacity`; nothing past it is written */
+#define PSPO_DEVERR_SEQ_ID   8  /* a seq_id outside [0, R); that token's loss and gradient are 0 */
+
+/* Flags of pspo_loss_fwd_bwd. */
+#define PSPO_ACCUMULATE_DW   1u /* d_w_head += gradient instead of d_w_head = gradient */
+
+/* Human-readable name of a status code (static storage). */
+const char* pspo_status_string(int status);
+
+/* Detail of the last error returned on the calling thread ("" if none). */
+const char* pspo_last_error(void);
+
+/* Version of this ABI (incremented on any incompatible change). */
+int pspo_abi_version(void);
+
+/*
+ * Host-side check of survival tables (Sec. 3.2: 1 >= xi_1 >= ... >= xi_T > 0).
+ *  xi      host, float64 [xi_off[P]]: xi[xi_off[p] + t - 1] = xi_{p,t}, t = 1..T_p.
+ *  xi_off  host, int64 [P+1], non-decreasing, xi_off[0] = 0.
+ * Returns PSPO_OK, PSPO_ERR_BAD_XI or PSPO_ERR_INVALID_ARG.  Touches no GPU.
+ */
+int pspo_validate_xi_host(const double* xi, const int64_t* xi_off, int32_t P);
+
+/*
+ * Cutoff sampling: one independent cutoff per completion drawn from the
+ * survival function xi of its prompt (Sec. 3.2, Pr(H >= t | x) = xi_t;
+ * Algorithm 1, the cutoff-sampling step).
+ *
+ * The table is realised exactly on 32-bit uniforms: q_{p,0} = 2^32,
+ * q_{p,t} = max(1, floor(xi_{p,t} * 2^32)); x_r is word 0 of
+ * Philox4x32-10(counter = (r, 0, lo32(offset), hi32(offset)),
+ * key = (lo32(seed), hi32(seed))) (Salmon et al., SC'11);
+ * H_r = min(T_r, max{t in [0, T_p] : x_r < q_{p,t}}).  Hence
+ * Pr(H_r >= t) = q_{p,t} / 2^32 for t <= T_r.
+ *
+ *  xi        device, float64 [xi_off[P]] survival tables (layout as above);
+ *            T_p = xi_off[p+1] - xi_off[p] must be >= every T_r of prompt p.
+ *  xi_off    device, int64 [P+1].
+ *  lengths   device, int32 [P*K], T_r >= 0.
+ *  seed, offset  the Philox key and the high half of the counter.
+ *  cutoffs   device, int32 [P*K] out: H_r in [0, T_r].
+ *  err_flag  device, int32 [1] or NULL: PSPO_DEVERR_BAD_XI if a table is invalid
+ *            (the cutoffs are then still in [0, T_r] but not from the law above).
+ * P = 0 or K = 0 is valid and enqueues nothing.
+ */
+int pspo_sample_cutoffs(const double* xi, const int64_t* xi_off, const int32_t* lengths,
+                        int32_t P, int32_t K, uint64_t seed, uint64_t offset,
+                        int32_t* cutoffs, int32_t* err_flag, hipStream_t stream);
+
+/*
+ * Prefix packing: keep tokens t <= H_r of every completion, concatenated in
+ * rollout order (varlen layout), each with its weight 1/xi_t realised as
+ * float32(2^32 / (double)q_{p,t}) (Sec. 3.2 / 3.3, the 1/xi_t factor of the
+ * truncated estimator; Algorithm 1, the reweighting of token losses).
+ *
+ *  cutoffs, lengths  device, int32 [R], R = P*K <= 65535; a cutoff is clamped to
+ *                    [0, min(T_r, T_p)] (its length and its prompt's table horizon).
+ *  xi, xi_off        device, as in pspo_sample_cutoffs.
+ *  capacity          host-known bound >= sum_r H_r (e.g. sum_r T_r); sizes the
+ *                    per-token outputs.  Excess tokens raise PSPO_DEVERR_CAPACITY.
+ *  target_full       device, int32 [sum T_r] or NULL: token ids of all completions.
+ *  logp_old_full     device, float32 [sum T_r] or NULL: old-policy log-probs.
+ *  hidden_full       device, bf16 bits [sum T_r, d] row-major or NULL (16-byte
+ *                    aligned, d % 8 == 0): final hidden states of all tokens.
+ *  cu_seqlens        device, int32 [R+1] out: cu[0] = 0, cu[r+1] = cu[r] + H_r.
+ *  full_off          device, int32 [R+1] out: offsets of completions in the
+ *                    unpacked arrays (exclusive scan of lengths).
+ *  src_row, seq_id   device, int32 [capacity] out: packed row i = cu[r] + j
+ *                    comes from unpacked row full_off[r] + j of completion r.
+ *  weight            device, float32 [capacity] out.
+ *  target, logp_old  device [capacity] out, gathered; may be NULL iff the
+ *                    corresponding *_full input is NULL.
+ *  hidden            device, bf16 bits [capacity, d] out, gathered; NULL iff
+ *                    hidden_full is NULL.
+ *  n_tokens          device, int32 [1] out: N = cu[R].
+ *  err_flag          device, int32 [1] or NULL.
+ */
+int pspo_pack_prefixes(const int32_t* cutoffs, const int32_t* lengths,
+                       const double* xi, const int64_t* xi_off, int32_t P, int32_t K,
+                       int32_t capacity,
+                       const int32_t* target_full, const float* logp_old_full,
+                       const uint16_t* hidden_full, int32_t d,
+                       int32_t* cu_seqlens, int32_t* full_off, int32_t* src_row,
+                       int32_t* seq_id, float* weight, int32_t* target, float* logp_old,
+                       uint16_t* hidden, int32_t* n_tokens, int32_t* err_flag,
+                       hipStream_t stream);
+
+/*
+ * Bytes of device workspace pspo_loss_fwd_bwd needs for N tokens (host-only,
+ * pure function of its arguments).
+ */
+size_t pspo_loss_workspace_bytes(int32_t N, int32_t d, int32_t V, uint32_t flags);
+
+/*
+ * Fused LM-head + prefix-weighted PPO loss, forward and backward.
+ *
+ * For every packed token i with hidden row h_i, target o_i, old log-prob
+ * lold_i, weight c_i and completion r = seq_id[i] with advantage A_r:
+ *   z_i   = W h_i                                  (App. D: LM-head logits, no bias)
+ *   l_i   = z_{i,o_i} - logsumexp(z_i)             (App. D, first log-sum-exp)
+ *   rho_i = exp(l_i - lold_i)                      (Sec. 3.1, importance ratio)
+ *   s_i   = min(rho_i A, clip(rho_i, 1-eps_low, 1+eps_high) A)   (Sec. 3.1, PPO objective)
+ *   loss  = -loss_scale * sum_i c_i s_i            (Sec. 3.2/3.3 truncated estimator, negated)
+ * and the exact gradients of `loss`:
+ *   delta_i = -loss_scale c_i mu_i rho_i A, mu_i = 1 iff the unclipped branch is active
+ *             (A > 0 and rho <= 1+eps_high, or A < 0 and rho >= 1-eps_low);
+ *   G_i     = delta_i (e_{o_i} - softmax(z_i))     (App. D: grad log p(o) = (e_o - p) h^T)
+ *   d_hidden[i] = G_i W,   d_w_head = sum_i G_i^T h_i.
+ * The [N, V] logits are never written to memory: the kernels recompute logit
+ * tiles on the matrix cores, keeping only per-token softmax statistics and a
+ * bounded vocabulary chunk of bf16 logit gradients in the workspace.
+ *
+ *  hidden     device, bf16 bits [N, d] row-major (packed prefix tokens).
+ *  w_head     device, bf16 bits [V, d] row-major.
+ *  target     device, int32 [N]; logp_old, weight: device float32 [N];
+ *  seq_id     device, int32 [N] in [0, R);  advantage: device float32 [R].
+ *  N >= 0, R >= 1 if N > 0, V >= 1, d > 0 with d % 64 == 0.  All device
+ *  pointers 16-byte aligned.
+ *  eps_low, eps_high in [0, 1); loss_scale finite (e.g. 1/(P*K)).
+ *  flags      PSPO_ACCUMULATE_DW or 0.
+ *  loss       device, float64 [1] out.
+ *  d_hidden   device, float32 [N, d] out.
+ *  d_w_head   device, float32 [V, d] out (or accumulated, see flags).
+ *  logp_new   device, float32 [N] out, or NULL.
+ *  stats      device, float64 [4] out, or NULL: { loss_scale * sum_i |c_i s_i|,
+ *             #tokens with A != 0 and mu = 0 (clipped), #tokens with A == 0,
+ *             max_i c_i }.
+ *  err_flag   device, int32 [1] or NULL (PSPO_DEVERR_TARGET, PSPO_DEVERR_SEQ_ID).
+ *  workspace  device, >= pspo_loss_workspace_bytes(N, d, V, flags) bytes,
+ *             256-byte aligned; its contents on entry are ignored.
+ * N = 0 is valid: loss = 0 and d_w_head is zeroed (unless accumulating).
+ */
+int pspo_loss_fwd_bwd(const uint16_t* hidden, const uint16_t* w_head, const int32_t* target,
+                      const float* logp_old, const float* weight, const int32_t* seq_id,
+                      const float* advantage, int32_t N, int32_t d, int32_t V, int32_t R,
+                      float eps_low, float eps_high, float loss_scale, uint32_t flags,
+                      double* loss, float* d_hidden, float* d_w_head, float* logp_new,
+                      double* stats, int32_t* err_flag, void* workspace, size_t workspace_bytes,
+                      hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PSPO_H_ */

@@ -81,9 +81,11 @@ def pack_prefixes(H, lengths, xi, xi_off, P: int, K: int, target_full=None, logp
     completion in the unpacked token arrays), src_row, seq_id, weight [N], and
     the gathered target / logp_old when given.
     """
-    H = np.asarray(H)
     lengths = np.asarray(lengths)
     R = P * K
+    # a cutoff never exceeds its completion's length nor its prompt's table horizon
+    horizon = np.diff(np.asarray(xi_off))
+    H = np.array([max(0, min(int(H[r]), int(lengths[r]), int(horizon[r // K]))) for r in range(R)], dtype=np.int64)
     cu = np.zeros(R + 1, dtype=np.int32)
     full_off = np.zeros(R + 1, dtype=np.int32)
     for r in range(R):

@@ -1,0 +1,56 @@
+// Internal helpers of libpspo (host error reporting, device vector types).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <cstdio>
+#include <string>
+
+#include "pspo.h"
+
+namespace pspo {
+
+// ---- host-side error reporting -------------------------------------------
+void set_last_error(const std::string& msg);
+void clear_last_error();
+
+// Returns `code` after recording `msg` as the thread's last error.
+inline int fail(int code, const std::string& msg) {
+  set_last_error(msg);
+  return code;
+}
+
+#define PSPO_REQUIRE(cond, code, msg) \
+  do {                                \
+    if (!(cond)) return ::pspo::fail((code), (msg)); \
+  } while (0)
+
+#define PSPO_HIP_CHECK(expr)                                                     \
+  do {                                                                           \
+    hipError_t e_ = (expr);                                                      \
+    if (e_ != hipSuccess)                                                        \
+      return ::pspo::fail(PSPO_ERR_HIP, std::string(#expr ": ") + hipGetErrorString(e_)); \
+  } while (0)
+
+// The kernels are written for CDNA4 (gfx950) only; this checks the current device.
+int require_gfx950();
+
+inline bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
+
+// ---- device vector types ---------------------------------------------------
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+// float -> bf16 bits, round to nearest even (finite inputs).
+__device__ __forceinline__ uint32_t f32_to_bf16_bits(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return u >> 16;
+}
+
+}  // namespace pspo

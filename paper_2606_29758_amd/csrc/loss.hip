@@ -1,0 +1,499 @@
+// Fused LM-head + prefix-weighted PPO loss, forward and backward, on the
+// matrix cores of gfx950.
+//
+// Per packed token i (PS-PPO Sec. 3.1 PPO objective, Sec. 3.2/3.3 truncated
+// estimator, App. D LM-head score):
+//   z_i = W h_i,  l_i = z_{i,o_i} - lse(z_i),  rho_i = exp(l_i - lold_i),
+//   s_i = min(rho_i A, clip(rho_i) A),  loss = -scale * sum_i c_i s_i,
+//   delta_i = -scale c_i mu_i rho_i A,  G_i = delta_i (e_{o_i} - softmax(z_i)),
+//   dH_i = G_i W,  dW = sum_i G_i^T h_i.
+//
+// Schedule (the [N, V] logits never reach memory):
+//   1. forward product z^T = W H^T in 256x256 tiles; the epilogue reduces each
+//      tile column (one token) to a partial (max, sum exp) over the tile's 256
+//      vocabulary rows and picks up the target logit;
+//   2. finalize: merge the partials into lse, then l, rho, the clip mask, delta
+//      and a deterministic float64 loss reduction;
+//   3. transposed bf16 copies H^T [d x Npad] and W^T [d x Vpad] (K-contiguous
+//      operands for the two gradient products);
+//   4. per vocabulary chunk of Vc rows: recompute the chunk's logit tiles and
+//      write the bf16 logit gradient Delta = delta (e_o - exp(z - lse)) in both
+//      layouts ([Npad x Vc] and [Vc x Npad]); then dW[chunk] = Delta^T H and
+//      dH += Delta W[chunk] as two more matrix-core products.
+#include <cmath>
+
+#include "common.h"
+#include "gemm.h"
+
+namespace pspo {
+namespace {
+
+constexpr int64_t kVocabChunk = 16384;   // rows of W per backward chunk
+constexpr float kNegInf = -INFINITY;
+
+// ---------------------------------------------------------------------------
+// Epilogues
+// ---------------------------------------------------------------------------
+
+// Forward: rows = vocabulary (A = W), columns = tokens (B = H).
+struct EpiForward {
+  int V, N;
+  int64_t ldp;  // stride between vocabulary tiles in the partial arrays (= Npad)
+  const int32_t* target;
+  float* part_m;
+  float* part_l;
+  float* zt;
+
+  __device__ __forceinline__ void apply(const AccTile& acc, int tm, int tn, int wm, int wn, int lane, float* smem) const {
+    float* red = smem;  // [2 wave rows][256 columns][m, l]
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int cl = acc_col(wn, j, lane);
+      const int t = tn * kTileN + cl;
+      const int tgt = (t < N) ? target[t] : -1;
+      float m = kNegInf;
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int v = tm * kTileM + acc_row(wm, i, r, lane);
+          const float x = acc.c[i][j][r];
+          if (v < V) {
+            m = fmaxf(m, x);
+            if (v == tgt) zt[t] = x;
+          }
+        }
+      m = fmaxf(m, __shfl_xor(m, 32));
+      float l = 0.f;
+      if (m != kNegInf) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int v = tm * kTileM + acc_row(wm, i, r, lane);
+            if (v < V) l += __expf(acc.c[i][j][r] - m);
+          }
+      }
+      l += __shfl_xor(l, 32);
+      if (lane < 32) {
+        red[(wm * 256 + cl) * 2 + 0] = m;
+        red[(wm * 256 + cl) * 2 + 1] = l;
+      }
+    }
+    __syncthreads();
+    const int c = threadIdx.x;
+    const float m0 = red[c * 2], l0 = red[c * 2 + 1];
+    const float m1 = red[(256 + c) * 2], l1 = red[(256 + c) * 2 + 1];
+    const float M = fmaxf(m0, m1);
+    float L = 0.f;
+    if (m0 != kNegInf) L += l0 * __expf(m0 - M);
+    if (m1 != kNegInf) L += l1 * __expf(m1 - M);
+    const int t = tn * kTileN + c;
+    if (t < N) {
+      part_m[tm * ldp + t] = M;
+      part_l[tm * ldp + t] = L;
+    }
+  }
+};
+
+// Backward logit gradient for one vocabulary chunk: rows = vocabulary rows
+// v0 + vl (A = W[v0:]), columns = tokens.  Writes bf16 Delta to
+// dT[vl][t] (ldT = Npad) and dN[t][vl] (ldN = Vc); zero outside t < N, v < V.
+struct EpiDelta {
+  int V, N, v0;
+  const int32_t* target;
+  const float* lse;
+  const float* delta;
+  uint16_t* dT;
+  int64_t ldT;
+  uint16_t* dN;
+  int64_t ldN;
+
+  __device__ __forceinline__ void apply(const AccTile& acc, int tm, int tn, int wm, int wn, int lane, float*) const {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int t = tn * kTileN + acc_col(wn, j, lane);
+      const bool tv = t < N;
+      const float dl = tv ? delta[t] : 0.f;
+      const float ls = tv ? lse[t] : 0.f;
+      const int tgt = tv ? target[t] : -1;
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int vl0 = tm * kTileM + acc_row(wm, i, g * 4, lane);
+          uint32_t b[4];
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const int vl = vl0 + q;
+            const int v = v0 + vl;
+            float dv = 0.f;
+            if (dl != 0.f && v < V) dv = dl * ((v == tgt ? 1.f : 0.f) - __expf(acc.c[i][j][g * 4 + q] - ls));
+            b[q] = f32_to_bf16_bits(dv);
+            dT[(int64_t)vl * ldT + t] = (uint16_t)b[q];
+          }
+          u32x2 packed;
+          packed.x = b[0] | (b[1] << 16);
+          packed.y = b[2] | (b[3] << 16);
+          *reinterpret_cast<u32x2*>(dN + (int64_t)t * ldN + vl0) = packed;
+        }
+    }
+  }
+};
+
+// dW rows v0 + vl (A = Delta^T), columns = hidden features (B = H^T).
+struct EpiDW {
+  int V, d, v0;
+  float* dW;
+  bool accumulate;
+
+  __device__ __forceinline__ void apply(const AccTile& acc, int tm, int tn, int wm, int wn, int lane, float*) const {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int col = tn * kTileN + acc_col(wn, j, lane);
+      if (col >= d) continue;
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int v = v0 + tm * kTileM + acc_row(wm, i, r, lane);
+          if (v < V) {
+            float* p = dW + (int64_t)v * d + col;
+            *p = accumulate ? *p + acc.c[i][j][r] : acc.c[i][j][r];
+          }
+        }
+    }
+  }
+};
+
+// dH rows = tokens (A = Delta), columns = hidden features (B = W^T[:, v0:]).
+struct EpiDH {
+  int N, d;
+  float* dH;
+  bool first;
+
+  __device__ __forceinline__ void apply(const AccTile& acc, int tm, int tn, int wm, int wn, int lane, float*) const {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int col = tn * kTileN + acc_col(wn, j, lane);
+      if (col >= d) continue;
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int t = tm * kTileM + acc_row(wm, i, r, lane);
+          if (t < N) {
+            float* p = dH + (int64_t)t * d + col;
+            *p = first ? acc.c[i][j][r] : *p + acc.c[i][j][r];
+          }
+        }
+    }
+  }
+};
+
+// ---------------------------------------------------------------------------
+// Small kernels
+// ---------------------------------------------------------------------------
+
+// dst[c][r] = r < rows ? src[r][c] : 0 for r < rows_pad, c < cols (bf16 bits).
+// 64 x 64 tiles through LDS; cols and rows_pad are multiples of 64.
+__global__ __launch_bounds__(256) void transpose_pad_kernel(const uint16_t* __restrict__ src, int rows, int cols,
+                                                            int64_t ld_src, uint16_t* __restrict__ dst,
+                                                            int64_t ld_dst) {
+  __shared__ uint16_t tile[64][66];
+  const int c0 = blockIdx.x * 64, r0 = blockIdx.y * 64;
+  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+  for (int rr = ty; rr < 64; rr += 4) {
+    const int r = r0 + rr;
+    tile[rr][tx] = (r < rows) ? src[(int64_t)r * ld_src + c0 + tx] : (uint16_t)0;
+  }
+  __syncthreads();
+  for (int cc = ty; cc < 64; cc += 4) dst[(int64_t)(c0 + cc) * ld_dst + r0 + tx] = tile[tx][cc];
+}
+
+__global__ void fill_f32_kernel(float* __restrict__ p, int64_t n, float v) {
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+    p[i] = v;
+}
+
+constexpr int kFinThreads = 256;
+
+template <class T>
+__device__ T block_sum(T v, T* sh) {
+  sh[threadIdx.x] = v;
+  __syncthreads();
+  for (int s = kFinThreads / 2; s > 0; s >>= 1) {
+    if (threadIdx.x < s) sh[threadIdx.x] += sh[threadIdx.x + s];
+    __syncthreads();
+  }
+  T r = sh[0];
+  __syncthreads();
+  return r;
+}
+
+__device__ float block_max(float v, float* sh) {
+  sh[threadIdx.x] = v;
+  __syncthreads();
+  for (int s = kFinThreads / 2; s > 0; s >>= 1) {
+    if (threadIdx.x < s) sh[threadIdx.x] = fmaxf(sh[threadIdx.x], sh[threadIdx.x + s]);
+    __syncthreads();
+  }
+  float r = sh[0];
+  __syncthreads();
+  return r;
+}
+
+// Per token: merge the vocabulary-tile partials into lse, then the PPO terms.
+// Each block writes (sum c s, sum |c s|, #clipped, #A==0) and max c to blk[5*b].
+__global__ __launch_bounds__(kFinThreads) void finalize_kernel(
+    int N, int V, int R, int ntv, int64_t ldp, const float* __restrict__ part_m, const float* __restrict__ part_l,
+    const float* __restrict__ zt, const int32_t* __restrict__ target, const float* __restrict__ logp_old,
+    const float* __restrict__ weight, const int32_t* __restrict__ seq_id, const float* __restrict__ adv,
+    float eps_low, float eps_high, float loss_scale, float* __restrict__ lse_out, float* __restrict__ delta_out,
+    float* __restrict__ logp_new, double* __restrict__ blk, int32_t* __restrict__ err_flag) {
+  __shared__ double shd[kFinThreads];
+  __shared__ float shf[kFinThreads];
+  const int t = blockIdx.x * kFinThreads + threadIdx.x;
+  double cs = 0.0, acs = 0.0, nclip = 0.0, nzero = 0.0;
+  float maxw = 0.f;
+  if (t < N) {
+    float M = kNegInf;
+    for (int k = 0; k < ntv; ++k) M = fmaxf(M, part_m[k * ldp + t]);
+    float L = 0.f;
+    for (int k = 0; k < ntv; ++k) L += part_l[k * ldp + t] * __expf(part_m[k * ldp + t] - M);
+    const float lse = M + logf(L);
+    const int tgt = target[t];
+    const int seq = seq_id[t];
+    const bool valid = tgt >= 0 && tgt < V && seq >= 0 && seq < R;
+    const float A = valid ? adv[seq] : 0.f;
+    const float c = weight[t];
+    float l = NAN, s = 0.f, dl = 0.f;
+    bool mu = false;
+    if (valid) {
+      l = zt[t] - lse;
+      const float rho = expf(l - logp_old[t]);
+      const float clipped = fminf(fmaxf(rho, 1.f - eps_low), 1.f + eps_high);
+      s = fminf(rho * A, clipped * A);
+      mu = (A > 0.f && rho <= 1.f + eps_high) || (A < 0.f && rho >= 1.f - eps_low);
+      dl = mu ? -loss_scale * c * rho * A : 0.f;
+    } else if (err_flag) {
+      atomicOr(err_flag, (tgt >= 0 && tgt < V) ? PSPO_DEVERR_SEQ_ID : PSPO_DEVERR_TARGET);
+    }
+    lse_out[t] = lse;
+    delta_out[t] = dl;
+    if (logp_new) logp_new[t] = l;
+    cs = (double)c * (double)s;
+    acs = fabs(cs);
+    nclip = (A != 0.f && !mu) ? 1.0 : 0.0;
+    nzero = (A == 0.f) ? 1.0 : 0.0;
+    maxw = c;
+  }
+  cs = block_sum(cs, shd);
+  acs = block_sum(acs, shd);
+  nclip = block_sum(nclip, shd);
+  nzero = block_sum(nzero, shd);
+  maxw = block_max(maxw, shf);
+  if (threadIdx.x == 0) {
+    double* o = blk + 5 * (int64_t)blockIdx.x;
+    o[0] = cs;
+    o[1] = acs;
+    o[2] = nclip;
+    o[3] = nzero;
+    o[4] = maxw;
+  }
+}
+
+// One block: fixed-order reduction of the per-block sums (deterministic).
+__global__ __launch_bounds__(kFinThreads) void reduce_loss_kernel(int nblk, const double* __restrict__ blk,
+                                                                  float loss_scale, double* __restrict__ loss,
+                                                                  double* __restrict__ stats) {
+  __shared__ double shd[kFinThreads];
+  double v[4] = {0, 0, 0, 0};
+  double mx = 0.0;
+  for (int b = threadIdx.x; b < nblk; b += kFinThreads) {
+    for (int k = 0; k < 4; ++k) v[k] += blk[5 * (int64_t)b + k];
+    mx = fmax(mx, blk[5 * (int64_t)b + 4]);
+  }
+  for (int k = 0; k < 4; ++k) v[k] = block_sum(v[k], shd);
+  shd[threadIdx.x] = mx;
+  __syncthreads();
+  for (int s = kFinThreads / 2; s > 0; s >>= 1) {
+    if (threadIdx.x < s) shd[threadIdx.x] = fmax(shd[threadIdx.x], shd[threadIdx.x + s]);
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    *loss = -(double)loss_scale * v[0];
+    if (stats) {
+      stats[0] = (double)loss_scale * v[1];
+      stats[1] = v[2];
+      stats[2] = v[3];
+      stats[3] = shd[0];
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Workspace plan
+// ---------------------------------------------------------------------------
+
+struct Plan {
+  int64_t Npad, Vpad, Vc, ntv, nfin;
+  int64_t off_pm, off_pl, off_zt, off_lse, off_delta, off_blk, off_ht, off_wt, off_dn, off_dt, total;
+};
+
+Plan make_plan(int64_t N, int64_t d, int64_t V) {
+  Plan p{};
+  p.Npad = round_up(N > 0 ? N : 1, kTileN);
+  p.Vpad = round_up(V, kTileM);
+  p.Vc = p.Vpad < kVocabChunk ? p.Vpad : kVocabChunk;
+  p.ntv = p.Vpad / kTileM;
+  p.nfin = (N + kFinThreads - 1) / kFinThreads;
+  int64_t o = 0;
+  auto take = [&](int64_t bytes) {
+    const int64_t at = o;
+    o = round_up(o + bytes, 256);
+    return at;
+  };
+  p.off_pm = take(p.ntv * p.Npad * 4);
+  p.off_pl = take(p.ntv * p.Npad * 4);
+  p.off_zt = take(p.Npad * 4);
+  p.off_lse = take(p.Npad * 4);
+  p.off_delta = take(p.Npad * 4);
+  p.off_blk = take((p.nfin > 0 ? p.nfin : 1) * 5 * 8);
+  p.off_ht = take(d * p.Npad * 2);
+  p.off_wt = take(d * p.Vpad * 2);
+  p.off_dn = take(p.Npad * p.Vc * 2);
+  p.off_dt = take(p.Vc * p.Npad * 2);
+  p.total = o;
+  return p;
+}
+
+template <class Epi>
+int launch_gemm(const GemmShape& g, const Epi& epi, hipStream_t stream) {
+  hipLaunchKernelGGL(gemm_nt_kernel<Epi>, dim3(gemm_grid(g.tiles_m, g.tiles_n)), dim3(kGemmThreads), 0, stream, g,
+                     epi);
+  PSPO_HIP_CHECK(hipGetLastError());
+  return PSPO_OK;
+}
+
+}  // namespace
+}  // namespace pspo
+
+extern "C" {
+
+size_t pspo_loss_workspace_bytes(int32_t N, int32_t d, int32_t V, uint32_t flags) {
+  (void)flags;
+  if (N < 0 || d <= 0 || V <= 0) return 0;
+  return (size_t)pspo::make_plan(N, d, V).total;
+}
+
+int pspo_loss_fwd_bwd(const uint16_t* hidden, const uint16_t* w_head, const int32_t* target, const float* logp_old,
+                      const float* weight, const int32_t* seq_id, const float* advantage, int32_t N, int32_t d,
+                      int32_t V, int32_t R, float eps_low, float eps_high, float loss_scale, uint32_t flags,
+                      double* loss, float* d_hidden, float* d_w_head, float* logp_new, double* stats,
+                      int32_t* err_flag, void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  using namespace pspo;
+  clear_last_error();
+  PSPO_REQUIRE(N >= 0 && R >= 0, PSPO_ERR_INVALID_ARG, "N and R must be >= 0");
+  PSPO_REQUIRE(d > 0 && V > 0, PSPO_ERR_INVALID_ARG, "d and V must be > 0");
+  PSPO_REQUIRE(d % 64 == 0, PSPO_ERR_UNSUPPORTED, "d must be a multiple of 64");
+  PSPO_REQUIRE(N == 0 || R > 0, PSPO_ERR_INVALID_ARG, "R must be > 0 when N > 0");
+  PSPO_REQUIRE((flags & ~PSPO_ACCUMULATE_DW) == 0, PSPO_ERR_INVALID_ARG, "unknown flag bits");
+  PSPO_REQUIRE(std::isfinite(eps_low) && eps_low >= 0.f && eps_low < 1.f, PSPO_ERR_INVALID_ARG,
+               "eps_low must lie in [0, 1)");
+  PSPO_REQUIRE(std::isfinite(eps_high) && eps_high >= 0.f && eps_high < 1.f, PSPO_ERR_INVALID_ARG,
+               "eps_high must lie in [0, 1)");
+  PSPO_REQUIRE(std::isfinite(loss_scale), PSPO_ERR_INVALID_ARG, "loss_scale must be finite");
+  PSPO_REQUIRE(loss && d_w_head, PSPO_ERR_INVALID_ARG, "loss and d_w_head must not be NULL");
+  PSPO_REQUIRE(aligned(loss, 8) && aligned(d_w_head, 16), PSPO_ERR_INVALID_ARG, "misaligned output pointer");
+  if (N > 0) {
+    PSPO_REQUIRE(hidden && w_head && target && logp_old && weight && seq_id && advantage && d_hidden,
+                 PSPO_ERR_INVALID_ARG, "null input pointer");
+    PSPO_REQUIRE(aligned(hidden, 16) && aligned(w_head, 16) && aligned(d_hidden, 16), PSPO_ERR_INVALID_ARG,
+                 "hidden, w_head and d_hidden must be 16-byte aligned");
+    PSPO_REQUIRE(aligned(target, 4) && aligned(logp_old, 4) && aligned(weight, 4) && aligned(seq_id, 4) &&
+                     aligned(advantage, 4) && aligned(logp_new, 4),
+                 PSPO_ERR_INVALID_ARG, "misaligned per-token pointer");
+    PSPO_REQUIRE(workspace != nullptr && aligned(workspace, 256), PSPO_ERR_INVALID_ARG,
+                 "workspace must be non-NULL and 256-byte aligned");
+  }
+  if (stats) PSPO_REQUIRE(aligned(stats, 8), PSPO_ERR_INVALID_ARG, "misaligned stats");
+  const Plan pl = make_plan(N, d, V);
+  PSPO_REQUIRE(N == 0 || workspace_bytes >= (size_t)pl.total, PSPO_ERR_WORKSPACE,
+               "workspace too small: need " + std::to_string(pl.total) + " bytes");
+  PSPO_REQUIRE(pl.Npad <= INT32_MAX && pl.Vpad <= INT32_MAX, PSPO_ERR_UNSUPPORTED, "problem too large");
+  if (int rc = require_gfx950()) return rc;
+
+  const bool accumulate = (flags & PSPO_ACCUMULATE_DW) != 0;
+  if (N == 0) {
+    if (!accumulate) {
+      hipLaunchKernelGGL(fill_f32_kernel, dim3(1024), dim3(256), 0, stream, d_w_head, (int64_t)V * d, 0.f);
+      PSPO_HIP_CHECK(hipGetLastError());
+    }
+    hipLaunchKernelGGL(reduce_loss_kernel, dim3(1), dim3(kFinThreads), 0, stream, 0, nullptr, loss_scale, loss,
+                       stats);
+    PSPO_HIP_CHECK(hipGetLastError());
+    return PSPO_OK;
+  }
+
+  char* ws = static_cast<char*>(workspace);
+  float* part_m = reinterpret_cast<float*>(ws + pl.off_pm);
+  float* part_l = reinterpret_cast<float*>(ws + pl.off_pl);
+  float* zt = reinterpret_cast<float*>(ws + pl.off_zt);
+  float* lse = reinterpret_cast<float*>(ws + pl.off_lse);
+  float* delta = reinterpret_cast<float*>(ws + pl.off_delta);
+  double* blk = reinterpret_cast<double*>(ws + pl.off_blk);
+  uint16_t* hT = reinterpret_cast<uint16_t*>(ws + pl.off_ht);
+  uint16_t* wT = reinterpret_cast<uint16_t*>(ws + pl.off_wt);
+  uint16_t* dN = reinterpret_cast<uint16_t*>(ws + pl.off_dn);
+  uint16_t* dT = reinterpret_cast<uint16_t*>(ws + pl.off_dt);
+
+  const int tiles_tok = (int)(pl.Npad / kTileN);
+  const int tiles_voc = (int)(pl.ntv);
+  const int tiles_d = (d + kTileN - 1) / kTileN;
+
+  // 1. forward logits -> per-tile softmax partials and target logits
+  {
+    GemmShape g{w_head, d, V, hidden, d, N, d, tiles_voc, tiles_tok};
+    EpiForward e{V, N, pl.Npad, target, part_m, part_l, zt};
+    if (int rc = launch_gemm(g, e, stream)) return rc;
+  }
+  // 2. lse, PPO terms, delta, loss
+  hipLaunchKernelGGL(finalize_kernel, dim3((unsigned)pl.nfin), dim3(kFinThreads), 0, stream, N, V, R, tiles_voc,
+                     pl.Npad, part_m, part_l, zt, target, logp_old, weight, seq_id, advantage, eps_low, eps_high,
+                     loss_scale, lse, delta, logp_new, blk, err_flag);
+  PSPO_HIP_CHECK(hipGetLastError());
+  hipLaunchKernelGGL(reduce_loss_kernel, dim3(1), dim3(kFinThreads), 0, stream, (int)pl.nfin, blk, loss_scale,
+                     loss, stats);
+  PSPO_HIP_CHECK(hipGetLastError());
+  // 3. K-contiguous copies for the gradient products
+  hipLaunchKernelGGL(transpose_pad_kernel, dim3(d / 64, (unsigned)(pl.Npad / 64)), dim3(256), 0, stream, hidden, N,
+                     d, (int64_t)d, hT, pl.Npad);
+  PSPO_HIP_CHECK(hipGetLastError());
+  hipLaunchKernelGGL(transpose_pad_kernel, dim3(d / 64, (unsigned)(pl.Vpad / 64)), dim3(256), 0, stream, w_head, V,
+                     d, (int64_t)d, wT, pl.Vpad);
+  PSPO_HIP_CHECK(hipGetLastError());
+  // 4. backward, one vocabulary chunk at a time
+  for (int64_t v0 = 0; v0 < pl.Vpad; v0 += pl.Vc) {
+    const int64_t vc = (pl.Vpad - v0) < pl.Vc ? (pl.Vpad - v0) : pl.Vc;
+    const int ctiles = (int)(vc / kTileM);
+    {
+      GemmShape g{w_head + v0 * d, d, (int)(V - v0), hidden, d, N, d, ctiles, tiles_tok};
+      EpiDelta e{V, N, (int)v0, target, lse, delta, dT, pl.Npad, dN, pl.Vc};
+      if (int rc = launch_gemm(g, e, stream)) return rc;
+    }
+    {
+      GemmShape g{dT, pl.Npad, (int)vc, hT, pl.Npad, d, (int)pl.Npad, ctiles, tiles_d};
+      EpiDW e{V, d, (int)v0, d_w_head, accumulate};
+      if (int rc = launch_gemm(g, e, stream)) return rc;
+    }
+    {
+      GemmShape g{dN, pl.Vc, (int)pl.Npad, wT + v0, pl.Vpad, d, (int)vc, tiles_tok, tiles_d};
+      EpiDH e{N, d, d_hidden, v0 == 0};
+      if (int rc = launch_gemm(g, e, stream)) return rc;
+    }
+  }
+  return PSPO_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,208 @@
+"""Python binding of libpspo (ctypes): argument marshalling only.
+
+Every step runs in the HIP kernels of libpspo.so; PyTorch only supplies device
+memory (tensors) and the current HIP stream.  If the library is missing the
+calls raise: there is no fallback implementation.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libpspo.so")
+
+PSPO_ACCUMULATE_DW = 1
+DEVERR_TARGET, DEVERR_BAD_XI, DEVERR_CAPACITY, DEVERR_SEQ_ID = 1, 2, 4, 8
+
+_P = ctypes.c_void_p
+_I32, _I64, _U32, _U64, _F32, _SZ = ctypes.c_int32, ctypes.c_int64, ctypes.c_uint32, ctypes.c_uint64, ctypes.c_float, ctypes.c_size_t
+
+_SIGNATURES = {
+    "pspo_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+    "pspo_last_error": (ctypes.c_char_p, []),
+    "pspo_abi_version": (ctypes.c_int, []),
+    "pspo_validate_xi_host": (ctypes.c_int, [_P, _P, _I32]),
+    "pspo_sample_cutoffs": (ctypes.c_int, [_P, _P, _P, _I32, _I32, _U64, _U64, _P, _P, _P]),
+    "pspo_pack_prefixes": (ctypes.c_int, [_P, _P, _P, _P, _I32, _I32, _I32, _P, _P, _P, _I32,
+                                          _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P]),
+    "pspo_loss_workspace_bytes": (_SZ, [_I32, _I32, _I32, _U32]),
+    "pspo_loss_fwd_bwd": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _I32, _I32, _I32, _I32,
+                                         _F32, _F32, _F32, _U32, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
+}
+
+_lib = None
+
+
+class PspoError(RuntimeError):
+    pass
+
+
+def load(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Loads libpspo.so (built by paper_2606_29758_amd.build); raises if it is missing."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(path):
+            raise PspoError(f"{path} not found: build it with `python -m paper_2606_29758_amd.build`")
+        lib = ctypes.CDLL(path)
+        for name, (res, args) in _SIGNATURES.items():
+            fn = getattr(lib, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = lib
+    return _lib
+
+
+def exported_symbols():
+    return list(_SIGNATURES)
+
+
+def _check(rc: int) -> None:
+    if rc != 0:
+        lib = load()
+        raise PspoError(f"{lib.pspo_status_string(rc).decode()}: {lib.pspo_last_error().decode()}")
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _dev(t: torch.Tensor, dtype, name: str) -> torch.Tensor:
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must have dtype {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t
+
+
+def _stream():
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def validate_xi_host(xi, xi_off) -> None:
+    """Host check of survival tables (numpy float64 / int64 arrays)."""
+    import numpy as np
+    xi = np.ascontiguousarray(xi, dtype=np.float64)
+    xi_off = np.ascontiguousarray(xi_off, dtype=np.int64)
+    _check(load().pspo_validate_xi_host(xi.ctypes.data_as(_P), xi_off.ctypes.data_as(_P), len(xi_off) - 1))
+
+
+def sample_cutoffs(xi, xi_off, lengths, P: int, K: int, seed: int, offset: int = 0,
+                   out: Optional[torch.Tensor] = None, err_flag: Optional[torch.Tensor] = None) -> torch.Tensor:
+    _dev(xi, torch.float64, "xi")
+    _dev(xi_off, torch.int64, "xi_off")
+    _dev(lengths, torch.int32, "lengths")
+    if out is None:
+        out = torch.empty(P * K, dtype=torch.int32, device=lengths.device)
+    _dev(out, torch.int32, "cutoffs")
+    if err_flag is not None:
+        _dev(err_flag, torch.int32, "err_flag")
+    _check(load().pspo_sample_cutoffs(_ptr(xi), _ptr(xi_off), _ptr(lengths), P, K,
+                                      seed & (2 ** 64 - 1), offset & (2 ** 64 - 1),
+                                      _ptr(out), _ptr(err_flag), _stream()))
+    return out
+
+
+def pack_prefixes(cutoffs, lengths, xi, xi_off, P: int, K: int, capacity: int,
+                  target_full=None, logp_old_full=None, hidden_full=None,
+                  err_flag: Optional[torch.Tensor] = None) -> dict:
+    """Returns device tensors: cu_seqlens, full_off, src_row, seq_id, weight, [target, logp_old,
+    hidden] (all sized by `capacity`) and n_tokens (int32 [1])."""
+    dev = lengths.device
+    _dev(cutoffs, torch.int32, "cutoffs")
+    _dev(lengths, torch.int32, "lengths")
+    _dev(xi, torch.float64, "xi")
+    _dev(xi_off, torch.int64, "xi_off")
+    R = P * K
+    out = dict(
+        cu_seqlens=torch.empty(R + 1, dtype=torch.int32, device=dev),
+        full_off=torch.empty(R + 1, dtype=torch.int32, device=dev),
+        src_row=torch.empty(capacity, dtype=torch.int32, device=dev),
+        seq_id=torch.empty(capacity, dtype=torch.int32, device=dev),
+        weight=torch.empty(capacity, dtype=torch.float32, device=dev),
+        n_tokens=torch.empty(1, dtype=torch.int32, device=dev),
+    )
+    d = 0
+    if target_full is not None:
+        _dev(target_full, torch.int32, "target_full")
+        out["target"] = torch.empty(capacity, dtype=torch.int32, device=dev)
+    if logp_old_full is not None:
+        _dev(logp_old_full, torch.float32, "logp_old_full")
+        out["logp_old"] = torch.empty(capacity, dtype=torch.float32, device=dev)
+    if hidden_full is not None:
+        _dev(hidden_full, torch.bfloat16, "hidden_full")
+        d = hidden_full.shape[1]
+        out["hidden"] = torch.empty((capacity, d), dtype=torch.bfloat16, device=dev)
+    if err_flag is not None:
+        _dev(err_flag, torch.int32, "err_flag")
+    _check(load().pspo_pack_prefixes(
+        _ptr(cutoffs), _ptr(lengths), _ptr(xi), _ptr(xi_off), P, K, capacity,
+        _ptr(target_full), _ptr(logp_old_full), _ptr(hidden_full), d,
+        _ptr(out["cu_seqlens"]), _ptr(out["full_off"]), _ptr(out["src_row"]), _ptr(out["seq_id"]),
+        _ptr(out["weight"]), _ptr(out.get("target")), _ptr(out.get("logp_old")), _ptr(out.get("hidden")),
+        _ptr(out["n_tokens"]), _ptr(err_flag), _stream()))
+    return out
+
+
+def loss_workspace_bytes(N: int, d: int, V: int, flags: int = 0) -> int:
+    return int(load().pspo_loss_workspace_bytes(N, d, V, flags))
+
+
+def loss_fwd_bwd(hidden, w_head, target, logp_old, weight, seq_id, advantage, N: int,
+                 eps_low: float, eps_high: float, loss_scale: float, flags: int = 0,
+                 d_w_head: Optional[torch.Tensor] = None, d_hidden: Optional[torch.Tensor] = None,
+                 workspace: Optional[torch.Tensor] = None, want_logp: bool = True, want_stats: bool = True,
+                 err_flag: Optional[torch.Tensor] = None) -> dict:
+    """Loss and gradients for the first N rows of the packed per-token tensors.
+
+    hidden: bf16 [>=N, d]; w_head: bf16 [V, d]; target int32, logp_old/weight float32,
+    seq_id int32 (all [>=N]); advantage float32 [R].  Returns loss (float64 [1]),
+    d_hidden (float32 [N, d] view), d_w_head (float32 [V, d]), logp_new, stats.
+    """
+    _dev(w_head, torch.bfloat16, "w_head")
+    V, d = w_head.shape
+    dev = w_head.device
+    _dev(advantage, torch.float32, "advantage")
+    if N > 0:
+        _dev(hidden, torch.bfloat16, "hidden")
+        _dev(target, torch.int32, "target")
+        _dev(logp_old, torch.float32, "logp_old")
+        _dev(weight, torch.float32, "weight")
+        _dev(seq_id, torch.int32, "seq_id")
+        if hidden.shape[1] != d:
+            raise ValueError("hidden and w_head disagree on d")
+        for name, t in (("hidden", hidden), ("target", target), ("logp_old", logp_old),
+                        ("weight", weight), ("seq_id", seq_id)):
+            if t.shape[0] < N:
+                raise ValueError(f"{name} has fewer than N rows")
+    if d_w_head is None:
+        d_w_head = torch.empty((V, d), dtype=torch.float32, device=dev)
+    _dev(d_w_head, torch.float32, "d_w_head")
+    if d_hidden is None:
+        d_hidden = torch.empty((max(N, 1), d), dtype=torch.float32, device=dev)
+    _dev(d_hidden, torch.float32, "d_hidden")
+    loss = torch.empty(1, dtype=torch.float64, device=dev)
+    logp = torch.empty(max(N, 1), dtype=torch.float32, device=dev) if want_logp else None
+    stats = torch.empty(4, dtype=torch.float64, device=dev) if want_stats else None
+    need = loss_workspace_bytes(N, d, V, flags)
+    if workspace is None:
+        workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=dev)
+    _dev(workspace, torch.uint8, "workspace")
+    if err_flag is not None:
+        _dev(err_flag, torch.int32, "err_flag")
+    _check(load().pspo_loss_fwd_bwd(
+        _ptr(hidden) if N > 0 else None, _ptr(w_head), _ptr(target) if N > 0 else None,
+        _ptr(logp_old) if N > 0 else None, _ptr(weight) if N > 0 else None,
+        _ptr(seq_id) if N > 0 else None, _ptr(advantage), N, d, V, advantage.shape[0],
+        float(eps_low), float(eps_high), float(loss_scale), flags,
+        _ptr(loss), _ptr(d_hidden), _ptr(d_w_head), _ptr(logp), _ptr(stats), _ptr(err_flag),
+        _ptr(workspace), workspace.numel(), _stream()))
+    return dict(loss=loss, d_hidden=d_hidden[:N], d_w_head=d_w_head,
+                logp_new=None if logp is None else logp[:N], stats=stats, workspace=workspace)

@@ -124,11 +124,34 @@ class Workload:
         return int(self.lengths.sum())
 
     def fingerprint(self) -> str:
-        """Digest of the small arrays; identifies the data a stored file belongs to."""
+        """Digest identifying the token data (not the cutoff tables) a stored file belongs to."""
         h = hashlib.sha256()
-        for a in (self.lengths, self.target_full, self.lp_noise, self.xi):
+        h.update(np.array([self.cfg.d, self.cfg.V, self.cfg.data_seed], dtype=np.int64).tobytes())
+        for a in (self.lengths, self.target_full, self.lp_noise):
             h.update(np.ascontiguousarray(a).tobytes())
         return h.hexdigest()[:16]
+
+
+def load_stored_logp_old(wl: "Workload", directory: str) -> np.ndarray:
+    """Old-policy log-probs stored for this workload's token data (float32 [sum T_r]).
+
+    Looks for ``logp_old_*.json`` in `directory` whose fingerprint matches, and raises
+    if none does (the stored file was made from different data).
+    """
+    import glob
+    import json
+    import os
+
+    fp = wl.fingerprint()
+    for meta_path in sorted(glob.glob(os.path.join(directory, "logp_old_*.json"))):
+        with open(meta_path) as f:
+            meta = json.load(f)
+        if meta.get("fingerprint") == fp:
+            arr = np.load(meta_path[:-5] + ".npy", allow_pickle=False)
+            if arr.shape != (wl.total_tokens,) or arr.dtype != np.float32:
+                raise ValueError(f"{meta_path}: stored array does not match the workload's shape")
+            return arr
+    raise FileNotFoundError(f"no stored old log-probs for workload {wl.cfg.name} (fingerprint {fp}) in {directory}")
 
 
 def round_to_bf16_bits(x: np.ndarray) -> np.ndarray:

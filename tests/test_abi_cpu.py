@@ -1,0 +1,155 @@
+"""The C ABI without a GPU: the library loads, exports every symbol the header
+declares, and rejects bad arguments with the documented status before any
+device work (these paths never reach the HIP runtime)."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2606_29758_amd import pspo
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+OK, INVALID, BAD_XI, WORKSPACE, UNSUPPORTED = 0, 1, 2, 3, 4
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(pspo.LIB_PATH):
+        pytest.fail("libpspo.so is not built (run __graft_entry__.build())")
+    return pspo.load()
+
+
+def _declared():
+    with open(os.path.join(ROOT, "include", "pspo.h")) as f:
+        text = f.read()
+    return sorted(set(re.findall(r"\b(pspo_[a-z_]+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol(lib):
+    names = _declared()
+    assert len(names) == 8
+    for name in names:
+        assert hasattr(lib, name), name
+    assert sorted(pspo.exported_symbols()) == names
+
+
+def test_version_and_status_strings(lib):
+    assert lib.pspo_abi_version() == 1
+    assert lib.pspo_status_string(0) == b"PSPO_OK"
+    assert lib.pspo_status_string(3) == b"PSPO_ERR_WORKSPACE"
+    assert lib.pspo_status_string(99) == b"PSPO_ERR_UNKNOWN"
+
+
+def _vx(xi, off):
+    xi = np.ascontiguousarray(xi, dtype=np.float64)
+    off = np.ascontiguousarray(off, dtype=np.int64)
+    return pspo.load().pspo_validate_xi_host(xi.ctypes.data_as(ctypes.c_void_p),
+                                             off.ctypes.data_as(ctypes.c_void_p), len(off) - 1)
+
+
+def test_validate_xi_host(lib):
+    assert _vx([1.0, 0.5, 0.5, 0.1, 1.0, 2 ** -40], [0, 4, 6]) == OK
+    assert _vx([1.0, 0.5, 0.6], [0, 3]) == BAD_XI
+    assert b"increases at t = 3" in lib.pspo_last_error()
+    assert _vx([1.0, 0.0], [0, 2]) == BAD_XI
+    assert _vx([1.25], [0, 1]) == BAD_XI
+    assert _vx([np.nan], [0, 1]) == BAD_XI
+    assert _vx([1.0], [1, 1]) == INVALID
+    assert _vx([1.0, 1.0], [0, 2, 1]) == INVALID
+    assert _vx([], [0]) == OK
+    with pytest.raises(pspo.PspoError, match="BAD_XI"):
+        pspo.validate_xi_host([0.5, 0.7], [0, 2])
+
+
+FAKE = ctypes.c_void_p(1 << 20)   # aligned, never dereferenced on these paths
+
+
+def _sample(lib, **kw):
+    a = dict(xi=FAKE, xi_off=FAKE, lengths=FAKE, P=1, K=1, seed=0, offset=0, cutoffs=FAKE, err=None, stream=None)
+    a.update(kw)
+    return lib.pspo_sample_cutoffs(a["xi"], a["xi_off"], a["lengths"], a["P"], a["K"], a["seed"], a["offset"],
+                                   a["cutoffs"], a["err"], a["stream"])
+
+
+def test_sample_cutoffs_argument_errors(lib):
+    assert _sample(lib, P=-1) == INVALID
+    assert _sample(lib, P=0) == OK          # nothing to do: no device work at all
+    assert _sample(lib, K=0) == OK
+    assert _sample(lib, xi=None) == INVALID
+    assert _sample(lib, cutoffs=None) == INVALID
+    assert _sample(lib, lengths=ctypes.c_void_p((1 << 20) + 2)) == INVALID
+    assert _sample(lib, P=1 << 16, K=1 << 16) == INVALID
+
+
+def _pack(lib, **kw):
+    a = dict(cut=FAKE, len=FAKE, xi=FAKE, xio=FAKE, P=2, K=2, cap=16, tf=FAKE, lf=FAKE, hf=FAKE, d=64,
+             cu=FAKE, fo=FAKE, src=FAKE, seq=FAKE, w=FAKE, t=FAKE, l=FAKE, h=FAKE, n=FAKE, err=None)
+    a.update(kw)
+    return lib.pspo_pack_prefixes(a["cut"], a["len"], a["xi"], a["xio"], a["P"], a["K"], a["cap"], a["tf"],
+                                  a["lf"], a["hf"], a["d"], a["cu"], a["fo"], a["src"], a["seq"], a["w"], a["t"],
+                                  a["l"], a["h"], a["n"], a["err"], None)
+
+
+def test_pack_prefixes_argument_errors(lib):
+    assert _pack(lib, cap=-1) == INVALID
+    assert _pack(lib, t=None) == INVALID            # target_full given without target
+    assert _pack(lib, lf=None) == INVALID
+    assert _pack(lib, hf=None) == INVALID
+    assert _pack(lib, d=12) == UNSUPPORTED           # 16-byte row gather needs d % 8 == 0
+    assert _pack(lib, d=0) == UNSUPPORTED
+    assert _pack(lib, h=ctypes.c_void_p((1 << 20) + 8)) == INVALID
+    assert _pack(lib, cu=None) == INVALID
+    assert _pack(lib, src=None) == INVALID
+    assert _pack(lib, P=300, K=300) == UNSUPPORTED   # more than 65535 completions
+
+
+def _loss(lib, **kw):
+    N, d, V = kw.get("N", 100), kw.get("d", 128), kw.get("V", 1000)
+    ws_bytes = lib.pspo_loss_workspace_bytes(max(N, 0), d, max(V, 1), 0)
+    a = dict(h=FAKE, w=FAKE, t=FAKE, lo=FAKE, c=FAKE, s=FAKE, adv=FAKE, N=N, d=d, V=V, R=4, el=0.1, eh=0.1,
+             scale=0.25, flags=0, loss=FAKE, dh=FAKE, dw=FAKE, lp=None, st=None, err=None, ws=FAKE, wsb=ws_bytes)
+    a.update(kw)
+    return lib.pspo_loss_fwd_bwd(a["h"], a["w"], a["t"], a["lo"], a["c"], a["s"], a["adv"], a["N"], a["d"], a["V"],
+                                 a["R"], a["el"], a["eh"], a["scale"], a["flags"], a["loss"], a["dh"], a["dw"],
+                                 a["lp"], a["st"], a["err"], a["ws"], a["wsb"], None)
+
+
+def test_loss_argument_errors(lib):
+    assert _loss(lib, N=-1) == INVALID
+    assert _loss(lib, d=0) == INVALID
+    assert _loss(lib, V=0) == INVALID
+    assert _loss(lib, d=96) == UNSUPPORTED
+    assert _loss(lib, R=0) == INVALID
+    assert _loss(lib, flags=2) == INVALID
+    assert _loss(lib, el=1.0) == INVALID
+    assert _loss(lib, eh=-0.1) == INVALID
+    assert _loss(lib, el=float("nan")) == INVALID
+    assert _loss(lib, scale=float("inf")) == INVALID
+    assert _loss(lib, loss=None) == INVALID
+    assert _loss(lib, dw=None) == INVALID
+    assert _loss(lib, h=None) == INVALID
+    assert _loss(lib, dh=None) == INVALID
+    assert _loss(lib, h=ctypes.c_void_p((1 << 20) + 4)) == INVALID
+    assert _loss(lib, ws=ctypes.c_void_p((1 << 20) + 16)) == INVALID
+    assert _loss(lib, ws=None) == INVALID
+    assert _loss(lib, wsb=1024) == WORKSPACE
+    assert b"workspace too small" in lib.pspo_last_error()
+
+
+def test_workspace_bytes(lib):
+    assert lib.pspo_loss_workspace_bytes(-1, 128, 100, 0) == 0
+    assert lib.pspo_loss_workspace_bytes(10, 0, 100, 0) == 0
+    a = lib.pspo_loss_workspace_bytes(1000, 3584, 152064, 0)
+    b = lib.pspo_loss_workspace_bytes(2000, 3584, 152064, 0)
+    assert 0 < a < b
+    # the dominant terms: bf16 logit-gradient chunks in both layouts (2 x Npad x 16384 x 2 B)
+    assert b > 2 * 2048 * 16384 * 2
+
+
+def test_binding_refuses_host_tensors():
+    import torch
+    with pytest.raises(ValueError, match="device tensor"):
+        pspo.sample_cutoffs(torch.ones(3, dtype=torch.float64), torch.zeros(2, dtype=torch.int64),
+                            torch.ones(1, dtype=torch.int32), 1, 1, 0)

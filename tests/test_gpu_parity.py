@@ -1,0 +1,267 @@
+"""GPU parity: the HIP path (through the C ABI) against the float64 oracle.
+
+Bar: bit-exact cutoffs, packing and weights; loss relative error <= 1e-4;
+d_hidden and d_w_head relative L2 error <= 1e-2 (bf16 inputs, fp32
+accumulation, bf16 logit gradients); per-token log-probs within 2e-4.
+Small workloads are compared element by element; the full-size workloads
+(in the launch configuration the benchmark times) are compared on sampled
+tokens the oracle computes one by one, plus identities that hold at any size.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import ppo_head as ohead
+from paper_2606_29758_amd import pipeline, pspo, synth
+
+from parity_util import (GRAD_REL_L2, LOGP_ATOL, LOSS_RTOL, ambiguous_clip, f32, logp_old_for,
+                         oracle_loss, oracle_sample_pack, rel_l2)
+
+pytestmark = pytest.mark.gpu
+
+MINI = {
+    "tiny": synth.CONFIGS["tiny"],
+    "tiny_full": synth.custom("tiny_full", "tiny", full_trajectory=True),
+    # the 7B and 1.5B vocabulary and width with a few short completions: several
+    # tiles in every dimension and ragged tails (V = 151936 is not a multiple of 256)
+    "mini7b": synth.custom("mini7b", "qwen7b", P=2, K=2, length_law=("uniform", 150, 420), data_seed=31),
+    "mini1p5b": synth.custom("mini1p5b", "qwen1.5b", P=2, K=3, length_law=("uniform", 60, 300), data_seed=21),
+}
+_CACHE = {}
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    assert torch.cuda.is_available(), "GPU tests need an MI355X"
+    pspo.load()
+
+
+def _workload(name):
+    if name not in _CACHE:
+        cfg = MINI.get(name) or synth.CONFIGS[name]
+        wl = synth.make_workload(cfg)
+        _CACHE.clear()   # keep at most one (possibly multi-GB) workload alive
+        _CACHE[name] = (wl, logp_old_for(wl))
+    return _CACHE[name]
+
+
+def _to_np(t):
+    return t.detach().cpu().numpy()
+
+
+def _check_pack(out, H, pk):
+    N = pk["n_tokens"]
+    assert np.array_equal(_to_np(out["cutoffs"]), H)
+    got = out["pack"]
+    assert int(_to_np(got["n_tokens"])[0]) == N
+    for key in ("cu_seqlens", "full_off"):
+        assert np.array_equal(_to_np(got[key]), pk[key]), key
+    for key in ("src_row", "seq_id", "weight", "target", "logp_old"):
+        assert np.array_equal(_to_np(got[key])[:N], pk[key]), key
+
+
+# ---------------------------------------------------------------- sampler + packer
+
+
+@pytest.mark.parametrize("name", ["tiny", "qwen1.5b", "qwen7b", "qwen7b_long", "qwen7b_full"])
+@pytest.mark.parametrize("seed,offset", [(0, 0), (7, 3), (2 ** 40 + 5, 2 ** 33 + 1)])
+def test_sample_and_pack_bitwise(name, seed, offset):
+    wl = synth.make_workload(name, with_matrices=False)
+    cfg = wl.cfg
+    lp = wl.lp_noise.astype(np.float32)   # any float32 per-token array exercises the gather
+    dev = "cuda"
+    t = lambda a, dt: torch.from_numpy(np.ascontiguousarray(a)).to(dev, dt)
+    xi, xi_off, lengths = t(wl.xi, torch.float64), t(wl.xi_off, torch.int64), t(wl.lengths, torch.int32)
+    err = torch.zeros(1, dtype=torch.int32, device=dev)
+    cut = pspo.sample_cutoffs(xi, xi_off, lengths, cfg.P, cfg.K, seed, offset, err_flag=err)
+    got = pspo.pack_prefixes(cut, lengths, xi, xi_off, cfg.P, cfg.K, wl.total_tokens,
+                             target_full=t(wl.target_full, torch.int32), logp_old_full=t(lp, torch.float32),
+                             err_flag=err)
+    H, pk = oracle_sample_pack(wl, lp, seed, offset)
+    _check_pack(dict(cutoffs=cut, pack=got), H, pk)
+    assert int(err.item()) == 0
+    if cfg.full_trajectory:
+        assert np.array_equal(H, wl.lengths) and np.all(pk["weight"] == 1.0)
+
+
+def test_hidden_gather_bitwise():
+    wl, lp = _workload("mini7b")
+    dw = pipeline.upload(wl, lp)
+    step = pipeline.Step(dw)
+    pk_gpu = step.sample_and_pack(seed=5)
+    H, pk = oracle_sample_pack(wl, lp, 5)
+    N = pk["n_tokens"]
+    got = _to_np(pk_gpu["hidden"].view(torch.int16))[:N].view(np.uint16)
+    assert np.array_equal(got, wl.hidden_bits[pk["src_row"]])
+
+
+# ---------------------------------------------------------------- loss fwd + bwd
+
+
+def _compare_loss(out, ref):
+    loss = float(out["loss"].item())
+    assert abs(loss - ref["loss"]) <= LOSS_RTOL * abs(ref["loss"]), (loss, ref["loss"])
+    lp = _to_np(out["logp_new"]).astype(np.float64)
+    assert np.max(np.abs(lp - ref["logp_new"])) <= LOGP_ATOL
+    assert _to_np(out["stats"])[0] == pytest.approx(ref["abs_mass"], rel=LOSS_RTOL)
+    e_h = rel_l2(_to_np(out["d_hidden"]), ref["d_hidden"])
+    e_w = rel_l2(_to_np(out["d_w_head"]), ref["d_w"])
+    print(f"loss rel {abs(loss - ref['loss']) / abs(ref['loss']):.2e}  dH relL2 {e_h:.2e}  dW relL2 {e_w:.2e}")
+    assert e_h <= GRAD_REL_L2 and e_w <= GRAD_REL_L2
+
+
+@pytest.mark.parametrize("name,seed", [("tiny", 0), ("tiny", 1), ("tiny", 123456789), ("tiny_full", 0),
+                                       ("mini1p5b", 0), ("mini7b", 3)])
+def test_loss_parity(name, seed):
+    wl, lp = _workload(name)
+    cfg = wl.cfg
+    dw = pipeline.upload(wl, lp)
+    out = pipeline.Step(dw)(seed=seed)
+    torch.cuda.synchronize()
+    H, pk = oracle_sample_pack(wl, lp, seed)
+    _check_pack(out, H, pk)
+    ref = oracle_loss(wl, pk)
+    assert not ambiguous_clip(ref, cfg.eps_low, cfg.eps_high).any()
+    _compare_loss(out, ref)
+    # the clip mask and degenerate groups agree exactly
+    A = wl.advantage[pk["seq_id"]]
+    st = _to_np(out["stats"])
+    assert int(st[1]) == int(np.sum((A != 0) & (ref["mu"] == 0)))
+    assert int(st[2]) == int(np.sum(A == 0))
+    assert st[3] == float(pk["weight"].max())
+    assert int(out["pack"]["n_tokens"].item()) == pk["n_tokens"]
+
+
+def test_deterministic():
+    wl, lp = _workload("tiny")
+    step = pipeline.Step(pipeline.upload(wl, lp))
+    a = step(seed=1)
+    la, dha, dwa = a["loss"].clone(), a["d_hidden"].clone(), a["d_w_head"].clone()
+    b = step(seed=1)
+    assert torch.equal(la, b["loss"]) and torch.equal(dha, b["d_hidden"]) and torch.equal(dwa, b["d_w_head"])
+
+
+def test_accumulate_flag():
+    wl, lp = _workload("tiny")
+    step = pipeline.Step(pipeline.upload(wl, lp))
+    one = step(seed=2)["d_w_head"].clone()
+    step.d_w.zero_()
+    pk = step.sample_and_pack(seed=2)
+    N = int(pk["n_tokens"].item())
+    step.loss(pk, N, flags=pspo.PSPO_ACCUMULATE_DW)
+    step.loss(pk, N, flags=pspo.PSPO_ACCUMULATE_DW)
+    assert torch.allclose(step.d_w, 2 * one, rtol=1e-6, atol=0)
+
+
+def test_empty_prefixes():
+    """Every cutoff 0 (xi_1 tiny): N = 0, loss 0, d_w_head zeroed."""
+    wl, lp = _workload("tiny")
+    wl0 = synth.Workload(**{**wl.__dict__, "xi": np.full_like(wl.xi, 2.0 ** -40)})
+    step = pipeline.Step(pipeline.upload(wl0, lp))
+    step.d_w.fill_(7.0)
+    out = step(seed=0)
+    assert out["N"] == 0
+    assert float(out["loss"].item()) == 0.0
+    assert not torch.any(out["d_w_head"])
+
+
+def test_zero_advantage():
+    wl, lp = _workload("tiny")
+    wl0 = synth.Workload(**{**wl.__dict__, "advantage": np.zeros_like(wl.advantage)})
+    out = pipeline.Step(pipeline.upload(wl0, lp))(seed=0)
+    assert float(out["loss"].item()) == 0.0
+    assert not torch.any(out["d_hidden"]) and not torch.any(out["d_w_head"])
+    assert int(out["stats"][2].item()) == out["N"]
+
+
+def test_device_error_flags():
+    wl, lp = _workload("tiny")
+    dw = pipeline.upload(wl, lp)
+    step = pipeline.Step(dw)
+    pk = step.sample_and_pack(seed=0)
+    N = int(pk["n_tokens"].item())
+    cfg = wl.cfg
+    # a target id outside [0, V): flagged, that token contributes nothing
+    tgt = pk["target"].clone()
+    tgt[3] = cfg.V
+    err = torch.zeros(1, dtype=torch.int32, device="cuda")
+    pspo.loss_fwd_bwd(pk["hidden"], dw.w_head, tgt, pk["logp_old"], pk["weight"], pk["seq_id"], dw.advantage, N,
+                      cfg.eps_low, cfg.eps_high, cfg.loss_scale, err_flag=err)
+    assert int(err.item()) & pspo.DEVERR_TARGET
+    # a seq_id outside [0, R)
+    seq = pk["seq_id"].clone()
+    seq[0] = cfg.R
+    err.zero_()
+    pspo.loss_fwd_bwd(pk["hidden"], dw.w_head, pk["target"], pk["logp_old"], pk["weight"], seq, dw.advantage, N,
+                      cfg.eps_low, cfg.eps_high, cfg.loss_scale, err_flag=err)
+    assert int(err.item()) & pspo.DEVERR_SEQ_ID
+    # an increasing xi table
+    bad = dw.xi.clone()
+    bad[5] = 1.0
+    bad[4] = 0.5
+    err.zero_()
+    pspo.sample_cutoffs(bad, dw.xi_off, dw.lengths, cfg.P, cfg.K, 0, 0, err_flag=err)
+    assert int(err.item()) & pspo.DEVERR_BAD_XI
+    # capacity below the kept-token count: flagged, n_tokens clipped, nothing written past it
+    err.zero_()
+    cut = pspo.sample_cutoffs(dw.xi, dw.xi_off, dw.lengths, cfg.P, cfg.K, 0, 0)
+    small = pspo.pack_prefixes(cut, dw.lengths, dw.xi, dw.xi_off, cfg.P, cfg.K, 10,
+                               target_full=dw.target_full, logp_old_full=dw.logp_old_full,
+                               hidden_full=dw.hidden_full, err_flag=err)
+    assert int(err.item()) & pspo.DEVERR_CAPACITY
+    assert int(small["n_tokens"].item()) == 10
+
+
+# ---------------------------------------------------------------- full size, sampled
+
+
+@pytest.mark.parametrize("name", ["qwen7b", "qwen7b_full", "qwen1.5b", "qwen7b_long"])
+def test_full_size_sampled(name):
+    wl, lp = _workload(name)
+    cfg = wl.cfg
+    print(f"[{name}] workload ready: {wl.total_tokens} tokens", flush=True)
+    dw = pipeline.upload(wl, lp)
+    out = pipeline.Step(dw)(seed=0)
+    torch.cuda.synchronize()
+    print(f"[{name}] GPU pass done, N = {out['N']}", flush=True)
+    H, pk = oracle_sample_pack(wl, lp, 0)
+    _check_pack(out, H, pk)
+    N = pk["n_tokens"]
+
+    rng = np.random.default_rng(17)
+    idx = np.unique(np.concatenate([[0, N - 1, N - 2], rng.choice(N, 45, replace=False)]))
+    sub = {k: pk[k][idx] for k in ("src_row", "seq_id", "weight", "target", "logp_old")}
+    ref = oracle_loss(wl, sub)
+    lp_gpu = _to_np(out["logp_new"])[idx].astype(np.float64)
+    assert np.max(np.abs(lp_gpu - ref["logp_new"])) <= LOGP_ATOL
+    amb = ambiguous_clip(ref, cfg.eps_low, cfg.eps_high)
+    dh = _to_np(out["d_hidden"][torch.from_numpy(idx).cuda()]).astype(np.float64)
+    for k in range(len(idx)):
+        if amb[k]:
+            continue
+        if ref["delta"][k] == 0:
+            assert not dh[k].any()
+        else:
+            assert rel_l2(dh[k], ref["d_hidden"][k]) <= GRAD_REL_L2, (k, idx[k])
+    print(f"[{name}] sampled rows match", flush=True)
+
+    # the loss is the float64 reduction of the per-token surrogate terms
+    lp_all = _to_np(out["logp_new"]).astype(np.float64)
+    rho = np.exp(lp_all - pk["logp_old"].astype(np.float64))
+    A = wl.advantage[pk["seq_id"]].astype(np.float64)
+    el, eh = f32(cfg.eps_low), f32(cfg.eps_high)
+    s = np.minimum(rho * A, np.clip(rho, 1 - el, 1 + eh) * A)
+    L_host = -f32(cfg.loss_scale) * np.sum(pk["weight"].astype(np.float64) * s)
+    assert float(out["loss"].item()) == pytest.approx(L_host, rel=LOSS_RTOL)
+
+    # identities of the gradient at any size: softmax rows sum to one, and
+    # <dW, W> = <dH, H> = sum_{i,v} G_iv z_iv
+    dW = out["d_w_head"].double()
+    col = dW.sum(dim=0)
+    assert float(col.norm() / dW.norm()) <= GRAD_REL_L2
+    Wd = dw.w_head.double()
+    Hd = out["pack"]["hidden"][:N].double()
+    a = float((dW * Wd).sum())
+    b = float((out["d_hidden"].double() * Hd).sum())
+    assert abs(a - b) <= GRAD_REL_L2 * max(abs(a), abs(b))
+    print(f"[{name}] identities hold", flush=True)
