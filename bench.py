@@ -1,0 +1,197 @@
+"""Benchmark of the PS-PPO hot path on one MI355X: prefix tokens/s of one update pass.
+
+A step is one pass of the whole hot path over one batch of synthetic rollouts
+already resident in HBM: Philox cutoff sampling, prefix packing (with the
+hidden-row gather), the 4-byte read of the packed token count, and the fused
+LM-head + prefix-weighted PPO loss forward and backward (dHidden, dW).
+
+Workload: the 7B-shaped batch (Qwen2.5-Math-7B head dims d = 3584,
+V = 152064; 8 prompts x 8 rollouts; lengths lognormal around 2048, clipped
+to [128, 8192]; per-prompt discrete Beta(a, b) cutoff laws, a, b ~ U[1, 4];
+old log-probs = new + N(0, 0.1^2)).
+
+Prints one JSON line.  `roofline` covers the loss call (the forward, logit-
+gradient, dW and dH matrix-core kernels it launches), timed with HIP events
+on the stream it runs on: achieved = 6 N V d algorithmic flops / mean call
+duration.  `cpu_baseline` times the float64 CPU oracle on a bounded sample of
+the same step (all cutoffs and packing, then the loss of the first
+--cpu-tokens packed tokens).
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2516.6     # MI355X dense bf16 MFMA (256 CUs x 2.4 GHz x 4096 flop/clk)
+GOLDEN = os.path.join(ROOT, "tests", "golden")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "loss_fwd_bwd_qwen7b_traffic.json")
+
+
+def source_hash():
+    """Digest of the HIP/C++ sources of libpspo (identifies the kernels counters were taken on)."""
+    import hashlib
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2606_29758_amd", "csrc")
+    for name in sorted(os.listdir(csrc)):
+        with open(os.path.join(csrc, name), "rb") as f:
+            h.update(name.encode() + f.read())
+    return h.hexdigest()[:16]
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="qwen7b")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--cpu-tokens", type=int, default=1024)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a device copy of known size (HBM counter calibration) and exit")
+    return ap.parse_args()
+
+
+def copy_calibration():
+    import torch
+    n = 1 << 30   # 1 GiB read + 1 GiB written per copy
+    a = torch.ones(n, dtype=torch.uint8, device="cuda")
+    b = torch.empty_like(a)
+    for _ in range(3):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes": n, "launches": 3}), flush=True)
+
+
+def cpu_baseline(wl, logp_old, ntok, seed):
+    """The oracle as it stands: sampling + packing of the whole batch, then the loss and
+    gradients of the first `ntok` packed tokens.  Returns the object for the JSON line."""
+    from threadpoolctl import threadpool_info
+    from oracle import cutoffs as ocut
+    from oracle import ppo_head as ohead
+
+    cfg = wl.cfg
+    t0 = time.perf_counter()
+    H = ocut.sample_cutoffs(wl.xi, wl.xi_off, wl.lengths, cfg.P, cfg.K, seed, 0)
+    pk = ocut.pack_prefixes(H, wl.lengths, wl.xi, wl.xi_off, cfg.P, cfg.K, wl.target_full, logp_old)
+    sel = slice(0, min(ntok, pk["n_tokens"]))
+    src = pk["src_row"][sel]
+    ohead.loss_fwd_bwd(wl.hidden_bits[src], wl.w_bits, pk["target"][sel], pk["logp_old"][sel],
+                       pk["weight"][sel], pk["seq_id"][sel], wl.advantage, float(np.float32(cfg.eps_low)),
+                       float(np.float32(cfg.eps_high)), float(np.float32(cfg.loss_scale)))
+    dt = time.perf_counter() - t0
+    n = sel.stop
+    threads = max([p.get("num_threads", 1) for p in threadpool_info() if p.get("user_api") == "blas"] or [1])
+    return {"value": n / dt, "unit": "prefix tokens/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"cutoffs and packing of all {cfg.R} rollouts, then loss + gradients of the first "
+                      f"{n} packed tokens (float64 numpy, {dt:.1f} s)"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1",
+                          "n_gpus_requested": args.gpus}), flush=True)
+        sys.exit(2)
+    if args.copy_calibration:
+        copy_calibration()
+        return
+
+    import torch
+    from paper_2606_29758_amd import pipeline, synth
+
+    wl = synth.make_workload(args.workload)
+    cfg = wl.cfg
+    logp_old = synth.load_stored_logp_old(wl, GOLDEN)
+    dw = pipeline.upload(wl, logp_old)
+    step = pipeline.Step(dw)
+    torch.cuda.synchronize()
+
+    stream = torch.cuda.current_stream()
+    ev = lambda: torch.cuda.Event(enable_timing=True)
+    for _ in range(args.warmup):
+        step(args.seed)
+    torch.cuda.synchronize()
+
+    loss_ms = []
+    starts, ends = [], []
+    t_start, t_end = ev(), ev()
+    torch.cuda.synchronize()
+    t_start.record(stream)
+    N = 0
+    for _ in range(args.steps):
+        pk = step.sample_and_pack(args.seed)
+        N = int(pk["n_tokens"].item())
+        s, e = ev(), ev()
+        s.record(stream)
+        out = step.loss(pk, N)
+        e.record(stream)
+        starts.append(s)
+        ends.append(e)
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    ms_step = t_start.elapsed_time(t_end) / args.steps
+    loss_ms = [s.elapsed_time(e) for s, e in zip(starts, ends)]
+    loss_avg = float(np.mean(loss_ms))
+    assert int(step.err.item()) == 0, "device error flag raised"
+
+    flops = 6.0 * N * cfg.V * cfg.d
+    achieved = flops / (loss_avg * 1e-3) / 1e12
+    # HBM bytes per call from the committed counter runs, only while the kernels
+    # are still the ones those counters were taken on
+    traffic = None
+    if os.path.exists(TRAFFIC_FILE):
+        with open(TRAFFIC_FILE) as f:
+            t = json.load(f)
+        if t.get("N") == N and t.get("workload") == args.workload and t.get("source_hash") == source_hash():
+            traffic = t.get("bytes_per_call")
+
+    result = {
+        "metric": "prefix tokens/sec for fused LM-head PPO loss fwd+bwd; % of bf16 MFMA peak",
+        "value": N / (ms_step * 1e-3),
+        "unit": "prefix tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": f"{args.workload}: {cfg.P} prompts x {cfg.K} rollouts, d={cfg.d}, V={cfg.V}, "
+                        f"lengths {cfg.length_law}, cutoff Beta law {cfg.beta_law}"
+                        f"{' (pinned to full length)' if cfg.full_trajectory else ''}, "
+                        f"logp_old noise sigma {cfg.sigma_lp}",
+            "prefix_tokens": N,
+            "total_tokens": int(wl.total_tokens),
+            "kept_fraction": N / wl.total_tokens,
+            "global_batch": cfg.R,
+            "parallelism": "single GPU",
+        },
+        "loss_call_ms": loss_avg,
+        "pct_bf16_peak": 100.0 * achieved / PEAK_BF16_TFLOPS,
+        "roofline": {
+            "bound": "mfma",
+            "kernel": "pspo_loss_fwd_bwd (forward, logit-gradient, dW and dH bf16 MFMA kernels)",
+            "achieved": achieved,
+            "peak": PEAK_BF16_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": achieved / PEAK_BF16_TFLOPS,
+            "traffic": traffic,
+        },
+    }
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(wl, logp_old, args.cpu_tokens, args.seed)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()
