@@ -119,7 +119,8 @@ __device__ __forceinline__ void stage_barrier() {
   __builtin_amdgcn_sched_barrier(0);
 }
 
-// Epilogue interface: `Epi::apply(acc, tm, tn, wm, wn, lane, smem)`; smem is the
+// Epilogue interface: `Epi::apply(acc, tm, tn, wm, wn, lane, smem)` (acc may be
+// overwritten); smem is the
 // (no longer needed) LDS ring, 160 KB, free for reductions: every load into
 // it has landed and all waves have passed a barrier before the call.
 template <class Epi>

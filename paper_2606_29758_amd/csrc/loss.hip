@@ -14,8 +14,8 @@
 //      vocabulary rows and picks up the target logit;
 //   2. finalize: merge the partials into lse, then l, rho, the clip mask, delta
 //      and a deterministic float64 loss reduction;
-//   3. transposed bf16 copies H^T [d x Npad] and W^T [d x Vpad] (K-contiguous
-//      operands for the two gradient products);
+//   3. transposed bf16 copies H^T [d x Npad] and, per vocabulary chunk,
+//      W[chunk]^T [d x Vc] (K-contiguous operands of the two gradient products);
 //   4. per vocabulary chunk of Vc rows: recompute the chunk's logit tiles and
 //      write the bf16 logit gradient Delta = delta (e_o - exp(z - lse)) in both
 //      layouts ([Npad x Vc] and [Vc x Npad]); then dW[chunk] = Delta^T H and
@@ -99,6 +99,8 @@ struct EpiForward {
 // Backward logit gradient for one vocabulary chunk: rows = vocabulary rows
 // v0 + vl (A = W[v0:]), columns = tokens.  Writes bf16 Delta to
 // dT[vl][t] (ldT = Npad) and dN[t][vl] (ldN = Vc); zero outside t < N, v < V.
+// The 256 x 256 bf16 tile goes through LDS once per layout so both global
+// layouts are written as whole 512-byte rows (16 bytes per lane).
 struct EpiDelta {
   int V, N, v0;
   const int32_t* target;
@@ -109,7 +111,23 @@ struct EpiDelta {
   uint16_t* dN;
   int64_t ldN;
 
-  __device__ __forceinline__ void apply(const AccTile& acc, int tm, int tn, int wm, int wn, int lane, float*) const {
+  // LDS tile: 256 rows x 512 bytes; 16-byte chunk c of row r stored at chunk c ^ (r & 31).
+  __device__ static __forceinline__ int tile_off(int row, int col) {
+    return row * 512 + ((((col >> 3) ^ (row & 31)) << 4) | ((col & 7) << 1));
+  }
+
+  // Copies the LDS tile (256 rows of 256 bf16) to rows of `dst` with stride `ld`.
+  __device__ static __forceinline__ void copy_out(const unsigned char* tile, uint16_t* dst, int64_t ld) {
+    for (int c = threadIdx.x; c < 256 * 32; c += kGemmThreads) {
+      const int row = c >> 5, chunk = c & 31;
+      const u32x4 v = *reinterpret_cast<const u32x4*>(tile + row * 512 + ((chunk ^ (row & 31)) << 4));
+      *reinterpret_cast<u32x4*>(dst + (int64_t)row * ld + chunk * 8) = v;
+    }
+  }
+
+  __device__ __forceinline__ void apply(AccTile& acc, int tm, int tn, int wm, int wn, int lane, float* smem) const {
+    unsigned char* tile = reinterpret_cast<unsigned char*>(smem);
+    // Delta in place of the logits
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int t = tn * kTileN + acc_col(wn, j, lane);
@@ -120,24 +138,45 @@ struct EpiDelta {
 #pragma unroll
       for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const int vl0 = tm * kTileM + acc_row(wm, i, g * 4, lane);
-          uint32_t b[4];
-#pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            const int vl = vl0 + q;
-            const int v = v0 + vl;
-            float dv = 0.f;
-            if (dl != 0.f && v < V) dv = dl * ((v == tgt ? 1.f : 0.f) - __expf(acc.c[i][j][g * 4 + q] - ls));
-            b[q] = f32_to_bf16_bits(dv);
-            dT[(int64_t)vl * ldT + t] = (uint16_t)b[q];
-          }
-          u32x2 packed;
-          packed.x = b[0] | (b[1] << 16);
-          packed.y = b[2] | (b[3] << 16);
-          *reinterpret_cast<u32x2*>(dN + (int64_t)t * ldN + vl0) = packed;
+        for (int r = 0; r < 16; ++r) {
+          const int v = v0 + tm * kTileM + acc_row(wm, i, r, lane);
+          float dv = 0.f;
+          if (dl != 0.f && v < V) dv = dl * ((v == tgt ? 1.f : 0.f) - __expf(acc.c[i][j][r] - ls));
+          acc.c[i][j][r] = dv;
         }
     }
+    // token-major layout: LDS row = token, 4 consecutive vocabulary entries per 8-byte write
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int tl = acc_col(wn, j, lane);
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int vl = acc_row(wm, i, g * 4, lane);
+          u32x2 packed;
+          packed.x = f32_to_bf16_bits(acc.c[i][j][g * 4 + 0]) | (f32_to_bf16_bits(acc.c[i][j][g * 4 + 1]) << 16);
+          packed.y = f32_to_bf16_bits(acc.c[i][j][g * 4 + 2]) | (f32_to_bf16_bits(acc.c[i][j][g * 4 + 3]) << 16);
+          *reinterpret_cast<u32x2*>(tile + tile_off(tl, vl)) = packed;
+        }
+    }
+    __syncthreads();
+    copy_out(tile, dN + (int64_t)(tn * kTileN) * ldN + tm * kTileM, ldN);
+    __syncthreads();
+    // vocabulary-major layout: LDS row = vocabulary entry
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int tl = acc_col(wn, j, lane);
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int vl = acc_row(wm, i, r, lane);
+          *reinterpret_cast<uint16_t*>(tile + tile_off(vl, tl)) = (uint16_t)f32_to_bf16_bits(acc.c[i][j][r]);
+        }
+    }
+    __syncthreads();
+    copy_out(tile, dT + (int64_t)(tm * kTileM) * ldT + tn * kTileN, ldT);
   }
 };
 
@@ -195,11 +234,15 @@ struct EpiDH {
 // Small kernels
 // ---------------------------------------------------------------------------
 
-// dst[c][r] = r < rows ? src[r][c] : 0 for r < rows_pad, c < cols (bf16 bits).
-// 64 x 64 tiles through LDS; cols and rows_pad are multiples of 64.
+// Transposed, zero-padded copy of a bf16 [rows x cols] matrix, in blocks of
+// `chunk` source rows: source row r, column c goes to
+//   dst[(r / chunk) * cols * ld + c * ld + r % chunk]   (0 for r >= rows),
+// i.e. block b is the [cols x chunk] transpose of rows [b*chunk, (b+1)*chunk)
+// with row stride ld >= chunk.  64 x 64 tiles through LDS; cols, chunk and the
+// padded row count are multiples of 64.
 __global__ __launch_bounds__(256) void transpose_pad_kernel(const uint16_t* __restrict__ src, int rows, int cols,
                                                             int64_t ld_src, uint16_t* __restrict__ dst,
-                                                            int64_t ld_dst) {
+                                                            int64_t chunk, int64_t ld) {
   __shared__ uint16_t tile[64][66];
   const int c0 = blockIdx.x * 64, r0 = blockIdx.y * 64;
   const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
@@ -208,7 +251,9 @@ __global__ __launch_bounds__(256) void transpose_pad_kernel(const uint16_t* __re
     tile[rr][tx] = (r < rows) ? src[(int64_t)r * ld_src + c0 + tx] : (uint16_t)0;
   }
   __syncthreads();
-  for (int cc = ty; cc < 64; cc += 4) dst[(int64_t)(c0 + cc) * ld_dst + r0 + tx] = tile[tx][cc];
+  const int64_t block = r0 / chunk, rin = r0 % chunk;
+  uint16_t* out = dst + block * cols * ld + rin;
+  for (int cc = ty; cc < 64; cc += 4) out[(int64_t)(c0 + cc) * ld + tx] = tile[tx][cc];
 }
 
 __global__ void fill_f32_kernel(float* __restrict__ p, int64_t n, float v) {
@@ -336,8 +381,14 @@ __global__ __launch_bounds__(kFinThreads) void reduce_loss_kernel(int nblk, cons
 // Workspace plan
 // ---------------------------------------------------------------------------
 
+// Row strides of the workspace matrices are padded by kStridePad elements
+// (128 bytes): power-of-two strides would send every row of a tile to the same
+// memory channels.
+constexpr int64_t kStridePad = 64;
+
 struct Plan {
   int64_t Npad, Vpad, Vc, ntv, nfin;
+  int64_t ldH, ldW, ldN, ldT;   // row strides of H^T, W^T blocks, Delta [t][v], Delta^T [v][t]
   int64_t off_pm, off_pl, off_zt, off_lse, off_delta, off_blk, off_ht, off_wt, off_dn, off_dt, total;
 };
 
@@ -348,6 +399,10 @@ Plan make_plan(int64_t N, int64_t d, int64_t V) {
   p.Vc = p.Vpad < kVocabChunk ? p.Vpad : kVocabChunk;
   p.ntv = p.Vpad / kTileM;
   p.nfin = (N + kFinThreads - 1) / kFinThreads;
+  p.ldH = p.Npad + kStridePad;
+  p.ldW = p.Vc + kStridePad;
+  p.ldN = p.Vc + kStridePad;
+  p.ldT = p.Npad + kStridePad;
   int64_t o = 0;
   auto take = [&](int64_t bytes) {
     const int64_t at = o;
@@ -360,10 +415,10 @@ Plan make_plan(int64_t N, int64_t d, int64_t V) {
   p.off_lse = take(p.Npad * 4);
   p.off_delta = take(p.Npad * 4);
   p.off_blk = take((p.nfin > 0 ? p.nfin : 1) * 5 * 8);
-  p.off_ht = take(d * p.Npad * 2);
-  p.off_wt = take(d * p.Vpad * 2);
-  p.off_dn = take(p.Npad * p.Vc * 2);
-  p.off_dt = take(p.Vc * p.Npad * 2);
+  p.off_ht = take(d * p.ldH * 2);
+  p.off_wt = take(d * ((p.Vpad + p.Vc - 1) / p.Vc) * p.ldW * 2);   // [V/Vc][d][ldW] blocks
+  p.off_dn = take(p.Npad * p.ldN * 2);
+  p.off_dt = take(p.Vc * p.ldT * 2);
   p.total = o;
   return p;
 }
@@ -468,10 +523,10 @@ int pspo_loss_fwd_bwd(const uint16_t* hidden, const uint16_t* w_head, const int3
   PSPO_HIP_CHECK(hipGetLastError());
   // 3. K-contiguous copies for the gradient products
   hipLaunchKernelGGL(transpose_pad_kernel, dim3(d / 64, (unsigned)(pl.Npad / 64)), dim3(256), 0, stream, hidden, N,
-                     d, (int64_t)d, hT, pl.Npad);
+                     d, (int64_t)d, hT, pl.Npad, pl.ldH);   // one block: H^T [d x Npad]
   PSPO_HIP_CHECK(hipGetLastError());
   hipLaunchKernelGGL(transpose_pad_kernel, dim3(d / 64, (unsigned)(pl.Vpad / 64)), dim3(256), 0, stream, w_head, V,
-                     d, (int64_t)d, wT, pl.Vpad);
+                     d, (int64_t)d, wT, pl.Vc, pl.ldW);     // per vocabulary chunk: W[chunk]^T [d x Vc]
   PSPO_HIP_CHECK(hipGetLastError());
   // 4. backward, one vocabulary chunk at a time
   for (int64_t v0 = 0; v0 < pl.Vpad; v0 += pl.Vc) {
@@ -479,16 +534,16 @@ int pspo_loss_fwd_bwd(const uint16_t* hidden, const uint16_t* w_head, const int3
     const int ctiles = (int)(vc / kTileM);
     {
       GemmShape g{w_head + v0 * d, d, (int)(V - v0), hidden, d, N, d, ctiles, tiles_tok};
-      EpiDelta e{V, N, (int)v0, target, lse, delta, dT, pl.Npad, dN, pl.Vc};
+      EpiDelta e{V, N, (int)v0, target, lse, delta, dT, pl.ldT, dN, pl.ldN};
       if (int rc = launch_gemm(g, e, stream)) return rc;
     }
     {
-      GemmShape g{dT, pl.Npad, (int)vc, hT, pl.Npad, d, (int)pl.Npad, ctiles, tiles_d};
+      GemmShape g{dT, pl.ldT, (int)vc, hT, pl.ldH, d, (int)pl.Npad, ctiles, tiles_d};
       EpiDW e{V, d, (int)v0, d_w_head, accumulate};
       if (int rc = launch_gemm(g, e, stream)) return rc;
     }
     {
-      GemmShape g{dN, pl.Vc, (int)pl.Npad, wT + v0, pl.Vpad, d, (int)vc, tiles_tok, tiles_d};
+      GemmShape g{dN, pl.ldN, (int)pl.Npad, wT + (v0 / pl.Vc) * d * pl.ldW, pl.ldW, d, (int)vc, tiles_tok, tiles_d};
       EpiDH e{N, d, d_hidden, v0 == 0};
       if (int rc = launch_gemm(g, e, stream)) return rc;
     }
