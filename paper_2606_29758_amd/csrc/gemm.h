@@ -6,28 +6,30 @@
 //   with K contiguous (row strides lda / ldb in elements), K % 32 == 0.
 //
 // Tiling: a 256-thread work-group (4 wave64s in a 2 x 2 arrangement) owns a
-// 256 x 256 C tile; each wave owns 128 x 128 = 4 x 4 blocks of the
-// v_mfma_f32_32x32x16_bf16 instruction, i.e. 256 fp32 accumulators per lane
-// (the whole AGPR file).
+// 256 x 256 C tile; each wave owns 128 x 128 = 8 x 8 blocks of the
+// v_mfma_f32_16x16x32_bf16 instruction, i.e. 256 fp32 accumulators per lane
+// (the whole AGPR file).  On real (random) bf16 operands this instruction
+// sustains a markedly higher rate than the 32x32x16 form at the same LDS
+// traffic per flop (measured on MI355X: ~86% vs ~77% of peak in a pure MFMA
+// loop), so it is the one used.
 //
-// Pipeline: K advances in steps of 32 through a ring of kStages LDS stages
-// (32 KB each: 256 rows x 64 bytes of A and of B).  Operands go from global
-// memory straight into LDS (global_load_lds_dwordx4: no staging registers, no
-// LDS-write instructions); each wave loads 64 rows of A and 64 rows of B per
-// step.  Step kt:
-//   1. sub-step 0: 16 MFMAs on register slot 0 while the sub-step-1 operands
-//      of stage kt are read into slot 1;
-//   2. wait for this wave's loads of step kt+1, then one work-group barrier:
-//      step kt+1 is now visible and every wave is done with step kt-1;
-//   3. sub-step 1: 16 MFMAs on slot 1 while the loads of step kt+kStages-1 go
-//      into the stage step kt-1 used and the sub-step-0 operands of step kt+1
-//      are read into slot 0.
-// A load therefore has kStages-2 steps (about 1000 MFMA cycles each) to land.
-// Each phase is written as groups of two MFMAs and one or two memory ops,
-// fenced with sched_barrier so the compiler keeps the interleave.
-// LDS rows are 64 bytes; the four 16-byte chunks of row r are stored XOR-ed
-// with ((r>>1) ^ (r>>2)) & 3, so the operand reads of consecutive rows hit
-// distinct banks.
+// Pipeline: K advances in steps of 32 (one MFMA depth) through a ring of
+// kStages LDS stages (32 KB each: 256 rows x 64 bytes of A and of B).
+// Operands go from global memory straight into LDS (global_load_lds_dwordx4:
+// no staging registers, no LDS-write instructions); each wave loads 64 rows of
+// A and 64 rows of B per step.  Step kt:
+//   1. 64 MFMAs on the register slot holding step kt's operands, interleaved
+//      with the 16 LDS reads of step kt+1's operands (into the other slot) and
+//      the 8 loads of step kt+kStages-1 into the stage step kt-1 used;
+//   2. wait until this wave's loads of step kt+2 have landed and its LDS reads
+//      are done, then one work-group barrier: step kt+2 is visible to all and
+//      every wave is done with the stage step kt used.
+// A load therefore has kStages-3 whole steps (about 1000 MFMA cycles each) to
+// land.  Each group of four MFMAs and its memory ops is fenced with
+// sched_barrier so the compiler keeps the interleave.  LDS rows are 64 bytes;
+// the four 16-byte chunks of row r are stored XOR-ed with ((r>>1) ^ (r>>2)) & 3,
+// which is bank-conflict free for the 16-row operand reads and repeats every
+// 16 rows, so all reads of a step use one per-lane base plus fixed offsets.
 //
 // Rows past M (or N) are clamped to the last valid row when loading; the
 // epilogue masks them.  Work-group -> tile mapping is XCD-aware: work-groups
@@ -50,6 +52,10 @@ constexpr int kLdsOperand = kTileM * kLdsRow;      // 16 KB
 constexpr int kLdsStage = 2 * kLdsOperand;         // A + B: 32 KB
 constexpr int kLdsBytes = kStages * kLdsStage;     // 160 KB
 
+// Accumulator layout: per wave 8 x 8 blocks of 16 x 16, four fp32 per lane each.
+constexpr int kBlocks = 8;
+constexpr int kAccPerBlock = 4;
+
 struct GemmShape {
   const uint16_t* A;
   int64_t lda;
@@ -62,15 +68,15 @@ struct GemmShape {
 };
 
 // Accumulator (i, j, r) of lane `lane` in wave (wm, wn) holds
-//   C[row0 + wm*128 + i*32 + (r/4)*8 + (lane/32)*4 + r%4][col0 + wn*128 + j*32 + lane%32].
+//   C[row0 + wm*128 + i*16 + (lane/16)*4 + r][col0 + wn*128 + j*16 + lane%16].
 struct AccTile {
-  f32x16 c[4][4];
+  f32x4 c[kBlocks][kBlocks];
 };
 
 __device__ __forceinline__ int acc_row(int wm, int i, int r, int lane) {
-  return wm * 128 + i * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
+  return wm * 128 + i * 16 + (lane >> 4) * 4 + r;
 }
-__device__ __forceinline__ int acc_col(int wn, int j, int lane) { return wn * 128 + j * 32 + (lane & 31); }
+__device__ __forceinline__ int acc_col(int wn, int j, int lane) { return wn * 128 + j * 16 + (lane & 15); }
 
 __device__ __forceinline__ int chunk_swizzle(int row) { return ((row >> 1) ^ (row >> 2)) & 3; }
 
@@ -98,10 +104,26 @@ struct Const {
   static constexpr int value = N;
 };
 
-// Scheduling-group masks of __builtin_amdgcn_sched_group_barrier.
-constexpr int kSchedMfma = 0x008, kSchedVmemRead = 0x020, kSchedDsRead = 0x100;
-
 typedef __attribute__((address_space(3))) void lds_void;
+
+// c += a * b on one 16 x 16 x 32 bf16 block, accumulating in place in AGPRs.
+// Written as inline asm with the accumulator tied in/out: through the builtin,
+// the register allocator is free to give the result a different AGPR quadruple
+// than the addend, and with all 256 AGPRs live it then rotates accumulators
+// through VGPRs with accvgpr read/write/mov copies on every loop trip (each of
+// which waits for the MFMA producing it).  The compiler's hazard tracking does
+// not see inline asm as an MFMA, so the kernel pads the MFMA -> VALU hazard
+// itself before its epilogue reads the accumulators (mfma_drain below); inside
+// the loop no instruction reads an accumulator within 64 MFMAs of its write.
+__device__ __forceinline__ void mfma_16x16x32(f32x4& c, const bf16x8& a, const bf16x8& b) {
+  asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+a"(c) : "v"(a), "v"(b));
+}
+
+// Enough independent wait states for any MFMA result to be readable by VALU,
+// accvgpr reads or memory instructions (16-pass worst case plus margin).
+__device__ __forceinline__ void mfma_drain() {
+  asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory");
+}
 
 // Work-group barrier for the LDS ring: waits until at most `Vm` of this wave's
 // global->LDS loads are outstanding and all its LDS reads are done, then
@@ -120,9 +142,9 @@ __device__ __forceinline__ void stage_barrier() {
 }
 
 // Epilogue interface: `Epi::apply(acc, tm, tn, wm, wn, lane, smem)` (acc may be
-// overwritten); smem is the
-// (no longer needed) LDS ring, 160 KB, free for reductions: every load into
-// it has landed and all waves have passed a barrier before the call.
+// overwritten); smem is the (no longer needed) LDS ring, 160 KB, free for
+// reductions: every load into it has landed and all waves have passed a
+// barrier before the call.
 template <class Epi>
 __global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_per_eu(1, 1)))
 void gemm_nt_kernel(GemmShape g, Epi epi) {
@@ -151,50 +173,44 @@ void gemm_nt_kernel(GemmShape g, Epi epi) {
   }
   const int wave_lds = wave * 64 * kLdsRow;
 
-  // MFMA operand reads: block i of A is row wm*128 + i*32 + lane%32; sub-step kk
-  // reads logical chunk kk*2 + lane/32.
-  int rdA[2][4], rdB[2][4];
-#pragma unroll
-  for (int kk = 0; kk < 2; ++kk)
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int ra = wm * 128 + i * 32 + (lane & 31);
-      const int rb = wn * 128 + i * 32 + (lane & 31);
-      const int c = kk * 2 + (lane >> 5);
-      rdA[kk][i] = ra * kLdsRow + ((c ^ chunk_swizzle(ra)) << 4);
-      rdB[kk][i] = kLdsOperand + rb * kLdsRow + ((c ^ chunk_swizzle(rb)) << 4);
-    }
+  // MFMA operand reads: block i of A is rows wm*128 + i*16 + lane%16, K chunk
+  // lane/16 (8 bf16 of the 32-deep step).  The swizzle of row r + 16 i equals
+  // that of row r, so block i is the lane's base plus i * 16 rows.
+  const int ra0 = wm * 128 + (lane & 15), rb0 = wn * 128 + (lane & 15);
+  const int rdA = ra0 * kLdsRow + (((lane >> 4) ^ chunk_swizzle(ra0)) << 4);
+  const int rdB = kLdsOperand + rb0 * kLdsRow + (((lane >> 4) ^ chunk_swizzle(rb0)) << 4);
 
-  bf16x8 fa[2][4], fb[2][4];
+  bf16x8 fa[2][kBlocks], fb[2][kBlocks];
   AccTile acc;
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < kBlocks; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc.c[i][j] = f32x16{};
+    for (int j = 0; j < kBlocks; ++j) acc.c[i][j] = f32x4{};
 
   const int nk = g.K / kTileK;
 
-  // Operand q (0..7) of a sub-step, in the order the MFMAs consume them:
-  // A0, B0, B1, B2, B3, A1, A2, A3.
-  auto read_frag = [&](int stage, auto kk, auto slot, auto q) {
-    constexpr int k = decltype(kk)::value;
-    constexpr int s = decltype(slot)::value;
-    constexpr int n = decltype(q)::value;
+  // Operand n (0..15) of a step, in the order the MFMAs consume them:
+  // A0, B0..B7, A1..A7.
+  auto read_frag = [&](int stage, auto slot, auto n) {
+    constexpr int s = decltype(slot)::value, q = decltype(n)::value;
     const unsigned char* base = lds + stage * kLdsStage;
-    if constexpr (n == 0) {
-      fa[s][0] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(base + rdA[k][0]));
-    } else if constexpr (n <= 4) {
-      fb[s][n - 1] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(base + rdB[k][n - 1]));
+    if constexpr (q == 0) {
+      fa[s][0] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(base + rdA));
+    } else if constexpr (q <= 8) {
+      fb[s][q - 1] =
+          __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(base + rdB + (q - 1) * 16 * kLdsRow));
     } else {
-      fa[s][n - 4] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(base + rdA[k][n - 4]));
+      fa[s][q - 8] =
+          __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(base + rdA + (q - 8) * 16 * kLdsRow));
     }
   };
-  // MFMA pair q (0..7) of a sub-step: blocks (q/2, 2*(q%2)) and (q/2, 2*(q%2)+1).
-  auto mfma_pair = [&](auto slot, auto q) {
+  // MFMA group q (0..15): blocks (q/2, 4*(q%2) .. 4*(q%2)+3).
+  auto mfma_group = [&](auto slot, auto q) {
     constexpr int s = decltype(slot)::value;
-    constexpr int i = decltype(q)::value / 2, j = 2 * (decltype(q)::value % 2);
-    acc.c[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[s][i], fb[s][j], acc.c[i][j], 0, 0, 0);
-    acc.c[i][j + 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[s][i], fb[s][j + 1], acc.c[i][j + 1], 0, 0, 0);
+    constexpr int i = decltype(q)::value / 2, j = 4 * (decltype(q)::value % 2);
+#pragma unroll
+    for (int jj = 0; jj < 4; ++jj)
+      mfma_16x16x32(acc.c[i][j + jj], fa[s][i], fb[s][j + jj]);
   };
   // Load instruction q (0..7) of a step: operand q/4, 16-row group q%4.
   auto issue_load = [&](int kt, int stage, auto q) {
@@ -211,74 +227,60 @@ void gemm_nt_kernel(GemmShape g, Epi epi) {
     issue_load(kt, stage, Const<4>{}); issue_load(kt, stage, Const<5>{});
     issue_load(kt, stage, Const<6>{}); issue_load(kt, stage, Const<7>{});
   };
-  auto read_all = [&](int stage, auto kk, auto slot) {
-    read_frag(stage, kk, slot, Const<0>{}); read_frag(stage, kk, slot, Const<1>{});
-    read_frag(stage, kk, slot, Const<2>{}); read_frag(stage, kk, slot, Const<3>{});
-    read_frag(stage, kk, slot, Const<4>{}); read_frag(stage, kk, slot, Const<5>{});
-    read_frag(stage, kk, slot, Const<6>{}); read_frag(stage, kk, slot, Const<7>{});
-  };
-  // Operand reads of one sub-step spread over MFMA groups 0..5 (two in groups
-  // 0 and 1), so the last read is issued four MFMAs before the next sub-step
-  // needs its operands.
-  auto reads_of_group = [&](int stage, auto kk, auto slot, auto q) {
+  // Group q of a step: 4 MFMAs on `slot`; the next step's 16 operands are read
+  // two per group in groups 0..7 (the last one 32 MFMAs before it is needed)
+  // and the 8 loads of step kt+kStages-1 go one per group in groups 8..15.
+  auto group = [&](auto slot, int next_stage, int kt_load, int refill, auto q) {
     constexpr int n = decltype(q)::value;
-    if constexpr (n < 2) {
-      read_frag(stage, kk, slot, Const<2 * n>{});
-      read_frag(stage, kk, slot, Const<2 * n + 1>{});
-    } else if constexpr (n < 6) {
-      read_frag(stage, kk, slot, Const<n + 2>{});
+    constexpr int other = 1 - decltype(slot)::value;
+    mfma_group(slot, q);
+    if constexpr (n < 8) {
+      read_frag(next_stage, Const<other>{}, Const<2 * n>{});
+      read_frag(next_stage, Const<other>{}, Const<2 * n + 1>{});
+    } else {
+      issue_load(kt_load, refill, Const<n - 8>{});
     }
-  };
-  // Sub-step 0 of stage `cur` (operands in slot 0) while the slot-1 operands of
-  // sub-step 1 are read: 8 groups of 2 MFMAs, fenced so the compiler keeps the
-  // interleave.
-  auto phase_a = [&](int cur, auto q) {
-    mfma_pair(Const<0>{}, q);
-    reads_of_group(cur, Const<1>{}, Const<1>{}, q);
     __builtin_amdgcn_sched_barrier(0);
   };
-  // Sub-step 1 (slot 1) while step kt+kStages-1 is loaded and the slot-0
-  // operands of the next stage are read: 8 groups of {2 MFMA, 1 load, reads}.
-  auto phase_b = [&](int kt_load, int refill, int next, auto q) {
-    mfma_pair(Const<1>{}, q);
-    issue_load(kt_load, refill, q);
-    reads_of_group(next, Const<0>{}, Const<0>{}, q);
-    __builtin_amdgcn_sched_barrier(0);
-  };
-
-  auto run_phase_a = [&](int cur) {
-    phase_a(cur, Const<0>{}); phase_a(cur, Const<1>{}); phase_a(cur, Const<2>{}); phase_a(cur, Const<3>{});
-    phase_a(cur, Const<4>{}); phase_a(cur, Const<5>{}); phase_a(cur, Const<6>{}); phase_a(cur, Const<7>{});
-    // this wave's loads of the next step have landed and its LDS reads are done;
-    // after the barrier every wave's have (the loads of later steps stay in flight)
+  auto step = [&](auto slot, int kt) {
+    const int next_stage = (kt + 1) % kStages;
+    const int refill = (kt + kStages - 1) % kStages;  // the stage step kt-1 used
+    const int kl = kt + kStages - 1;
+    group(slot, next_stage, kl, refill, Const<0>{}); group(slot, next_stage, kl, refill, Const<1>{});
+    group(slot, next_stage, kl, refill, Const<2>{}); group(slot, next_stage, kl, refill, Const<3>{});
+    group(slot, next_stage, kl, refill, Const<4>{}); group(slot, next_stage, kl, refill, Const<5>{});
+    group(slot, next_stage, kl, refill, Const<6>{}); group(slot, next_stage, kl, refill, Const<7>{});
+    group(slot, next_stage, kl, refill, Const<8>{}); group(slot, next_stage, kl, refill, Const<9>{});
+    group(slot, next_stage, kl, refill, Const<10>{}); group(slot, next_stage, kl, refill, Const<11>{});
+    group(slot, next_stage, kl, refill, Const<12>{}); group(slot, next_stage, kl, refill, Const<13>{});
+    group(slot, next_stage, kl, refill, Const<14>{}); group(slot, next_stage, kl, refill, Const<15>{});
     stage_barrier<(kStages - 3) * 8>();
   };
 
-  auto run_phase_b = [&](int kt) {
-    const int next = (kt + 1) % kStages;
-    const int refill = (kt + kStages - 1) % kStages;  // the stage step kt-1 used
-    const int kl = kt + kStages - 1;
-    phase_b(kl, refill, next, Const<0>{}); phase_b(kl, refill, next, Const<1>{});
-    phase_b(kl, refill, next, Const<2>{}); phase_b(kl, refill, next, Const<3>{});
-    phase_b(kl, refill, next, Const<4>{}); phase_b(kl, refill, next, Const<5>{});
-    phase_b(kl, refill, next, Const<6>{}); phase_b(kl, refill, next, Const<7>{});
-  };
-
-  // prologue: steps 0 .. kStages-2 in flight, step 0 visible, sub-step 0 of step 0
+  // prologue: steps 0 .. kStages-2 in flight; step 0 visible, its operands in
+  // slot 0; then step 1 visible (read during step 0)
   for (int s = 0; s < kStages - 1; ++s) issue_loads(s, s);
   stage_barrier<(kStages - 2) * 8>();
-  read_all(0, Const<0>{}, Const<0>{});
-  run_phase_a(0);
+  read_frag(0, Const<0>{}, Const<0>{}); read_frag(0, Const<0>{}, Const<1>{});
+  read_frag(0, Const<0>{}, Const<2>{}); read_frag(0, Const<0>{}, Const<3>{});
+  read_frag(0, Const<0>{}, Const<4>{}); read_frag(0, Const<0>{}, Const<5>{});
+  read_frag(0, Const<0>{}, Const<6>{}); read_frag(0, Const<0>{}, Const<7>{});
+  read_frag(0, Const<0>{}, Const<8>{}); read_frag(0, Const<0>{}, Const<9>{});
+  read_frag(0, Const<0>{}, Const<10>{}); read_frag(0, Const<0>{}, Const<11>{});
+  read_frag(0, Const<0>{}, Const<12>{}); read_frag(0, Const<0>{}, Const<13>{});
+  read_frag(0, Const<0>{}, Const<14>{}); read_frag(0, Const<0>{}, Const<15>{});
+  stage_barrier<(kStages - 3) * 8>();
 
-  // Iteration kt: sub-step 1 of step kt (loads of step kt+kStages-1 and the
-  // slot-0 operands of step kt+1 issued alongside), then sub-step 0 of step kt+1.
-  for (int kt = 0; kt + 1 < nk; ++kt) {
-    run_phase_b(kt);
-    run_phase_a((kt + 1) % kStages);
+  int kt = 0;
+  for (; kt + 1 < nk; kt += 2) {
+    step(Const<0>{}, kt);
+    step(Const<1>{}, kt + 1);
   }
-  run_phase_b(nk - 1);
+  if (kt < nk) step(Const<0>{}, kt);
+
   // drain the (clamped, unused) loads still in flight before LDS is reused
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  mfma_drain();
   __syncthreads();
 
   epi.apply(acc, tm, tn, wm, wn, lane, reinterpret_cast<float*>(lds));

@@ -47,15 +47,15 @@ struct EpiForward {
   __device__ __forceinline__ void apply(const AccTile& acc, int tm, int tn, int wm, int wn, int lane, float* smem) const {
     float* red = smem;  // [2 wave rows][256 columns][m, l]
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
+    for (int j = 0; j < kBlocks; ++j) {
       const int cl = acc_col(wn, j, lane);
       const int t = tn * kTileN + cl;
       const int tgt = (t < N) ? target[t] : -1;
       float m = kNegInf;
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+      for (int i = 0; i < kBlocks; ++i)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
+        for (int r = 0; r < kAccPerBlock; ++r) {
           const int v = tm * kTileM + acc_row(wm, i, r, lane);
           const float x = acc.c[i][j][r];
           if (v < V) {
@@ -63,19 +63,21 @@ struct EpiForward {
             if (v == tgt) zt[t] = x;
           }
         }
+      m = fmaxf(m, __shfl_xor(m, 16));
       m = fmaxf(m, __shfl_xor(m, 32));
       float l = 0.f;
       if (m != kNegInf) {
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+        for (int i = 0; i < kBlocks; ++i)
 #pragma unroll
-          for (int r = 0; r < 16; ++r) {
+          for (int r = 0; r < kAccPerBlock; ++r) {
             const int v = tm * kTileM + acc_row(wm, i, r, lane);
             if (v < V) l += __expf(acc.c[i][j][r] - m);
           }
       }
+      l += __shfl_xor(l, 16);
       l += __shfl_xor(l, 32);
-      if (lane < 32) {
+      if (lane < 16) {
         red[(wm * 256 + cl) * 2 + 0] = m;
         red[(wm * 256 + cl) * 2 + 1] = l;
       }
@@ -129,48 +131,47 @@ struct EpiDelta {
     unsigned char* tile = reinterpret_cast<unsigned char*>(smem);
     // Delta in place of the logits
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
+    for (int j = 0; j < kBlocks; ++j) {
       const int t = tn * kTileN + acc_col(wn, j, lane);
       const bool tv = t < N;
       const float dl = tv ? delta[t] : 0.f;
       const float ls = tv ? lse[t] : 0.f;
       const int tgt = tv ? target[t] : -1;
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+      for (int i = 0; i < kBlocks; ++i)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
+        for (int r = 0; r < kAccPerBlock; ++r) {
           const int v = v0 + tm * kTileM + acc_row(wm, i, r, lane);
           float dv = 0.f;
           if (dl != 0.f && v < V) dv = dl * ((v == tgt ? 1.f : 0.f) - __expf(acc.c[i][j][r] - ls));
           acc.c[i][j][r] = dv;
         }
     }
-    // token-major layout: LDS row = token, 4 consecutive vocabulary entries per 8-byte write
+    // token-major layout: LDS row = token, the lane's 4 consecutive vocabulary
+    // entries of a block in one 8-byte write
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
+    for (int j = 0; j < kBlocks; ++j) {
       const int tl = acc_col(wn, j, lane);
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const int vl = acc_row(wm, i, g * 4, lane);
-          u32x2 packed;
-          packed.x = f32_to_bf16_bits(acc.c[i][j][g * 4 + 0]) | (f32_to_bf16_bits(acc.c[i][j][g * 4 + 1]) << 16);
-          packed.y = f32_to_bf16_bits(acc.c[i][j][g * 4 + 2]) | (f32_to_bf16_bits(acc.c[i][j][g * 4 + 3]) << 16);
-          *reinterpret_cast<u32x2*>(tile + tile_off(tl, vl)) = packed;
-        }
+      for (int i = 0; i < kBlocks; ++i) {
+        const int vl = acc_row(wm, i, 0, lane);
+        u32x2 packed;
+        packed.x = f32_to_bf16_bits(acc.c[i][j][0]) | (f32_to_bf16_bits(acc.c[i][j][1]) << 16);
+        packed.y = f32_to_bf16_bits(acc.c[i][j][2]) | (f32_to_bf16_bits(acc.c[i][j][3]) << 16);
+        *reinterpret_cast<u32x2*>(tile + tile_off(tl, vl)) = packed;
+      }
     }
     __syncthreads();
     copy_out(tile, dN + (int64_t)(tn * kTileN) * ldN + tm * kTileM, ldN);
     __syncthreads();
     // vocabulary-major layout: LDS row = vocabulary entry
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
+    for (int j = 0; j < kBlocks; ++j) {
       const int tl = acc_col(wn, j, lane);
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+      for (int i = 0; i < kBlocks; ++i)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
+        for (int r = 0; r < kAccPerBlock; ++r) {
           const int vl = acc_row(wm, i, r, lane);
           *reinterpret_cast<uint16_t*>(tile + tile_off(vl, tl)) = (uint16_t)f32_to_bf16_bits(acc.c[i][j][r]);
         }
@@ -188,13 +189,13 @@ struct EpiDW {
 
   __device__ __forceinline__ void apply(const AccTile& acc, int tm, int tn, int wm, int wn, int lane, float*) const {
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
+    for (int j = 0; j < kBlocks; ++j) {
       const int col = tn * kTileN + acc_col(wn, j, lane);
       if (col >= d) continue;
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+      for (int i = 0; i < kBlocks; ++i)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
+        for (int r = 0; r < kAccPerBlock; ++r) {
           const int v = v0 + tm * kTileM + acc_row(wm, i, r, lane);
           if (v < V) {
             float* p = dW + (int64_t)v * d + col;
@@ -213,13 +214,13 @@ struct EpiDH {
 
   __device__ __forceinline__ void apply(const AccTile& acc, int tm, int tn, int wm, int wn, int lane, float*) const {
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
+    for (int j = 0; j < kBlocks; ++j) {
       const int col = tn * kTileN + acc_col(wn, j, lane);
       if (col >= d) continue;
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+      for (int i = 0; i < kBlocks; ++i)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
+        for (int r = 0; r < kAccPerBlock; ++r) {
           const int t = tm * kTileM + acc_row(wm, i, r, lane);
           if (t < N) {
             float* p = dH + (int64_t)t * d + col;
