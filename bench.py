@@ -12,8 +12,11 @@ old log-probs = new + N(0, 0.1^2)).
 
 Prints one JSON line.  `roofline` covers the loss call (the forward, logit-
 gradient, dW and dH matrix-core kernels it launches), timed with HIP events
-on the stream it runs on: achieved = 6 N V d algorithmic flops / mean call
-duration.  `cpu_baseline` times the float64 CPU oracle on a bounded sample of
+on the stream it runs on: achieved = (2 N + 4 n_bwd) V d algorithmic flops /
+mean call duration, where n_bwd counts the tokens whose logit gradient is not
+identically zero (the others add nothing to dH or dW and are skipped).
+`dense_equivalent_tflops` is 6 N V d / duration, the rate a path that ran the
+gradient products over every token would need for the same throughput.  `cpu_baseline` times the float64 CPU oracle on a bounded sample of
 the same step (all cutoffs and packing, then the loss of the first
 --cpu-tokens packed tokens).
 """
@@ -140,9 +143,14 @@ def main():
     loss_ms = [s.elapsed_time(e) for s, e in zip(starts, ends)]
     loss_avg = float(np.mean(loss_ms))
     assert int(step.err.item()) == 0, "device error flag raised"
+    n_bwd = int(out["stats"][4].item())   # tokens with a nonzero logit-gradient row
 
-    flops = 6.0 * N * cfg.V * cfg.d
+    # matrix-core work the step needs: the forward over all N tokens (2 N V d),
+    # dH and dW over the n_bwd tokens whose logit gradient is not zero (4 n_bwd V d;
+    # every other token contributes exactly zero to both)
+    flops = (2.0 * N + 4.0 * n_bwd) * cfg.V * cfg.d
     achieved = flops / (loss_avg * 1e-3) / 1e12
+    dense_equiv = 6.0 * N * cfg.V * cfg.d / (loss_avg * 1e-3) / 1e12
     # HBM bytes per call from the committed counter runs, only while the kernels
     # are still the ones those counters were taken on
     traffic = None
@@ -171,6 +179,7 @@ def main():
                         f"{' (pinned to full length)' if cfg.full_trajectory else ''}, "
                         f"logp_old noise sigma {cfg.sigma_lp}",
             "prefix_tokens": N,
+            "backward_tokens": n_bwd,
             "total_tokens": int(wl.total_tokens),
             "kept_fraction": N / wl.total_tokens,
             "global_batch": cfg.R,
@@ -178,9 +187,12 @@ def main():
         },
         "loss_call_ms": loss_avg,
         "pct_bf16_peak": 100.0 * achieved / PEAK_BF16_TFLOPS,
+        "dense_equivalent_tflops": dense_equiv,
         "roofline": {
             "bound": "mfma",
             "kernel": "pspo_loss_fwd_bwd (forward, logit-gradient, dW and dH bf16 MFMA kernels)",
+            "flops": "(2 N + 4 n_bwd) V d per call: forward over all prefix tokens, dH and dW over "
+                     "the tokens with a nonzero logit gradient",
             "achieved": achieved,
             "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s",

@@ -176,9 +176,12 @@ size_t pspo_loss_workspace_bytes(int32_t N, int32_t d, int32_t V, uint32_t flags
  *  d_hidden   device, float32 [N, d] out.
  *  d_w_head   device, float32 [V, d] out (or accumulated, see flags).
  *  logp_new   device, float32 [N] out, or NULL.
- *  stats      device, float64 [4] out, or NULL: { loss_scale * sum_i |c_i s_i|,
+ *  stats      device, float64 [5] out, or NULL: { loss_scale * sum_i |c_i s_i|,
  *             #tokens with A != 0 and mu = 0 (clipped), #tokens with A == 0,
- *             max_i c_i }.
+ *             max_i c_i, #tokens with delta_i != 0 }.  Only the last group
+ *             of tokens enters the backward products: every other token has
+ *             delta_i = 0, hence a zero row of G, a zero d_hidden row and no
+ *             d_w_head term, so skipping it is exact.
  *  err_flag   device, int32 [1] or NULL (PSPO_DEVERR_TARGET, PSPO_DEVERR_SEQ_ID).
  *  workspace  device, >= pspo_loss_workspace_bytes(N, d, V, flags) bytes,
  *             256-byte aligned; its contents on entry are ignored.

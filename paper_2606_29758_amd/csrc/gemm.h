@@ -3,7 +3,7 @@
 // these "NT" products:
 //
 //   C[m][n] = sum_k A[m][k] * B[n][k],  A: [M x K], B: [N x K], both row-major
-//   with K contiguous (row strides lda / ldb in elements), K % 32 == 0.
+//   with K contiguous (row strides lda / ldb in elements), K % 32 == 0, K > 0.
 //
 // Tiling: a 256-thread work-group (4 wave64s in a 2 x 2 arrangement) owns a
 // 256 x 256 C tile; each wave owns 128 x 128 = 8 x 8 blocks of the
@@ -32,7 +32,9 @@
 // 16 rows, so all reads of a step use one per-lane base plus fixed offsets.
 //
 // Rows past M (or N) are clamped to the last valid row when loading; the
-// epilogue masks them.  Work-group -> tile mapping is XCD-aware: work-groups
+// epilogue masks them.  B rows can be gathered through an index map, and one
+// dimension can be bounded by a count that lives in device memory (so a
+// product over a data-dependent subset of tokens needs no host round trip).  Work-group -> tile mapping is XCD-aware: work-groups
 // are dispatched round-robin over the 8 XCDs, so consecutive tile ids are
 // handed to the same XCD, in a grouped order that keeps 8 A-tiles resident
 // while B-tiles stream (L2 reuse inside each XCD's private cache).
@@ -56,6 +58,9 @@ constexpr int kLdsBytes = kStages * kLdsStage;     // 160 KB
 constexpr int kBlocks = 8;
 constexpr int kAccPerBlock = 4;
 
+// Which dimension of a product a device-resident bound applies to.
+constexpr int kDynNone = 0, kDynM = 1, kDynN = 2, kDynK = 3;
+
 struct GemmShape {
   const uint16_t* A;
   int64_t lda;
@@ -64,7 +69,14 @@ struct GemmShape {
   int64_t ldb;
   int N;
   int K;
-  int tiles_m, tiles_n;
+  int tiles_m, tiles_n;      // grid extent (host-side upper bound)
+  // Optional gather: row r of the B operand is row b_rows[r] of B.
+  const int32_t* b_rows = nullptr;
+  // Optional bound read from device memory when the kernel starts: limits M
+  // (kDynM) or N (kDynN) to *dyn, or K (kDynK) to *dyn rounded up to kTileK.
+  // Tiles outside the bound exit at once; a shorter K shortens the loop.
+  const int32_t* dyn = nullptr;
+  int dyn_dim = kDynNone;
 };
 
 // Accumulator (i, j, r) of lane `lane` in wave (wm, wn) holds
@@ -80,14 +92,23 @@ __device__ __forceinline__ int acc_col(int wn, int j, int lane) { return wn * 12
 
 __device__ __forceinline__ int chunk_swizzle(int row) { return ((row >> 1) ^ (row >> 2)) & 3; }
 
-__device__ __forceinline__ bool map_tile(const GemmShape& g, int& tm, int& tn) {
+// Tile of work-group blockIdx.x among the tiles_m x tiles_n tiles that cover
+// an M x N product (tiles_m/n: the launch's extents, possibly more than the
+// product needs when M or N is bounded on the device).  The tile count is
+// taken from the actual M and N so that the work spreads over all XCDs even
+// when a device-side bound leaves only part of the launch with work.
+__device__ __forceinline__ bool map_tile(int tiles_m, int tiles_n, int M, int N, int& tm, int& tn) {
+  tiles_m = min(tiles_m, (M + kTileM - 1) / kTileM);
+  tiles_n = min(tiles_n, (N + kTileN - 1) / kTileN);
+  const int total = tiles_m * tiles_n;
+  const int per_xcd = (total + kNumXcd - 1) / kNumXcd;
   const int bid = blockIdx.x;
-  const int per_xcd = gridDim.x / kNumXcd;  // grid is padded to a multiple of 8
+  if (bid / kNumXcd >= per_xcd) return false;
   const int t = (bid % kNumXcd) * per_xcd + bid / kNumXcd;
-  if (t >= g.tiles_m * g.tiles_n) return false;
-  const int width = kGroupM * g.tiles_n;
+  if (t >= total) return false;
+  const int width = kGroupM * tiles_n;
   const int first = (t / width) * kGroupM;
-  const int gsize = min(g.tiles_m - first, kGroupM);
+  const int gsize = min(tiles_m - first, kGroupM);
   const int rem = t % width;
   tm = first + rem % gsize;
   tn = rem / gsize;
@@ -150,8 +171,15 @@ __global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_pe
 void gemm_nt_kernel(GemmShape g, Epi epi) {
   __shared__ __attribute__((aligned(1024))) unsigned char lds[kLdsBytes];
 
+  int M = g.M, N = g.N, K = g.K;
+  if (g.dyn != nullptr) {
+    const int v = max(__builtin_amdgcn_readfirstlane(*g.dyn), 0);
+    if (g.dyn_dim == kDynM) M = min(M, v);
+    else if (g.dyn_dim == kDynN) N = min(N, v);
+    else if (g.dyn_dim == kDynK) K = min(K, (v + kTileK - 1) / kTileK * kTileK);
+  }
   int tm, tn;
-  if (!map_tile(g, tm, tn)) return;
+  if (!map_tile(g.tiles_m, g.tiles_n, M, N, tm, tn)) return;
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -166,8 +194,9 @@ void gemm_nt_kernel(GemmShape g, Epi epi) {
   for (int q = 0; q < 4; ++q) {
     const int row = wave * 64 + q * 16 + (lane >> 2);
     const int chunk = (lane & 3) ^ chunk_swizzle(row);
-    const int ra = min(tm * kTileM + row, g.M - 1);
-    const int rb = min(tn * kTileN + row, g.N - 1);
+    const int ra = min(tm * kTileM + row, M - 1);
+    int rb = min(tn * kTileN + row, N - 1);
+    if (g.b_rows != nullptr) rb = g.b_rows[rb];
     src[0][q] = reinterpret_cast<const unsigned char*>(g.A) + (int64_t)ra * g.lda * 2 + chunk * 16;
     src[1][q] = reinterpret_cast<const unsigned char*>(g.B) + (int64_t)rb * g.ldb * 2 + chunk * 16;
   }
@@ -187,7 +216,7 @@ void gemm_nt_kernel(GemmShape g, Epi epi) {
 #pragma unroll
     for (int j = 0; j < kBlocks; ++j) acc.c[i][j] = f32x4{};
 
-  const int nk = g.K / kTileK;
+  const int nk = K / kTileK;
 
   // Operand n (0..15) of a step, in the order the MFMAs consume them:
   // A0, B0..B7, A1..A7.
@@ -215,7 +244,7 @@ void gemm_nt_kernel(GemmShape g, Epi epi) {
   // Load instruction q (0..7) of a step: operand q/4, 16-row group q%4.
   auto issue_load = [&](int kt, int stage, auto q) {
     constexpr int o = decltype(q)::value / 4, r = decltype(q)::value % 4;
-    const int64_t koff = (int64_t)min(kt, nk - 1) * (kTileK * 2);
+    const int64_t koff = (int64_t)max(min(kt, nk - 1), 0) * (kTileK * 2);
     __builtin_amdgcn_global_load_lds(src[o][r] + koff,
                                      (lds_void*)(lds + stage * kLdsStage + wave_lds + o * kLdsOperand +
                                                  r * 16 * kLdsRow),
@@ -258,7 +287,9 @@ void gemm_nt_kernel(GemmShape g, Epi epi) {
   };
 
   // prologue: steps 0 .. kStages-2 in flight; step 0 visible, its operands in
-  // slot 0; then step 1 visible (read during step 0)
+  // slot 0; then step 1 visible (read during step 0).  With nk == 0 (a
+  // device-side K bound of 0) the loads and reads still happen, at K offset 0,
+  // but no MFMA consumes them and the accumulators stay zero.
   for (int s = 0; s < kStages - 1; ++s) issue_loads(s, s);
   stage_barrier<(kStages - 2) * 8>();
   read_frag(0, Const<0>{}, Const<0>{}); read_frag(0, Const<0>{}, Const<1>{});

@@ -99,8 +99,9 @@ struct EpiForward {
 };
 
 // Backward logit gradient for one vocabulary chunk: rows = vocabulary rows
-// v0 + vl (A = W[v0:]), columns = tokens.  Writes bf16 Delta to
-// dT[vl][t] (ldT = Npad) and dN[t][vl] (ldN = Vc); zero outside t < N, v < V.
+// v0 + vl (A = W[v0:]), columns = the compacted tokens that carry gradient
+// (column t is token tok[t], t < *n_dev).  Writes bf16 Delta to dT[vl][t]
+// and dN[t][vl]; zero outside t < *n_dev, v < V.
 // The 256 x 256 bf16 tile goes through LDS once per layout so both global
 // layouts are written as whole 512-byte rows (16 bytes per lane).
 struct EpiDelta {
@@ -112,6 +113,8 @@ struct EpiDelta {
   int64_t ldT;
   uint16_t* dN;
   int64_t ldN;
+  const int32_t* tok;    // column t of the tile is token tok[t] (columns t < *n_dev)
+  const int32_t* n_dev;
 
   // LDS tile: 256 rows x 512 bytes; 16-byte chunk c of row r stored at chunk c ^ (r & 31).
   __device__ static __forceinline__ int tile_off(int row, int col) {
@@ -129,14 +132,16 @@ struct EpiDelta {
 
   __device__ __forceinline__ void apply(AccTile& acc, int tm, int tn, int wm, int wn, int lane, float* smem) const {
     unsigned char* tile = reinterpret_cast<unsigned char*>(smem);
+    const int n = min(N, __builtin_amdgcn_readfirstlane(*n_dev));
     // Delta in place of the logits
 #pragma unroll
     for (int j = 0; j < kBlocks; ++j) {
       const int t = tn * kTileN + acc_col(wn, j, lane);
-      const bool tv = t < N;
-      const float dl = tv ? delta[t] : 0.f;
-      const float ls = tv ? lse[t] : 0.f;
-      const int tgt = tv ? target[t] : -1;
+      const bool tv = t < n;
+      const int to = tv ? tok[t] : 0;
+      const float dl = tv ? delta[to] : 0.f;
+      const float ls = tv ? lse[to] : 0.f;
+      const int tgt = tv ? target[to] : -1;
 #pragma unroll
       for (int i = 0; i < kBlocks; ++i)
 #pragma unroll
@@ -206,28 +211,33 @@ struct EpiDW {
   }
 };
 
-// dH rows = tokens (A = Delta), columns = hidden features (B = W^T[:, v0:]).
+// dH rows = compacted tokens (A = Delta), columns = hidden features
+// (B = W^T[:, v0:]); row t is written to d_hidden row tok[t], t < *n_dev.
 struct EpiDH {
   int N, d;
   float* dH;
   bool first;
+  const int32_t* tok;
+  const int32_t* n_dev;
 
   __device__ __forceinline__ void apply(const AccTile& acc, int tm, int tn, int wm, int wn, int lane, float*) const {
+    const int n = min(N, __builtin_amdgcn_readfirstlane(*n_dev));
 #pragma unroll
-    for (int j = 0; j < kBlocks; ++j) {
-      const int col = tn * kTileN + acc_col(wn, j, lane);
-      if (col >= d) continue;
+    for (int i = 0; i < kBlocks; ++i)
 #pragma unroll
-      for (int i = 0; i < kBlocks; ++i)
+      for (int r = 0; r < kAccPerBlock; ++r) {
+        const int t = tm * kTileM + acc_row(wm, i, r, lane);
+        if (t >= n) continue;
+        float* row = dH + (int64_t)tok[t] * d;
 #pragma unroll
-        for (int r = 0; r < kAccPerBlock; ++r) {
-          const int t = tm * kTileM + acc_row(wm, i, r, lane);
-          if (t < N) {
-            float* p = dH + (int64_t)t * d + col;
+        for (int j = 0; j < kBlocks; ++j) {
+          const int col = tn * kTileN + acc_col(wn, j, lane);
+          if (col < d) {
+            float* p = row + col;
             *p = first ? acc.c[i][j][r] : *p + acc.c[i][j][r];
           }
         }
-    }
+      }
   }
 };
 
@@ -241,15 +251,24 @@ struct EpiDH {
 // i.e. block b is the [cols x chunk] transpose of rows [b*chunk, (b+1)*chunk)
 // with row stride ld >= chunk.  64 x 64 tiles through LDS; cols, chunk and the
 // padded row count are multiples of 64.
+// Optionally, row r of the source is row rmap[r] of `src` and only the first
+// min(rows, *n_dev) rows are present; 64-row blocks wholly past that count are
+// not written (no product reads them).
 __global__ __launch_bounds__(256) void transpose_pad_kernel(const uint16_t* __restrict__ src, int rows, int cols,
                                                             int64_t ld_src, uint16_t* __restrict__ dst,
-                                                            int64_t chunk, int64_t ld) {
+                                                            int64_t chunk, int64_t ld,
+                                                            const int32_t* __restrict__ rmap,
+                                                            const int32_t* __restrict__ n_dev) {
   __shared__ uint16_t tile[64][66];
   const int c0 = blockIdx.x * 64, r0 = blockIdx.y * 64;
   const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+  if (n_dev != nullptr) {
+    rows = min(rows, *n_dev);
+    if (r0 >= (rows + 63) / 64 * 64) return;
+  }
   for (int rr = ty; rr < 64; rr += 4) {
     const int r = r0 + rr;
-    tile[rr][tx] = (r < rows) ? src[(int64_t)r * ld_src + c0 + tx] : (uint16_t)0;
+    tile[rr][tx] = (r < rows) ? src[(int64_t)(rmap ? rmap[r] : r) * ld_src + c0 + tx] : (uint16_t)0;
   }
   __syncthreads();
   const int64_t block = r0 / chunk, rin = r0 % chunk;
@@ -263,6 +282,45 @@ __global__ void fill_f32_kernel(float* __restrict__ p, int64_t n, float v) {
 }
 
 constexpr int kFinThreads = 256;
+constexpr int kCompactThreads = 1024;
+
+// Indices of the tokens whose logit gradient is not identically zero
+// (delta != 0), in increasing order, and their count; the count also goes to
+// stats[4].  One block: each thread owns a contiguous slice of tokens.
+__global__ __launch_bounds__(kCompactThreads) void compact_active_kernel(int N, const float* __restrict__ delta,
+                                                                         int32_t* __restrict__ idx,
+                                                                         int32_t* __restrict__ n_act,
+                                                                         double* __restrict__ stats) {
+  __shared__ int sh[kCompactThreads];
+  const int per = (N + kCompactThreads - 1) / kCompactThreads;
+  const int t0 = min(N, (int)threadIdx.x * per), t1 = min(N, t0 + per);
+  int cnt = 0;
+  for (int t = t0; t < t1; ++t) cnt += delta[t] != 0.f;
+  sh[threadIdx.x] = cnt;
+  __syncthreads();
+  for (int off = 1; off < kCompactThreads; off <<= 1) {
+    const int v = threadIdx.x >= off ? sh[threadIdx.x - off] : 0;
+    __syncthreads();
+    sh[threadIdx.x] += v;
+    __syncthreads();
+  }
+  int pos = sh[threadIdx.x] - cnt;
+  for (int t = t0; t < t1; ++t)
+    if (delta[t] != 0.f) idx[pos++] = t;
+  if (threadIdx.x == kCompactThreads - 1) {
+    *n_act = sh[threadIdx.x];
+    if (stats) stats[4] = (double)sh[threadIdx.x];
+  }
+}
+
+// d_hidden rows of tokens with delta == 0 are exactly zero.
+__global__ __launch_bounds__(256) void zero_inactive_rows_kernel(int d, const float* __restrict__ delta,
+                                                                 float* __restrict__ dH) {
+  const int t = blockIdx.x;
+  if (delta[t] != 0.f) return;
+  f32x4* row = reinterpret_cast<f32x4*>(dH + (int64_t)t * d);
+  for (int c = threadIdx.x; c < d / 4; c += blockDim.x) row[c] = f32x4{0.f, 0.f, 0.f, 0.f};
+}
 
 template <class T>
 __device__ T block_sum(T v, T* sh) {
@@ -374,6 +432,7 @@ __global__ __launch_bounds__(kFinThreads) void reduce_loss_kernel(int nblk, cons
       stats[1] = v[2];
       stats[2] = v[3];
       stats[3] = shd[0];
+      if (nblk == 0) stats[4] = 0.0;   // otherwise written by compact_active_kernel
     }
   }
 }
@@ -390,7 +449,8 @@ constexpr int64_t kStridePad = 64;
 struct Plan {
   int64_t Npad, Vpad, Vc, ntv, nfin;
   int64_t ldH, ldW, ldN, ldT;   // row strides of H^T, W^T blocks, Delta [t][v], Delta^T [v][t]
-  int64_t off_pm, off_pl, off_zt, off_lse, off_delta, off_blk, off_ht, off_wt, off_dn, off_dt, total;
+  int64_t off_pm, off_pl, off_zt, off_lse, off_delta, off_idx, off_nact, off_blk, off_ht, off_wt, off_dn, off_dt,
+      total;
 };
 
 Plan make_plan(int64_t N, int64_t d, int64_t V) {
@@ -415,6 +475,8 @@ Plan make_plan(int64_t N, int64_t d, int64_t V) {
   p.off_zt = take(p.Npad * 4);
   p.off_lse = take(p.Npad * 4);
   p.off_delta = take(p.Npad * 4);
+  p.off_idx = take(p.Npad * 4);
+  p.off_nact = take(4);
   p.off_blk = take((p.nfin > 0 ? p.nfin : 1) * 5 * 8);
   p.off_ht = take(d * p.ldH * 2);
   p.off_wt = take(d * ((p.Vpad + p.Vc - 1) / p.Vc) * p.ldW * 2);   // [V/Vc][d][ldW] blocks
@@ -498,6 +560,8 @@ int pspo_loss_fwd_bwd(const uint16_t* hidden, const uint16_t* w_head, const int3
   float* zt = reinterpret_cast<float*>(ws + pl.off_zt);
   float* lse = reinterpret_cast<float*>(ws + pl.off_lse);
   float* delta = reinterpret_cast<float*>(ws + pl.off_delta);
+  int32_t* act_idx = reinterpret_cast<int32_t*>(ws + pl.off_idx);
+  int32_t* n_act = reinterpret_cast<int32_t*>(ws + pl.off_nact);
   double* blk = reinterpret_cast<double*>(ws + pl.off_blk);
   uint16_t* hT = reinterpret_cast<uint16_t*>(ws + pl.off_ht);
   uint16_t* wT = reinterpret_cast<uint16_t*>(ws + pl.off_wt);
@@ -522,30 +586,39 @@ int pspo_loss_fwd_bwd(const uint16_t* hidden, const uint16_t* w_head, const int3
   hipLaunchKernelGGL(reduce_loss_kernel, dim3(1), dim3(kFinThreads), 0, stream, (int)pl.nfin, blk, loss_scale,
                      loss, stats);
   PSPO_HIP_CHECK(hipGetLastError());
-  // 3. K-contiguous copies for the gradient products
+  // 3. the backward runs over the tokens with delta != 0 only (every other
+  //    token has a zero logit-gradient row: zero d_hidden row, no dW term)
+  hipLaunchKernelGGL(compact_active_kernel, dim3(1), dim3(kCompactThreads), 0, stream, N, delta, act_idx, n_act,
+                     stats);
+  PSPO_HIP_CHECK(hipGetLastError());
+  hipLaunchKernelGGL(zero_inactive_rows_kernel, dim3((unsigned)N), dim3(256), 0, stream, d, delta, d_hidden);
+  PSPO_HIP_CHECK(hipGetLastError());
+  // 4. K-contiguous copies for the gradient products
   hipLaunchKernelGGL(transpose_pad_kernel, dim3(d / 64, (unsigned)(pl.Npad / 64)), dim3(256), 0, stream, hidden, N,
-                     d, (int64_t)d, hT, pl.Npad, pl.ldH);   // one block: H^T [d x Npad]
+                     d, (int64_t)d, hT, pl.Npad, pl.ldH, act_idx, n_act);   // H[active]^T [d x Npad]
   PSPO_HIP_CHECK(hipGetLastError());
   hipLaunchKernelGGL(transpose_pad_kernel, dim3(d / 64, (unsigned)(pl.Vpad / 64)), dim3(256), 0, stream, w_head, V,
-                     d, (int64_t)d, wT, pl.Vc, pl.ldW);     // per vocabulary chunk: W[chunk]^T [d x Vc]
+                     d, (int64_t)d, wT, pl.Vc, pl.ldW, nullptr, nullptr);  // per chunk: W[chunk]^T [d x Vc]
   PSPO_HIP_CHECK(hipGetLastError());
-  // 4. backward, one vocabulary chunk at a time
+  // 5. backward, one vocabulary chunk at a time; every product is bounded by
+  //    the active-token count in device memory
   for (int64_t v0 = 0; v0 < pl.Vpad; v0 += pl.Vc) {
     const int64_t vc = (pl.Vpad - v0) < pl.Vc ? (pl.Vpad - v0) : pl.Vc;
     const int ctiles = (int)(vc / kTileM);
     {
-      GemmShape g{w_head + v0 * d, d, (int)(V - v0), hidden, d, N, d, ctiles, tiles_tok};
-      EpiDelta e{V, N, (int)v0, target, lse, delta, dT, pl.ldT, dN, pl.ldN};
+      GemmShape g{w_head + v0 * d, d, (int)(V - v0), hidden, d, N, d, ctiles, tiles_tok, act_idx, n_act, kDynN};
+      EpiDelta e{V, N, (int)v0, target, lse, delta, dT, pl.ldT, dN, pl.ldN, act_idx, n_act};
       if (int rc = launch_gemm(g, e, stream)) return rc;
     }
     {
-      GemmShape g{dT, pl.ldT, (int)vc, hT, pl.ldH, d, (int)pl.Npad, ctiles, tiles_d};
+      GemmShape g{dT, pl.ldT, (int)vc, hT, pl.ldH, d, (int)pl.Npad, ctiles, tiles_d, nullptr, n_act, kDynK};
       EpiDW e{V, d, (int)v0, d_w_head, accumulate};
       if (int rc = launch_gemm(g, e, stream)) return rc;
     }
     {
-      GemmShape g{dN, pl.ldN, (int)pl.Npad, wT + (v0 / pl.Vc) * d * pl.ldW, pl.ldW, d, (int)vc, tiles_tok, tiles_d};
-      EpiDH e{N, d, d_hidden, v0 == 0};
+      GemmShape g{dN,       pl.ldN,   (int)pl.Npad, wT + (v0 / pl.Vc) * d * pl.ldW, pl.ldW, d, (int)vc, tiles_tok,
+                  tiles_d, nullptr, n_act, kDynM};
+      EpiDH e{N, d, d_hidden, v0 == 0, act_idx, n_act};
       if (int rc = launch_gemm(g, e, stream)) return rc;
     }
   }

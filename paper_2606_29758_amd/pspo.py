@@ -190,7 +190,7 @@ def loss_fwd_bwd(hidden, w_head, target, logp_old, weight, seq_id, advantage, N:
     _dev(d_hidden, torch.float32, "d_hidden")
     loss = torch.empty(1, dtype=torch.float64, device=dev)
     logp = torch.empty(max(N, 1), dtype=torch.float32, device=dev) if want_logp else None
-    stats = torch.empty(4, dtype=torch.float64, device=dev) if want_stats else None
+    stats = torch.empty(5, dtype=torch.float64, device=dev) if want_stats else None
     need = loss_workspace_bytes(N, d, V, flags)
     if workspace is None:
         workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=dev)

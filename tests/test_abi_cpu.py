@@ -36,7 +36,7 @@ def test_exports_every_declared_symbol(lib):
 
 
 def test_version_and_status_strings(lib):
-    assert lib.pspo_abi_version() == 1
+    assert lib.pspo_abi_version() == 2
     assert lib.pspo_status_string(0) == b"PSPO_OK"
     assert lib.pspo_status_string(3) == b"PSPO_ERR_WORKSPACE"
     assert lib.pspo_status_string(99) == b"PSPO_ERR_UNKNOWN"

@@ -7,6 +7,8 @@ Small workloads are compared element by element; the full-size workloads
 (in the launch configuration the benchmark times) are compared on sampled
 tokens the oracle computes one by one, plus identities that hold at any size.
 """
+import dataclasses
+
 import numpy as np
 import pytest
 import torch
@@ -129,6 +131,8 @@ def test_loss_parity(name, seed):
     assert int(st[1]) == int(np.sum((A != 0) & (ref["mu"] == 0)))
     assert int(st[2]) == int(np.sum(A == 0))
     assert st[3] == float(pk["weight"].max())
+    # the backward ran over exactly the tokens with a nonzero logit-gradient row
+    assert int(st[4]) == int(np.sum(ref["delta"] != 0))
     assert int(out["pack"]["n_tokens"].item()) == pk["n_tokens"]
 
 
@@ -172,6 +176,22 @@ def test_zero_advantage():
     assert float(out["loss"].item()) == 0.0
     assert not torch.any(out["d_hidden"]) and not torch.any(out["d_w_head"])
     assert int(out["stats"][2].item()) == out["N"]
+    assert int(out["stats"][4].item()) == 0   # no token enters the backward products
+
+
+def test_all_tokens_active():
+    """No clipping and no zero advantage: every token enters the backward."""
+    wl, lp = _workload("tiny")
+    cfg = dataclasses.replace(wl.cfg, eps_low=0.9, eps_high=0.9)
+    adv = np.where(wl.advantage >= 0, 1.0, -1.0).astype(wl.advantage.dtype)
+    wl1 = synth.Workload(**{**wl.__dict__, "cfg": cfg, "advantage": adv})
+    out = pipeline.Step(pipeline.upload(wl1, lp))(seed=4)
+    torch.cuda.synchronize()
+    H, pk = oracle_sample_pack(wl1, lp, 4)
+    ref = oracle_loss(wl1, pk)
+    assert np.all(ref["delta"] != 0)
+    assert int(out["stats"][4].item()) == out["N"] == pk["n_tokens"]
+    _compare_loss(out, ref)
 
 
 def test_device_error_flags():
