@@ -3,7 +3,9 @@
 A step is one pass of the whole hot path over one batch of synthetic rollouts
 already resident in HBM: Philox cutoff sampling, prefix packing (with the
 hidden-row gather), the 4-byte read of the packed token count, and the fused
-LM-head + prefix-weighted PPO loss forward and backward (dHidden, dW).
+LM-head + prefix-weighted PPO loss forward and backward (loss, dHidden, dW;
+per-token log-probs are not requested, so the forward skips the tokens of
+zero-advantage completions, whose loss terms and gradients are exactly zero).
 
 Workload: the 7B-shaped batch (Qwen2.5-Math-7B head dims d = 3584,
 V = 152064; 8 prompts x 8 rollouts; lengths lognormal around 2048, clipped
@@ -12,9 +14,11 @@ old log-probs = new + N(0, 0.1^2)).
 
 Prints one JSON line.  `roofline` covers the loss call (the forward, logit-
 gradient, dW and dH matrix-core kernels it launches), timed with HIP events
-on the stream it runs on: achieved = (2 N + 4 n_bwd) V d algorithmic flops /
-mean call duration, where n_bwd counts the tokens whose logit gradient is not
-identically zero (the others add nothing to dH or dW and are skipped).
+on the stream it runs on: achieved = (2 n_fwd + 4 n_bwd) V d algorithmic
+flops / mean call duration, where n_fwd counts the tokens of completions with a
+nonzero advantage (the only ones whose loss term can be nonzero) and n_bwd the
+tokens whose logit gradient is not identically zero (the others add nothing to
+dH or dW); the kernels skip the rest.
 `dense_equivalent_tflops` is 6 N V d / duration, the rate a path that ran the
 gradient products over every token would need for the same throughput.  `cpu_baseline` times the float64 CPU oracle on a bounded sample of
 the same step (all cutoffs and packing, then the loss of the first
@@ -119,7 +123,7 @@ def main():
     stream = torch.cuda.current_stream()
     ev = lambda: torch.cuda.Event(enable_timing=True)
     for _ in range(args.warmup):
-        step(args.seed)
+        step(args.seed, want_logp=False)
     torch.cuda.synchronize()
 
     loss_ms = []
@@ -133,7 +137,7 @@ def main():
         N = int(pk["n_tokens"].item())
         s, e = ev(), ev()
         s.record(stream)
-        out = step.loss(pk, N)
+        out = step.loss(pk, N, want_logp=False)
         e.record(stream)
         starts.append(s)
         ends.append(e)
@@ -143,12 +147,14 @@ def main():
     loss_ms = [s.elapsed_time(e) for s, e in zip(starts, ends)]
     loss_avg = float(np.mean(loss_ms))
     assert int(step.err.item()) == 0, "device error flag raised"
-    n_bwd = int(out["stats"][4].item())   # tokens with a nonzero logit-gradient row
+    st = out["stats"].cpu().numpy()
+    n_fwd = N - int(st[2])   # tokens of completions with A != 0: the forward's columns
+    n_bwd = int(st[4])       # tokens with a nonzero logit-gradient row
 
-    # matrix-core work the step needs: the forward over all N tokens (2 N V d),
-    # dH and dW over the n_bwd tokens whose logit gradient is not zero (4 n_bwd V d;
-    # every other token contributes exactly zero to both)
-    flops = (2.0 * N + 4.0 * n_bwd) * cfg.V * cfg.d
+    # matrix-core work the step needs: the forward over the n_fwd tokens whose loss
+    # term can be nonzero (2 n_fwd V d), dH and dW over the n_bwd tokens whose logit
+    # gradient is not zero (4 n_bwd V d); every other token contributes exactly zero
+    flops = (2.0 * n_fwd + 4.0 * n_bwd) * cfg.V * cfg.d
     achieved = flops / (loss_avg * 1e-3) / 1e12
     dense_equiv = 6.0 * N * cfg.V * cfg.d / (loss_avg * 1e-3) / 1e12
     # HBM bytes per call from the committed counter runs, only while the kernels
@@ -179,6 +185,7 @@ def main():
                         f"{' (pinned to full length)' if cfg.full_trajectory else ''}, "
                         f"logp_old noise sigma {cfg.sigma_lp}",
             "prefix_tokens": N,
+            "forward_tokens": n_fwd,
             "backward_tokens": n_bwd,
             "total_tokens": int(wl.total_tokens),
             "kept_fraction": N / wl.total_tokens,
@@ -191,8 +198,8 @@ def main():
         "roofline": {
             "bound": "mfma",
             "kernel": "pspo_loss_fwd_bwd (forward, logit-gradient, dW and dH bf16 MFMA kernels)",
-            "flops": "(2 N + 4 n_bwd) V d per call: forward over all prefix tokens, dH and dW over "
-                     "the tokens with a nonzero logit gradient",
+            "flops": "(2 n_fwd + 4 n_bwd) V d per call: forward over the tokens of completions with "
+                     "A != 0, dH and dW over the tokens with a nonzero logit gradient",
             "achieved": achieved,
             "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s",

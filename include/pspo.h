@@ -175,7 +175,10 @@ size_t pspo_loss_workspace_bytes(int32_t N, int32_t d, int32_t V, uint32_t flags
  *  loss       device, float64 [1] out.
  *  d_hidden   device, float32 [N, d] out.
  *  d_w_head   device, float32 [V, d] out (or accumulated, see flags).
- *  logp_new   device, float32 [N] out, or NULL.
+ *  logp_new   device, float32 [N] out, or NULL.  When NULL, the forward
+ *             computes logits only for the tokens of completions with A != 0:
+ *             a zero advantage makes a token's loss term and gradient exactly
+ *             zero, and every other output is unchanged (bitwise).
  *  stats      device, float64 [5] out, or NULL: { loss_scale * sum_i |c_i s_i|,
  *             #tokens with A != 0 and mu = 0 (clipped), #tokens with A == 0,
  *             max_i c_i, #tokens with delta_i != 0 }.  Only the last group

@@ -35,7 +35,9 @@ constexpr float kNegInf = -INFINITY;
 // Epilogues
 // ---------------------------------------------------------------------------
 
-// Forward: rows = vocabulary (A = W), columns = tokens (B = H).
+// Forward: rows = vocabulary (A = W), columns = the tokens whose logits are
+// needed (B = H rows gathered through tok); writes per-column softmax
+// partials of each 256-row vocabulary tile and the target logit.
 struct EpiForward {
   int V, N;
   int64_t ldp;  // stride between vocabulary tiles in the partial arrays (= Npad)
@@ -43,14 +45,17 @@ struct EpiForward {
   float* part_m;
   float* part_l;
   float* zt;
+  const int32_t* tok;    // column t is token tok[t] (columns t < *n_dev)
+  const int32_t* n_dev;
 
   __device__ __forceinline__ void apply(const AccTile& acc, int tm, int tn, int wm, int wn, int lane, float* smem) const {
     float* red = smem;  // [2 wave rows][256 columns][m, l]
+    const int n = min(N, __builtin_amdgcn_readfirstlane(*n_dev));
 #pragma unroll
     for (int j = 0; j < kBlocks; ++j) {
       const int cl = acc_col(wn, j, lane);
       const int t = tn * kTileN + cl;
-      const int tgt = (t < N) ? target[t] : -1;
+      const int tgt = (t < n) ? target[tok[t]] : -1;
       float m = kNegInf;
 #pragma unroll
       for (int i = 0; i < kBlocks; ++i)
@@ -91,7 +96,7 @@ struct EpiForward {
     if (m0 != kNegInf) L += l0 * __expf(m0 - M);
     if (m1 != kNegInf) L += l1 * __expf(m1 - M);
     const int t = tn * kTileN + c;
-    if (t < N) {
+    if (t < n) {
       part_m[tm * ldp + t] = M;
       part_l[tm * ldp + t] = L;
     }
@@ -284,18 +289,17 @@ __global__ void fill_f32_kernel(float* __restrict__ p, int64_t n, float v) {
 constexpr int kFinThreads = 256;
 constexpr int kCompactThreads = 1024;
 
-// Indices of the tokens whose logit gradient is not identically zero
-// (delta != 0), in increasing order, and their count; the count also goes to
-// stats[4].  One block: each thread owns a contiguous slice of tokens.
-__global__ __launch_bounds__(kCompactThreads) void compact_active_kernel(int N, const float* __restrict__ delta,
-                                                                         int32_t* __restrict__ idx,
-                                                                         int32_t* __restrict__ n_act,
-                                                                         double* __restrict__ stats) {
+// Order-preserving compaction of the tokens t < N with keep(t), by one block
+// (each thread owns a contiguous slice): idx[0 .. count) are their indices in
+// increasing order; pos[t] (if pos is not NULL) is t's place in idx, or -1.
+// Returns the count in every thread.
+template <class Keep>
+__device__ int compact_tokens(int N, Keep keep, int32_t* __restrict__ idx, int32_t* __restrict__ pos) {
   __shared__ int sh[kCompactThreads];
   const int per = (N + kCompactThreads - 1) / kCompactThreads;
   const int t0 = min(N, (int)threadIdx.x * per), t1 = min(N, t0 + per);
   int cnt = 0;
-  for (int t = t0; t < t1; ++t) cnt += delta[t] != 0.f;
+  for (int t = t0; t < t1; ++t) cnt += keep(t) ? 1 : 0;
   sh[threadIdx.x] = cnt;
   __syncthreads();
   for (int off = 1; off < kCompactThreads; off <<= 1) {
@@ -304,12 +308,47 @@ __global__ __launch_bounds__(kCompactThreads) void compact_active_kernel(int N, 
     sh[threadIdx.x] += v;
     __syncthreads();
   }
-  int pos = sh[threadIdx.x] - cnt;
-  for (int t = t0; t < t1; ++t)
-    if (delta[t] != 0.f) idx[pos++] = t;
-  if (threadIdx.x == kCompactThreads - 1) {
-    *n_act = sh[threadIdx.x];
-    if (stats) stats[4] = (double)sh[threadIdx.x];
+  int p = sh[threadIdx.x] - cnt;
+  for (int t = t0; t < t1; ++t) {
+    const bool k = keep(t);
+    if (k) idx[p] = t;
+    if (pos) pos[t] = k ? p : -1;
+    p += k ? 1 : 0;
+  }
+  return sh[kCompactThreads - 1];
+}
+
+// Tokens whose logits the forward computes: all of them when every token's
+// log-prob is wanted, else those of completions with A != 0 (a zero advantage
+// makes the token's loss term and gradient exactly zero, so its logits are
+// not needed; a token with an invalid completion id is left to finalize,
+// which flags it).
+__global__ __launch_bounds__(kCompactThreads) void compact_forward_kernel(int N, int R, int all,
+                                                                          const int32_t* __restrict__ seq_id,
+                                                                          const float* __restrict__ adv,
+                                                                          int32_t* __restrict__ idx,
+                                                                          int32_t* __restrict__ pos,
+                                                                          int32_t* __restrict__ count) {
+  auto keep = [&](int t) {
+    if (all) return true;
+    const int s = seq_id[t];
+    return s >= 0 && s < R && adv[s] != 0.f;
+  };
+  const int n = compact_tokens(N, keep, idx, pos);
+  if (threadIdx.x == 0) *count = n;
+}
+
+// Tokens whose logit gradient is not identically zero (delta != 0): the
+// backward products run over these only.  The count also goes to stats[4].
+__global__ __launch_bounds__(kCompactThreads) void compact_active_kernel(int N, const float* __restrict__ delta,
+                                                                         int32_t* __restrict__ idx,
+                                                                         int32_t* __restrict__ n_act,
+                                                                         double* __restrict__ stats) {
+  auto keep = [&](int t) { return delta[t] != 0.f; };
+  const int n = compact_tokens(N, keep, idx, nullptr);
+  if (threadIdx.x == 0) {
+    *n_act = n;
+    if (stats) stats[4] = (double)n;
   }
 }
 
@@ -351,7 +390,8 @@ __device__ float block_max(float v, float* sh) {
 // Each block writes (sum c s, sum |c s|, #clipped, #A==0) and max c to blk[5*b].
 __global__ __launch_bounds__(kFinThreads) void finalize_kernel(
     int N, int V, int R, int ntv, int64_t ldp, const float* __restrict__ part_m, const float* __restrict__ part_l,
-    const float* __restrict__ zt, const int32_t* __restrict__ target, const float* __restrict__ logp_old,
+    const float* __restrict__ zt, const int32_t* __restrict__ fwd_pos, const int32_t* __restrict__ target,
+    const float* __restrict__ logp_old,
     const float* __restrict__ weight, const int32_t* __restrict__ seq_id, const float* __restrict__ adv,
     float eps_low, float eps_high, float loss_scale, float* __restrict__ lse_out, float* __restrict__ delta_out,
     float* __restrict__ logp_new, double* __restrict__ blk, int32_t* __restrict__ err_flag) {
@@ -361,11 +401,16 @@ __global__ __launch_bounds__(kFinThreads) void finalize_kernel(
   double cs = 0.0, acs = 0.0, nclip = 0.0, nzero = 0.0;
   float maxw = 0.f;
   if (t < N) {
-    float M = kNegInf;
-    for (int k = 0; k < ntv; ++k) M = fmaxf(M, part_m[k * ldp + t]);
-    float L = 0.f;
-    for (int k = 0; k < ntv; ++k) L += part_l[k * ldp + t] * __expf(part_m[k * ldp + t] - M);
-    const float lse = M + logf(L);
+    // column of this token's forward partials; -1: its logits were not needed
+    const int col = fwd_pos[t];
+    float lse = NAN;
+    if (col >= 0) {
+      float M = kNegInf;
+      for (int k = 0; k < ntv; ++k) M = fmaxf(M, part_m[k * ldp + col]);
+      float L = 0.f;
+      for (int k = 0; k < ntv; ++k) L += part_l[k * ldp + col] * __expf(part_m[k * ldp + col] - M);
+      lse = M + logf(L);
+    }
     const int tgt = target[t];
     const int seq = seq_id[t];
     const bool valid = tgt >= 0 && tgt < V && seq >= 0 && seq < R;
@@ -373,16 +418,17 @@ __global__ __launch_bounds__(kFinThreads) void finalize_kernel(
     const float c = weight[t];
     float l = NAN, s = 0.f, dl = 0.f;
     bool mu = false;
-    if (valid) {
-      l = zt[t] - lse;
+    if (valid && col >= 0) {
+      l = zt[col] - lse;
       const float rho = expf(l - logp_old[t]);
       const float clipped = fminf(fmaxf(rho, 1.f - eps_low), 1.f + eps_high);
       s = fminf(rho * A, clipped * A);
       mu = (A > 0.f && rho <= 1.f + eps_high) || (A < 0.f && rho >= 1.f - eps_low);
       dl = mu ? -loss_scale * c * rho * A : 0.f;
-    } else if (err_flag) {
+    } else if (!valid && err_flag) {
       atomicOr(err_flag, (tgt >= 0 && tgt < V) ? PSPO_DEVERR_SEQ_ID : PSPO_DEVERR_TARGET);
     }
+    // (a valid token without forward partials has A == 0: zero loss term and gradient)
     lse_out[t] = lse;
     delta_out[t] = dl;
     if (logp_new) logp_new[t] = l;
@@ -449,8 +495,8 @@ constexpr int64_t kStridePad = 64;
 struct Plan {
   int64_t Npad, Vpad, Vc, ntv, nfin;
   int64_t ldH, ldW, ldN, ldT;   // row strides of H^T, W^T blocks, Delta [t][v], Delta^T [v][t]
-  int64_t off_pm, off_pl, off_zt, off_lse, off_delta, off_idx, off_nact, off_blk, off_ht, off_wt, off_dn, off_dt,
-      total;
+  int64_t off_pm, off_pl, off_zt, off_lse, off_delta, off_fidx, off_fpos, off_nfwd, off_idx, off_nact, off_blk, off_ht,
+      off_wt, off_dn, off_dt, total;
 };
 
 Plan make_plan(int64_t N, int64_t d, int64_t V) {
@@ -475,6 +521,9 @@ Plan make_plan(int64_t N, int64_t d, int64_t V) {
   p.off_zt = take(p.Npad * 4);
   p.off_lse = take(p.Npad * 4);
   p.off_delta = take(p.Npad * 4);
+  p.off_fidx = take(p.Npad * 4);
+  p.off_fpos = take(p.Npad * 4);
+  p.off_nfwd = take(4);
   p.off_idx = take(p.Npad * 4);
   p.off_nact = take(4);
   p.off_blk = take((p.nfin > 0 ? p.nfin : 1) * 5 * 8);
@@ -560,6 +609,9 @@ int pspo_loss_fwd_bwd(const uint16_t* hidden, const uint16_t* w_head, const int3
   float* zt = reinterpret_cast<float*>(ws + pl.off_zt);
   float* lse = reinterpret_cast<float*>(ws + pl.off_lse);
   float* delta = reinterpret_cast<float*>(ws + pl.off_delta);
+  int32_t* fwd_idx = reinterpret_cast<int32_t*>(ws + pl.off_fidx);
+  int32_t* fwd_pos = reinterpret_cast<int32_t*>(ws + pl.off_fpos);
+  int32_t* n_fwd = reinterpret_cast<int32_t*>(ws + pl.off_nfwd);
   int32_t* act_idx = reinterpret_cast<int32_t*>(ws + pl.off_idx);
   int32_t* n_act = reinterpret_cast<int32_t*>(ws + pl.off_nact);
   double* blk = reinterpret_cast<double*>(ws + pl.off_blk);
@@ -572,35 +624,39 @@ int pspo_loss_fwd_bwd(const uint16_t* hidden, const uint16_t* w_head, const int3
   const int tiles_voc = (int)(pl.ntv);
   const int tiles_d = (d + kTileN - 1) / kTileN;
 
-  // 1. forward logits -> per-tile softmax partials and target logits
+  // 1. the tokens whose logits are needed (all of them if logp_new is wanted)
+  hipLaunchKernelGGL(compact_forward_kernel, dim3(1), dim3(kCompactThreads), 0, stream, N, R,
+                     logp_new != nullptr ? 1 : 0, seq_id, advantage, fwd_idx, fwd_pos, n_fwd);
+  PSPO_HIP_CHECK(hipGetLastError());
+  // 2. forward logits -> per-tile softmax partials and target logits
   {
-    GemmShape g{w_head, d, V, hidden, d, N, d, tiles_voc, tiles_tok};
-    EpiForward e{V, N, pl.Npad, target, part_m, part_l, zt};
+    GemmShape g{w_head, d, V, hidden, d, N, d, tiles_voc, tiles_tok, fwd_idx, n_fwd, kDynN};
+    EpiForward e{V, N, pl.Npad, target, part_m, part_l, zt, fwd_idx, n_fwd};
     if (int rc = launch_gemm(g, e, stream)) return rc;
   }
-  // 2. lse, PPO terms, delta, loss
+  // 3. lse, PPO terms, delta, loss
   hipLaunchKernelGGL(finalize_kernel, dim3((unsigned)pl.nfin), dim3(kFinThreads), 0, stream, N, V, R, tiles_voc,
-                     pl.Npad, part_m, part_l, zt, target, logp_old, weight, seq_id, advantage, eps_low, eps_high,
-                     loss_scale, lse, delta, logp_new, blk, err_flag);
+                     pl.Npad, part_m, part_l, zt, fwd_pos, target, logp_old, weight, seq_id, advantage, eps_low,
+                     eps_high, loss_scale, lse, delta, logp_new, blk, err_flag);
   PSPO_HIP_CHECK(hipGetLastError());
   hipLaunchKernelGGL(reduce_loss_kernel, dim3(1), dim3(kFinThreads), 0, stream, (int)pl.nfin, blk, loss_scale,
                      loss, stats);
   PSPO_HIP_CHECK(hipGetLastError());
-  // 3. the backward runs over the tokens with delta != 0 only (every other
+  // 4. the backward runs over the tokens with delta != 0 only (every other
   //    token has a zero logit-gradient row: zero d_hidden row, no dW term)
   hipLaunchKernelGGL(compact_active_kernel, dim3(1), dim3(kCompactThreads), 0, stream, N, delta, act_idx, n_act,
                      stats);
   PSPO_HIP_CHECK(hipGetLastError());
   hipLaunchKernelGGL(zero_inactive_rows_kernel, dim3((unsigned)N), dim3(256), 0, stream, d, delta, d_hidden);
   PSPO_HIP_CHECK(hipGetLastError());
-  // 4. K-contiguous copies for the gradient products
+  // 5. K-contiguous copies for the gradient products
   hipLaunchKernelGGL(transpose_pad_kernel, dim3(d / 64, (unsigned)(pl.Npad / 64)), dim3(256), 0, stream, hidden, N,
                      d, (int64_t)d, hT, pl.Npad, pl.ldH, act_idx, n_act);   // H[active]^T [d x Npad]
   PSPO_HIP_CHECK(hipGetLastError());
   hipLaunchKernelGGL(transpose_pad_kernel, dim3(d / 64, (unsigned)(pl.Vpad / 64)), dim3(256), 0, stream, w_head, V,
                      d, (int64_t)d, wT, pl.Vc, pl.ldW, nullptr, nullptr);  // per chunk: W[chunk]^T [d x Vc]
   PSPO_HIP_CHECK(hipGetLastError());
-  // 5. backward, one vocabulary chunk at a time; every product is bounded by
+  // 6. backward, one vocabulary chunk at a time; every product is bounded by
   //    the active-token count in device memory
   for (int64_t v0 = 0; v0 < pl.Vpad; v0 += pl.Vc) {
     const int64_t vc = (pl.Vpad - v0) < pl.Vc ? (pl.Vpad - v0) : pl.Vc;

@@ -70,17 +70,19 @@ class Step:
                                   target_full=dw.target_full, logp_old_full=dw.logp_old_full,
                                   hidden_full=dw.hidden_full, err_flag=self.err)
 
-    def loss(self, pk: dict, N: int, flags: int = 0) -> dict:
+    def loss(self, pk: dict, N: int, flags: int = 0, want_logp: bool = True) -> dict:
+        """want_logp=False: no per-token log-probs, and the forward skips the tokens of
+        zero-advantage completions (their loss terms and gradients are exactly zero)."""
         dw = self.dw
         return pspo.loss_fwd_bwd(pk["hidden"], dw.w_head, pk["target"], pk["logp_old"], pk["weight"],
                                  pk["seq_id"], dw.advantage, N, dw.eps_low, dw.eps_high, dw.loss_scale,
                                  flags=flags, d_w_head=self.d_w, d_hidden=self.d_h,
-                                 workspace=self.workspace, err_flag=self.err)
+                                 workspace=self.workspace, err_flag=self.err, want_logp=want_logp)
 
-    def __call__(self, seed: int, offset: int = 0, flags: int = 0) -> dict:
+    def __call__(self, seed: int, offset: int = 0, flags: int = 0, want_logp: bool = True) -> dict:
         pk = self.sample_and_pack(seed, offset)
         N = int(pk["n_tokens"].item())   # the one host sync of a step
-        out = self.loss(pk, N, flags)
+        out = self.loss(pk, N, flags, want_logp)
         out["pack"] = pk
         out["N"] = N
         out["cutoffs"] = self.cutoffs

@@ -17,7 +17,8 @@ the implementation appendix; none of that data is reproduced):
   every xi_t > 0 as Sec. 3.2 requires.  The full-trajectory control uses
   xi == 1;
 * binary rewards R_r and the broadcast critic-free advantage A_r = R_r - mean
-  of the group's rewards (Sec. 3.1, broadcast advantage with a group-mean
+  of the group's rewards, optionally divided by the group's std (GRPO-style
+  normalisation, one of the paper's baselines) (Sec. 3.1, broadcast advantage with a group-mean
   baseline);
 * target token ids o_t, uniform over the vocabulary;
 * Gaussian noise eps_t ~ N(0, sigma_lp^2) per token, from which the caller
@@ -58,6 +59,9 @@ class SynthConfig:
     w_std: float = 0.02
     eps_low: float = 0.1
     eps_high: float = 0.1
+    # "mean": A = R - group mean (the broadcast critic-free advantage);
+    # "std": additionally divided by the group's population std + 1e-6 (GRPO)
+    adv_norm: str = "mean"
 
     @property
     def R(self) -> int:
@@ -232,7 +236,12 @@ def make_workload(cfg, with_matrices: bool = True) -> Workload:
     else:
         raise ValueError(rl)
     grp = rewards.reshape(P, K)
-    advantage = (grp - grp.mean(axis=1, keepdims=True)).reshape(R).astype(np.float32)
+    centred = grp - grp.mean(axis=1, keepdims=True)
+    if cfg.adv_norm == "std":
+        centred = centred / (grp.std(axis=1, keepdims=True) + 1e-6)
+    elif cfg.adv_norm != "mean":
+        raise ValueError(cfg.adv_norm)
+    advantage = centred.reshape(R).astype(np.float32)
 
     S = int(lengths.sum())
     target_full = g_tgt.integers(0, cfg.V, size=S).astype(np.int32)

@@ -136,6 +136,55 @@ def test_loss_parity(name, seed):
     assert int(out["pack"]["n_tokens"].item()) == pk["n_tokens"]
 
 
+@pytest.mark.parametrize("name,eps_low,eps_high,adv_norm", [("mini7b", 0.2, 0.28, "mean"),
+                                                            ("tiny", 0.1, 0.1, "std"),
+                                                            ("mini1p5b", 0.2, 0.28, "std")])
+def test_loss_variants(name, eps_low, eps_high, adv_norm):
+    """Loss variants of the paper's baselines as parameters: asymmetric clip range
+    (clip-higher) and std-normalised group advantages."""
+    wl, lp = _workload(name)
+    cfg = dataclasses.replace(wl.cfg, eps_low=eps_low, eps_high=eps_high, adv_norm=adv_norm)
+    adv = synth.make_workload(cfg, with_matrices=False).advantage
+    wl1 = synth.Workload(**{**wl.__dict__, "cfg": cfg, "advantage": adv})
+    out = pipeline.Step(pipeline.upload(wl1, lp))(seed=5)
+    torch.cuda.synchronize()
+    H, pk = oracle_sample_pack(wl1, lp, 5)
+    _check_pack(out, H, pk)
+    ref = oracle_loss(wl1, pk)
+    assert not ambiguous_clip(ref, eps_low, eps_high).any()
+    _compare_loss(out, ref)
+    A = adv[pk["seq_id"]]
+    st = _to_np(out["stats"])
+    assert int(st[1]) == int(np.sum((A != 0) & (ref["mu"] == 0)))
+    assert int(st[4]) == int(np.sum(ref["delta"] != 0))
+
+
+@pytest.mark.parametrize("name", ["tiny", "mini7b"])
+def test_without_logp_is_identical(name):
+    """Without per-token log-probs the forward skips zero-advantage tokens; every other
+    output is bitwise the same, and still matches the oracle."""
+    wl, lp = _workload(name)
+    adv = wl.advantage.copy()
+    adv[:wl.cfg.K] = 0.0      # one group with equal rewards, so that some tokens are skipped
+    wl = synth.Workload(**{**wl.__dict__, "advantage": adv})
+    step = pipeline.Step(pipeline.upload(wl, lp))
+    a = step(seed=6)
+    la, dha, dwa, sa = (a[k].clone() for k in ("loss", "d_hidden", "d_w_head", "stats"))
+    b = step(seed=6, want_logp=False)
+    torch.cuda.synchronize()
+    assert b["logp_new"] is None
+    assert torch.equal(la, b["loss"]) and torch.equal(sa, b["stats"])
+    assert torch.equal(dha, b["d_hidden"]) and torch.equal(dwa, b["d_w_head"])
+    A = wl.advantage[_to_np(a["pack"]["seq_id"][:a["N"]])]
+    assert 0 < np.sum(A == 0) < a["N"]   # the skip is exercised
+    assert int(step.err.item()) == 0
+    H, pk = oracle_sample_pack(wl, lp, 6)
+    ref = oracle_loss(wl, pk)
+    assert abs(float(b["loss"].item()) - ref["loss"]) <= LOSS_RTOL * abs(ref["loss"])
+    assert rel_l2(_to_np(b["d_hidden"]), ref["d_hidden"]) <= GRAD_REL_L2
+    assert rel_l2(_to_np(b["d_w_head"]), ref["d_w"]) <= GRAD_REL_L2
+
+
 def test_deterministic():
     wl, lp = _workload("tiny")
     step = pipeline.Step(pipeline.upload(wl, lp))
@@ -241,9 +290,15 @@ def test_full_size_sampled(name):
     cfg = wl.cfg
     print(f"[{name}] workload ready: {wl.total_tokens} tokens", flush=True)
     dw = pipeline.upload(wl, lp)
-    out = pipeline.Step(dw)(seed=0)
+    step = pipeline.Step(dw)
+    lean = step(seed=0, want_logp=False)    # the benchmark's configuration
+    lean = {k: lean[k].clone() for k in ("loss", "d_hidden", "d_w_head", "stats")}
+    out = step(seed=0)
     torch.cuda.synchronize()
     print(f"[{name}] GPU pass done, N = {out['N']}", flush=True)
+    for k in ("loss", "d_hidden", "d_w_head", "stats"):
+        assert torch.equal(lean[k], out[k]), k
+    del lean
     H, pk = oracle_sample_pack(wl, lp, 0)
     _check_pack(out, H, pk)
     N = pk["n_tokens"]

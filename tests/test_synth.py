@@ -1,4 +1,5 @@
 """Checks of the seeded workload generator against independent definitions."""
+import dataclasses
 import numpy as np
 import pytest
 import torch
@@ -34,6 +35,23 @@ def test_advantage_is_group_mean_centred():
     ref = ppo_head.advantages(wl.rewards, wl.cfg.K)
     assert np.array_equal(wl.advantage, ref.astype(np.float32))
     assert np.allclose(wl.advantage.reshape(-1, wl.cfg.K).sum(axis=1), 0.0, atol=1e-6)
+
+
+def test_std_normalised_advantage():
+    """GRPO-style advantages: each group with unequal rewards has mean 0 and population
+    variance 1 (up to the 1e-6 guard); groups with equal rewards get A = 0."""
+    cfg = dataclasses.replace(synth.CONFIGS["qwen1.5b"], adv_norm="std")
+    wl = synth.make_workload(cfg, with_matrices=False)
+    ref = ppo_head.advantages(wl.rewards, cfg.K, std_normalise=True)
+    assert np.array_equal(wl.advantage, ref.astype(np.float32))
+    g = ref.reshape(-1, cfg.K)
+    r = wl.rewards.reshape(-1, cfg.K)
+    const = (r == r[:, :1]).all(axis=1)
+    assert const.any() and (~const).any()
+    assert np.all(g[const] == 0)
+    assert np.allclose(g[~const].mean(axis=1), 0, atol=1e-12)
+    sd = r[~const].std(axis=1)
+    assert np.allclose((g[~const] ** 2).mean(axis=1), (sd / (sd + 1e-6)) ** 2, rtol=1e-12)
 
 
 @pytest.mark.parametrize("T", [1, 7, 64, 500])
