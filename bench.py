@@ -60,6 +60,9 @@ def parse():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--cpu-tokens", type=int, default=4096)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--pass", dest="which", choices=["update", "proxy"], default="update",
+                    help="update: the policy-update hot path (default); proxy: the forward-only "
+                         "output-head score proxy over every completion token")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a device copy of known size (HBM counter calibration) and exit")
     return ap.parse_args()
@@ -100,6 +103,56 @@ def cpu_baseline(wl, logp_old, ntok, seed):
                       f"{n} packed tokens (float64 numpy, {dt:.1f} s)"}
 
 
+def bench_proxy(args):
+    """Forward-only score-proxy pass (gamma, log p(o)) over every completion token."""
+    import torch
+    from paper_2606_29758_amd import pipeline, pspo, synth
+
+    wl = synth.make_workload(args.workload)
+    cfg = wl.cfg
+    dw = pipeline.upload(wl, np.zeros(wl.total_tokens, dtype=np.float32))
+    N = int(wl.total_tokens)
+    ws = torch.empty(pspo.score_proxy_workspace_bytes(N, cfg.d, cfg.V), dtype=torch.uint8, device="cuda")
+    err = torch.zeros(1, dtype=torch.int32, device="cuda")
+    run = lambda: pspo.score_proxy(dw.hidden_full, dw.w_head, dw.target_full, N, workspace=ws, err_flag=err)
+    for _ in range(args.warmup):
+        run()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    s.record(stream)
+    for _ in range(args.steps):
+        run()
+    e.record(stream)
+    torch.cuda.synchronize()
+    ms = s.elapsed_time(e) / args.steps
+    assert int(err.item()) == 0, "device error flag raised"
+    flops = 2.0 * N * cfg.V * cfg.d
+    achieved = flops / (ms * 1e-3) / 1e12
+    result = {
+        "metric": "completion tokens/sec for the output-head score proxy pass (forward only); % of bf16 MFMA peak",
+        "value": N / (ms * 1e-3), "unit": "completion tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": f"{args.workload}: every completion token, d={cfg.d}, V={cfg.V}", "tokens": N},
+        "roofline": {"bound": "mfma", "kernel": "pspo_score_proxy (forward bf16 MFMA kernel + two-sum epilogue)",
+                     "flops": "2 N V d per call", "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None},
+    }
+    if not args.no_cpu_baseline:
+        from threadpoolctl import threadpool_info
+        from oracle import score_proxy as osp
+        n = min(args.cpu_tokens, N)
+        t0 = time.perf_counter()
+        osp.score_proxy(wl.hidden_bits[:n], wl.w_bits, wl.target_full[:n])
+        dt = time.perf_counter() - t0
+        threads = max([p.get("num_threads", 1) for p in threadpool_info() if p.get("user_api") == "blas"] or [1])
+        result["cpu_baseline"] = {"value": n / dt, "unit": "completion tokens/s", "cores": int(threads),
+                                  "kind": "oracle",
+                                  "sample": f"gamma of the first {n} completion tokens (float64 numpy, {dt:.1f} s)"}
+    print(json.dumps(result), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -108,6 +161,9 @@ def main():
         sys.exit(2)
     if args.copy_calibration:
         copy_calibration()
+        return
+    if args.which == "proxy":
+        bench_proxy(args)
         return
 
     import torch

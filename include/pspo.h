@@ -198,6 +198,41 @@ int pspo_loss_fwd_bwd(const uint16_t* hidden, const uint16_t* w_head, const int3
                       double* stats, int32_t* err_flag, void* workspace, size_t workspace_bytes,
                       hipStream_t stream);
 
+/*
+ * Bytes of device workspace pspo_score_proxy needs (host-only, pure function).
+ */
+size_t pspo_score_proxy_workspace_bytes(int32_t N, int32_t d, int32_t V);
+
+/*
+ * Output-head score proxy of the cutoff design, forward only (Sec. 3.3,
+ * Eq. gamma_proxy; App. D, output-head score proxy).  Run under the old policy
+ * over every completion token before the cutoff probabilities are designed.
+ * For every row i with hidden state h_i, logits z_i = W h_i,
+ * p_i = softmax(z_i) and generated token o_i:
+ *   gamma_i = ||h_i||^2 ||e_{o_i} - p_i||^2 = ||h_i||^2 (1 - 2 p_i(o_i) + ||p_i||^2),
+ * the squared Frobenius norm of grad_W log p_i(o_i) (App. D).  The kernels form
+ * ||e_o - p||^2 from per-tile sums of exp(z - m) and exp(2 (z - m)) over the
+ * non-target entries (the second reduction of App. D, split so that no term
+ * cancels as p(o) -> 1).  The [N, V] logits are never written to memory.
+ *
+ *  hidden     device, bf16 bits [N, d] row-major; w_head: device, bf16 bits [V, d].
+ *  target     device, int32 [N]: the generated token of each row.
+ *  N >= 0, V >= 1, d > 0 with d % 64 == 0; device pointers 16-byte aligned.
+ *  gamma      device, float32 [N] out.
+ *  logp       device, float32 [N] out, or NULL: log p_i(o_i) (the old-policy
+ *             log-probs the update later consumes).
+ *  p_sq       device, float32 [N] out, or NULL: ||p_i||^2 = exp(l2 - 2 l1).
+ *  err_flag   device, int32 [1] or NULL: PSPO_DEVERR_TARGET if a target lies
+ *             outside [0, V); that row's outputs are NaN.
+ *  workspace  device, >= pspo_score_proxy_workspace_bytes(N, d, V) bytes,
+ *             256-byte aligned; contents on entry ignored.
+ * N = 0 is valid and does nothing.
+ */
+int pspo_score_proxy(const uint16_t* hidden, const uint16_t* w_head, const int32_t* target,
+                     int32_t N, int32_t d, int32_t V, float* gamma, float* logp, float* p_sq,
+                     int32_t* err_flag, void* workspace, size_t workspace_bytes,
+                     hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -17,6 +17,9 @@ It is a plain, slow, float64 implementation written from the paper:
   clipped ratio surrogate (Sec. 3.1, PPO objective) weighted by the cutoff
   correction, and its exact gradients with respect to the hidden rows and the
   head (App. D: grad_W log p(o) = (e_o - p) h^T).
+* ``score_proxy`` -- the output-head score proxy of the cutoff design,
+  gamma = ||h||^2 ||e_o - p||^2 (Sec. 3.3, Eq. gamma_proxy; App. D), from its
+  definition.
 
 Parity pins (what fixes each function other than itself) live in the
 ``-m "not gpu"`` tests: Philox known-answer vectors, the exact counting law of

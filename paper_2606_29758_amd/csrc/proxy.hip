@@ -1,0 +1,254 @@
+// Output-head score proxy of the cutoff design, forward only (Sec. 3.3,
+// Eq. gamma_proxy; App. D): for every completion token, under the old policy,
+//
+//   gamma = ||h||^2 * ||e_o - p||^2,   p = softmax(W h),  o = the generated token,
+//
+// the squared norm of the score of log p(o) with respect to the head W.  App. D
+// evaluates ||e_o - p||^2 as 1 - 2 p(o) + ||p||^2 from two log-sum-exp
+// reductions, lse(z) and lse(2z).  The kernels keep the same kind of second
+// reduction but split off the target entry: per vocabulary tile, with the tile
+// maximum m and e_v = exp(z_v - m),
+//
+//   S1 = sum_{v != o} e_v,   S2 = sum_{v != o} e_v^2,
+//
+// and after merging the tiles (with e_o = exp(z_o - M) at the common maximum M)
+//
+//   ||e_o - p||^2 = (1 - p(o))^2 + sum_{v != o} p_v^2 = (S1^2 + S2) / (S1 + e_o)^2,
+//
+// a sum of non-negative terms with no cancellation when p(o) -> 1 (where
+// 1 - 2 p(o) + ||p||^2 in float32 would lose every digit).  ||p||^2 and
+// log p(o) come out of the same sums.  The [N, V] logits are never stored.
+#include <cmath>
+#include <string>
+
+#include "common.h"
+#include "gemm.h"
+
+namespace pspo {
+namespace {
+
+constexpr float kNegInf = -INFINITY;
+
+// rows = vocabulary (A = W), columns = tokens (B = H).  Writes, per column and
+// 256-row vocabulary tile, (m, S1, S2) over the tile's rows other than the
+// column's target, and the target logit.
+struct EpiProxy {
+  int V, N;
+  int64_t ldp;  // stride between vocabulary tiles in the partial arrays (= Npad)
+  const int32_t* target;
+  float* part_m;
+  float* part_s1;
+  float* part_s2;
+  float* zt;
+
+  __device__ __forceinline__ void apply(const AccTile& acc, int tm, int tn, int wm, int wn, int lane, float* smem) const {
+    float* red = smem;  // [2 wave rows][256 columns][m, S1, S2]
+#pragma unroll
+    for (int j = 0; j < kBlocks; ++j) {
+      const int cl = acc_col(wn, j, lane);
+      const int t = tn * kTileN + cl;
+      const int tgt = (t < N) ? target[t] : -1;
+      float m = kNegInf;
+#pragma unroll
+      for (int i = 0; i < kBlocks; ++i)
+#pragma unroll
+        for (int r = 0; r < kAccPerBlock; ++r) {
+          const int v = tm * kTileM + acc_row(wm, i, r, lane);
+          const float x = acc.c[i][j][r];
+          if (v < V) {
+            m = fmaxf(m, x);
+            if (v == tgt) zt[t] = x;
+          }
+        }
+      m = fmaxf(m, __shfl_xor(m, 16));
+      m = fmaxf(m, __shfl_xor(m, 32));
+      float s1 = 0.f, s2 = 0.f;
+      if (m != kNegInf) {
+#pragma unroll
+        for (int i = 0; i < kBlocks; ++i)
+#pragma unroll
+          for (int r = 0; r < kAccPerBlock; ++r) {
+            const int v = tm * kTileM + acc_row(wm, i, r, lane);
+            if (v < V && v != tgt) {
+              const float e = __expf(acc.c[i][j][r] - m);
+              s1 += e;
+              s2 += e * e;
+            }
+          }
+      }
+      s1 += __shfl_xor(s1, 16);
+      s1 += __shfl_xor(s1, 32);
+      s2 += __shfl_xor(s2, 16);
+      s2 += __shfl_xor(s2, 32);
+      if (lane < 16) {
+        float* o = red + (wm * 256 + cl) * 3;
+        o[0] = m;
+        o[1] = s1;
+        o[2] = s2;
+      }
+    }
+    __syncthreads();
+    const int c = threadIdx.x;
+    const float* a = red + c * 3;
+    const float* b = red + (256 + c) * 3;
+    const float M = fmaxf(a[0], b[0]);
+    float S1 = 0.f, S2 = 0.f;
+    if (a[0] != kNegInf) {
+      const float f = __expf(a[0] - M);
+      S1 += a[1] * f;
+      S2 += a[2] * f * f;
+    }
+    if (b[0] != kNegInf) {
+      const float f = __expf(b[0] - M);
+      S1 += b[1] * f;
+      S2 += b[2] * f * f;
+    }
+    const int t = tn * kTileN + c;
+    if (t < N) {
+      part_m[tm * ldp + t] = M;
+      part_s1[tm * ldp + t] = S1;
+      part_s2[tm * ldp + t] = S2;
+    }
+  }
+};
+
+// ||h||^2 of each bf16 row, one wave per row (16-byte loads), float32 sums.
+__global__ __launch_bounds__(256) void row_sqnorm_kernel(const uint16_t* __restrict__ h, int N, int d,
+                                                         float* __restrict__ out) {
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (row >= N) return;
+  const u32x4* p = reinterpret_cast<const u32x4*>(h + (int64_t)row * d);
+  float s = 0.f;
+  for (int c = lane; c < d / 8; c += 64) {
+    const u32x4 v = p[c];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const float lo = __uint_as_float(v[k] << 16), hi = __uint_as_float(v[k] & 0xFFFF0000u);
+      s += lo * lo + hi * hi;
+    }
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o);
+  if (lane == 0) out[row] = s;
+}
+
+// Merge the vocabulary-tile partials of each token and form gamma, log p(o), ||p||^2.
+__global__ __launch_bounds__(256) void proxy_finalize_kernel(int N, int V, int ntv, int64_t ldp,
+                                                             const float* __restrict__ part_m,
+                                                             const float* __restrict__ part_s1,
+                                                             const float* __restrict__ part_s2,
+                                                             const float* __restrict__ zt,
+                                                             const float* __restrict__ hn,
+                                                             const int32_t* __restrict__ target,
+                                                             float* __restrict__ gamma, float* __restrict__ logp,
+                                                             float* __restrict__ p_sq, int32_t* __restrict__ err_flag) {
+  const int t = blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= N) return;
+  const int tgt = target[t];
+  if (tgt < 0 || tgt >= V) {
+    gamma[t] = NAN;
+    if (logp) logp[t] = NAN;
+    if (p_sq) p_sq[t] = NAN;
+    if (err_flag) atomicOr(err_flag, PSPO_DEVERR_TARGET);
+    return;
+  }
+  float M = kNegInf;
+  for (int k = 0; k < ntv; ++k) M = fmaxf(M, part_m[k * ldp + t]);
+  float S1 = 0.f, S2 = 0.f;
+  for (int k = 0; k < ntv; ++k) {
+    const float m = part_m[k * ldp + t];
+    if (m == kNegInf) continue;
+    const float f = __expf(m - M);
+    S1 += part_s1[k * ldp + t] * f;
+    S2 += part_s2[k * ldp + t] * f * f;
+  }
+  const float et = expf(zt[t] - M);     // the target's entry (M >= z_o, so et <= 1)
+  const float L = S1 + et;               // sum_v exp(z_v - M) >= 1
+  const float inv = 1.f / L;
+  gamma[t] = hn[t] * ((S1 * inv) * (S1 * inv) + S2 * inv * inv);
+  if (logp) logp[t] = (zt[t] - M) - logf(L);
+  if (p_sq) p_sq[t] = (S2 + et * et) * inv * inv;
+}
+
+struct ProxyPlan {
+  int64_t Npad, Vpad, ntv;
+  int64_t off_m, off_s1, off_s2, off_zt, off_hn, total;
+};
+
+ProxyPlan make_proxy_plan(int64_t N, int64_t V) {
+  ProxyPlan p{};
+  p.Npad = round_up(N > 0 ? N : 1, kTileN);
+  p.Vpad = round_up(V, kTileM);
+  p.ntv = p.Vpad / kTileM;
+  int64_t o = 0;
+  auto take = [&](int64_t bytes) {
+    const int64_t at = o;
+    o = round_up(o + bytes, 256);
+    return at;
+  };
+  p.off_m = take(p.ntv * p.Npad * 4);
+  p.off_s1 = take(p.ntv * p.Npad * 4);
+  p.off_s2 = take(p.ntv * p.Npad * 4);
+  p.off_zt = take(p.Npad * 4);
+  p.off_hn = take(p.Npad * 4);
+  p.total = o;
+  return p;
+}
+
+}  // namespace
+}  // namespace pspo
+
+extern "C" {
+
+size_t pspo_score_proxy_workspace_bytes(int32_t N, int32_t d, int32_t V) {
+  if (N < 0 || d <= 0 || V <= 0) return 0;
+  return (size_t)pspo::make_proxy_plan(N, V).total;
+}
+
+int pspo_score_proxy(const uint16_t* hidden, const uint16_t* w_head, const int32_t* target, int32_t N, int32_t d,
+                     int32_t V, float* gamma, float* logp, float* p_sq, int32_t* err_flag, void* workspace,
+                     size_t workspace_bytes, hipStream_t stream) {
+  using namespace pspo;
+  clear_last_error();
+  PSPO_REQUIRE(N >= 0, PSPO_ERR_INVALID_ARG, "N must be >= 0");
+  PSPO_REQUIRE(d > 0 && V > 0, PSPO_ERR_INVALID_ARG, "d and V must be > 0");
+  PSPO_REQUIRE(d % 64 == 0, PSPO_ERR_UNSUPPORTED, "d must be a multiple of 64");
+  if (N == 0) return PSPO_OK;
+  PSPO_REQUIRE(hidden && w_head && target && gamma, PSPO_ERR_INVALID_ARG, "null input or gamma pointer");
+  PSPO_REQUIRE(aligned(hidden, 16) && aligned(w_head, 16), PSPO_ERR_INVALID_ARG,
+               "hidden and w_head must be 16-byte aligned");
+  PSPO_REQUIRE(aligned(target, 4) && aligned(gamma, 4) && aligned(logp, 4) && aligned(p_sq, 4),
+               PSPO_ERR_INVALID_ARG, "misaligned per-token pointer");
+  PSPO_REQUIRE(workspace != nullptr && aligned(workspace, 256), PSPO_ERR_INVALID_ARG,
+               "workspace must be non-NULL and 256-byte aligned");
+  const ProxyPlan pl = make_proxy_plan(N, V);
+  PSPO_REQUIRE(workspace_bytes >= (size_t)pl.total, PSPO_ERR_WORKSPACE,
+               "workspace too small: need " + std::to_string(pl.total) + " bytes");
+  PSPO_REQUIRE(pl.Npad <= INT32_MAX && pl.Vpad <= INT32_MAX, PSPO_ERR_UNSUPPORTED, "problem too large");
+  if (int rc = require_gfx950()) return rc;
+
+  char* ws = static_cast<char*>(workspace);
+  float* part_m = reinterpret_cast<float*>(ws + pl.off_m);
+  float* part_s1 = reinterpret_cast<float*>(ws + pl.off_s1);
+  float* part_s2 = reinterpret_cast<float*>(ws + pl.off_s2);
+  float* zt = reinterpret_cast<float*>(ws + pl.off_zt);
+  float* hn = reinterpret_cast<float*>(ws + pl.off_hn);
+
+  const int tiles_tok = (int)(pl.Npad / kTileN);
+  const int tiles_voc = (int)pl.ntv;
+  {
+    GemmShape g{w_head, d, V, hidden, d, N, d, tiles_voc, tiles_tok};
+    EpiProxy e{V, N, pl.Npad, target, part_m, part_s1, part_s2, zt};
+    hipLaunchKernelGGL(gemm_nt_kernel<EpiProxy>, dim3(gemm_grid(tiles_voc, tiles_tok)), dim3(kGemmThreads), 0,
+                       stream, g, e);
+    PSPO_HIP_CHECK(hipGetLastError());
+  }
+  hipLaunchKernelGGL(row_sqnorm_kernel, dim3((unsigned)((N + 3) / 4)), dim3(256), 0, stream, hidden, N, d, hn);
+  PSPO_HIP_CHECK(hipGetLastError());
+  hipLaunchKernelGGL(proxy_finalize_kernel, dim3((unsigned)((N + 255) / 256)), dim3(256), 0, stream, N, V,
+                     tiles_voc, pl.Npad, part_m, part_s1, part_s2, zt, hn, target, gamma, logp, p_sq, err_flag);
+  PSPO_HIP_CHECK(hipGetLastError());
+  return PSPO_OK;
+}
+
+}  // extern "C"

@@ -32,6 +32,8 @@ _SIGNATURES = {
     "pspo_loss_workspace_bytes": (_SZ, [_I32, _I32, _I32, _U32]),
     "pspo_loss_fwd_bwd": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _I32, _I32, _I32, _I32,
                                          _F32, _F32, _F32, _U32, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
+    "pspo_score_proxy_workspace_bytes": (_SZ, [_I32, _I32, _I32]),
+    "pspo_score_proxy": (ctypes.c_int, [_P, _P, _P, _I32, _I32, _I32, _P, _P, _P, _P, _P, _SZ, _P]),
 }
 
 _lib = None
@@ -206,3 +208,36 @@ def loss_fwd_bwd(hidden, w_head, target, logp_old, weight, seq_id, advantage, N:
         _ptr(workspace), workspace.numel(), _stream()))
     return dict(loss=loss, d_hidden=d_hidden[:N], d_w_head=d_w_head,
                 logp_new=None if logp is None else logp[:N], stats=stats, workspace=workspace)
+
+
+def score_proxy_workspace_bytes(N: int, d: int, V: int) -> int:
+    return int(load().pspo_score_proxy_workspace_bytes(N, d, V))
+
+
+def score_proxy(hidden, w_head, target, N: int, want_logp: bool = True, want_p_sq: bool = False,
+                workspace: Optional[torch.Tensor] = None, err_flag: Optional[torch.Tensor] = None) -> dict:
+    """Output-head score proxy gamma (and optionally log p(o), ||p||^2) of the first N rows."""
+    _dev(w_head, torch.bfloat16, "w_head")
+    V, d = w_head.shape
+    dev = w_head.device
+    if N > 0:
+        _dev(hidden, torch.bfloat16, "hidden")
+        _dev(target, torch.int32, "target")
+        if hidden.shape[1] != d:
+            raise ValueError("hidden and w_head disagree on d")
+        if hidden.shape[0] < N or target.shape[0] < N:
+            raise ValueError("hidden or target has fewer than N rows")
+    gamma = torch.empty(max(N, 1), dtype=torch.float32, device=dev)
+    logp = torch.empty(max(N, 1), dtype=torch.float32, device=dev) if want_logp else None
+    p_sq = torch.empty(max(N, 1), dtype=torch.float32, device=dev) if want_p_sq else None
+    need = score_proxy_workspace_bytes(N, d, V)
+    if workspace is None:
+        workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=dev)
+    _dev(workspace, torch.uint8, "workspace")
+    if err_flag is not None:
+        _dev(err_flag, torch.int32, "err_flag")
+    _check(load().pspo_score_proxy(
+        _ptr(hidden) if N > 0 else None, _ptr(w_head), _ptr(target) if N > 0 else None, N, d, V,
+        _ptr(gamma), _ptr(logp), _ptr(p_sq), _ptr(err_flag), _ptr(workspace), workspace.numel(), _stream()))
+    return dict(gamma=gamma[:N], logp=None if logp is None else logp[:N],
+                p_sq=None if p_sq is None else p_sq[:N], workspace=workspace)

@@ -29,14 +29,14 @@ def _declared():
 
 def test_exports_every_declared_symbol(lib):
     names = _declared()
-    assert len(names) == 8
+    assert len(names) == 10
     for name in names:
         assert hasattr(lib, name), name
     assert sorted(pspo.exported_symbols()) == names
 
 
 def test_version_and_status_strings(lib):
-    assert lib.pspo_abi_version() == 2
+    assert lib.pspo_abi_version() == 3
     assert lib.pspo_status_string(0) == b"PSPO_OK"
     assert lib.pspo_status_string(3) == b"PSPO_ERR_WORKSPACE"
     assert lib.pspo_status_string(99) == b"PSPO_ERR_UNKNOWN"
@@ -146,6 +146,39 @@ def test_workspace_bytes(lib):
     assert 0 < a < b
     # the dominant terms: bf16 logit-gradient chunks in both layouts (2 x Npad x 16384 x 2 B)
     assert b > 2 * 2048 * 16384 * 2
+
+
+def _proxy(lib, **kw):
+    N, d, V = kw.get("N", 100), kw.get("d", 128), kw.get("V", 1000)
+    ws_bytes = lib.pspo_score_proxy_workspace_bytes(max(N, 0), d, max(V, 1))
+    a = dict(h=FAKE, w=FAKE, t=FAKE, N=N, d=d, V=V, g=FAKE, lp=None, ps=None, err=None, ws=FAKE, wsb=ws_bytes)
+    a.update(kw)
+    return lib.pspo_score_proxy(a["h"], a["w"], a["t"], a["N"], a["d"], a["V"], a["g"], a["lp"], a["ps"],
+                                a["err"], a["ws"], a["wsb"], None)
+
+
+def test_score_proxy_argument_errors(lib):
+    assert _proxy(lib, N=0, h=None, t=None, g=None, ws=None) == OK   # nothing to do, no device work
+    assert _proxy(lib, N=-1) == INVALID
+    assert _proxy(lib, d=0) == INVALID
+    assert _proxy(lib, V=0) == INVALID
+    assert _proxy(lib, d=96) == UNSUPPORTED
+    assert _proxy(lib, g=None) == INVALID
+    assert _proxy(lib, h=None) == INVALID
+    assert _proxy(lib, t=None) == INVALID
+    assert _proxy(lib, h=ctypes.c_void_p((1 << 20) + 4)) == INVALID
+    assert _proxy(lib, lp=ctypes.c_void_p((1 << 20) + 2)) == INVALID
+    assert _proxy(lib, ws=None) == INVALID
+    assert _proxy(lib, wsb=1024) == WORKSPACE
+    assert b"workspace too small" in lib.pspo_last_error()
+
+
+def test_score_proxy_workspace_bytes(lib):
+    assert lib.pspo_score_proxy_workspace_bytes(-1, 128, 100) == 0
+    assert lib.pspo_score_proxy_workspace_bytes(10, 128, 0) == 0
+    # three float32 partials per (256-row vocabulary tile, token) plus two per-token arrays
+    b = lib.pspo_score_proxy_workspace_bytes(1000, 3584, 152064)
+    assert b >= 3 * 594 * 1024 * 4 + 2 * 1024 * 4
 
 
 def test_binding_refuses_host_tensors():
