@@ -17,6 +17,10 @@ It is a plain, slow, float64 implementation written from the paper:
   clipped ratio surrogate (Sec. 3.1, PPO objective) weighted by the cutoff
   correction, and its exact gradients with respect to the hidden rows and the
   head (App. D: grad_W log p(o) = (e_o - p) h^T).
+* ``cutoff_design`` -- the cutoff design: per-step weights w_t = gbar_t u_t
+  from the score proxy and the reward-uncertainty proxy (App. E), the
+  budgeted monotone optimum by pooling adjacent violators with the xi <= 1 cap
+  (App. F) and the Uniform / Time-prior / Heuristic variants.
 * ``score_proxy`` -- the output-head score proxy of the cutoff design,
   gamma = ||h||^2 ||e_o - p||^2 (Sec. 3.3, Eq. gamma_proxy; App. D), from its
   definition.
