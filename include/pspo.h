@@ -233,6 +233,81 @@ int pspo_score_proxy(const uint16_t* hidden, const uint16_t* w_head, const int32
                      int32_t* err_flag, void* workspace, size_t workspace_bytes,
                      hipStream_t stream);
 
+/* Variants of the cutoff design (Sec. 4 ablation: Optimized, Heuristic, Uniform, Time prior). */
+enum {
+  PSPO_DESIGN_OPTIMIZED = 0,
+  PSPO_DESIGN_HEURISTIC = 1,
+  PSPO_DESIGN_UNIFORM = 2,
+  PSPO_DESIGN_TIME_PRIOR = 3
+};
+
+/*
+ * Per-step weights of the cutoff design ("Computing xi", Algorithm 1; Sec. 3.3,
+ * Eq. wtilde_factorized1; App. E).  For prompt p (completions r = pK+k,
+ * k < K, lengths T_r) and step t = 1..T_p (T_p = max_k T_{pK+k}), over the
+ * n_t completions with T_r >= t:
+ *   gamma_bar_t = (1/n_t) sum_r gamma_r(t),
+ *   u_t = 1/2 - 1/(2 n_t) || sum_{r succeeded} pi_r(.|t) - sum_{r failed} pi_r(.|t) ||_1,
+ *   w_t = gamma_bar_t u_t,
+ * i.e. App. E's 1/2 - 1/2 || p pibar_G - (1-p) pibar_B ||_1 with p, pibar_G and
+ * pibar_B estimated from the completions alive at t.  pi_r(.|t) is the
+ * old policy's next-token distribution at completion token t, known through its
+ * top-k entries; the mass outside them counts as one coordinate shared by all
+ * completions.  Float64 throughout.
+ *
+ *  gamma       device, float32 [S]: the score proxy of every completion token
+ *              (pspo_score_proxy), completions laid out one after another.
+ *  topk_ids    device, int32 [S, topk]; topk_logp: device, float32 [S, topk]:
+ *              the top-k next-token ids and log-probs at each completion token
+ *              (as the rollout engine reports them; distinct ids per row).
+ *  lengths     device, int32 [P K]; full_off: device, int32 [P K + 1], the
+ *              exclusive scan of lengths (as pspo_pack_prefixes writes it).
+ *  rewards     device, float32 [P K]; a completion succeeded iff reward > 1/2.
+ *  xi_off      device, int64 [P + 1]: the layout of the per-step outputs (the
+ *              xi-table layout: xi_off[p+1] - xi_off[p] = T_p); total_T = xi_off[P]
+ *              (host value, sizes the launch).
+ *  1 <= K <= 64, topk >= 1, K * topk <= 256.
+ *  w           device, float64 [total_T] out; gamma_bar, u: device, float64
+ *              [total_T] out, or NULL.
+ *  err_flag    PSPO_DEVERR_BAD_XI if some step of a table has no alive
+ *              completion (the table is longer than the prompt's completions);
+ *              w = NaN there.
+ */
+int pspo_design_weights(const float* gamma, const int32_t* topk_ids, const float* topk_logp,
+                        int32_t topk, const int32_t* lengths, const int32_t* full_off,
+                        const float* rewards, const int64_t* xi_off, int32_t P, int32_t K,
+                        int64_t total_T, double* w, double* gamma_bar, double* u,
+                        int32_t* err_flag, hipStream_t stream);
+
+/* Bytes of device workspace pspo_design_cutoffs needs (host-only). */
+size_t pspo_design_workspace_bytes(int64_t total_T);
+
+/*
+ * Cutoff survival tables from the per-step weights (Sec. 3.3, Eq. design_problem;
+ * App. F).  Per prompt: minimise sum_t w_t / xi_t subject to
+ * sum_t xi_t = budget (the expected prefix length) and 1 >= xi_1 >= ... >= xi_T > 0.
+ * PSPO_DESIGN_OPTIMIZED: Pooling Adjacent Violators gives blocks with scores
+ * s_m = sqrt(W_m / L_m) non-increasing (App. F); xi = min(1, kappa s_m) with the
+ * saturated prefix at 1 and kappa spending the rest of the budget.
+ * PSPO_DESIGN_HEURISTIC: min(1, budget sqrt(w_t) / sum_j sqrt(w_j)) followed by a
+ * running minimum.  PSPO_DESIGN_UNIFORM: xi_t = (T - t + 1) / T (H uniform on
+ * 1..T).  PSPO_DESIGN_TIME_PRIOR: xi_t = exp(-lambda (t - 1)).  If budget >= T
+ * every xi is 1; if every weight is 0, xi = budget / T.  Every xi is floored at
+ * 2^-32 (the sampler's resolution).  The result is a valid input of
+ * pspo_sample_cutoffs.
+ *
+ *  w           device, float64 [total_T] (xi_off layout), finite and >= 0
+ *              (else PSPO_DEVERR_BAD_XI and that prompt's table is NaN).
+ *  xi_off      device, int64 [P + 1]; total_T = xi_off[P] (host value).
+ *  budget      > 0.  lambda >= 0 (used by PSPO_DESIGN_TIME_PRIOR only).
+ *  xi          device, float64 [total_T] out.
+ *  workspace   device, >= pspo_design_workspace_bytes(total_T) bytes, 256-byte aligned.
+ */
+int pspo_design_cutoffs(const double* w, const int64_t* xi_off, int32_t P, int64_t total_T,
+                        double budget, int32_t variant, double lambda, double* xi,
+                        void* workspace, size_t workspace_bytes, int32_t* err_flag,
+                        hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -66,7 +66,14 @@ def proxy_weights(gamma, topk_ids, topk_logp, lengths, rewards, P: int, K: int) 
                     mass += pr
                 rest += sign * max(0.0, 1.0 - mass)
             l1 = sum(abs(x) for x in diff.values()) + abs(rest)
-            u.append(0.5 - 0.5 * l1 / n)
+            n_succ = sum(1 for r in alive if rewards[r] > 0.5)
+            if n_succ == 0 or n_succ == n:
+                # equal rewards among the alive completions: p is 0 or 1 and the norm is
+                # exactly 1, so u = 0 (taken exactly, not through rounding)
+                u.append(0.0)
+            else:
+                # the norm is at most 1 (triangle inequality), so u >= 0: clamp rounding below it
+                u.append(max(0.0, 0.5 - 0.5 * l1 / n))
     gbar = np.array(gbar)
     u = np.array(u)
     return dict(gbar=gbar, u=u, w=gbar * u)
@@ -105,14 +112,19 @@ def design_xi(w, budget: float, variant: int = OPTIMIZED, lam: float = 0.0) -> n
         return np.maximum(xi, XI_FLOOR)
     blocks = pav_blocks(w)
     score = [math.sqrt(W / L) for _, L, W in blocks]
+    # rest[m] = sum_{j >= m} L_j s_j, accumulated from the last block
+    rest = [0.0] * len(blocks)
+    acc = 0.0
+    for m in range(len(blocks) - 1, -1, -1):
+        acc += blocks[m][1] * score[m]
+        rest[m] = acc
     xi = np.empty(T)
     saturated = 0
     for m in range(len(blocks)):
-        rest = sum(L * s for (_, L, _), s in zip(blocks[m:], score[m:]))
-        if rest == 0.0:                         # only zero-weight blocks left
+        if rest[m] == 0.0:                      # only zero-weight blocks left
             kappa = None
             break
-        kappa = (budget - saturated) / rest
+        kappa = (budget - saturated) / rest[m]
         if kappa * score[m] <= 1.0:
             break
         saturated += blocks[m][1]

@@ -1,0 +1,289 @@
+// Cutoff design of PS-PPO ("Computing xi" of Algorithm 1; Sec. 3.3, App. E, F).
+//
+// Weights.  For prompt p (completions r = pK .. pK+K-1, lengths T_r,
+// T_p = max_r T_r) and step t = 1..T_p, over the n_t completions alive at t
+// (T_r >= t):
+//   gbar_t = (1/n_t) sum_r gamma_r(t)                 (output-head score proxy, App. D)
+//   u_t    = 1/2 - 1/(2 n_t) || sum_{r in G_t} pi_r(.|t) - sum_{r in B_t} pi_r(.|t) ||_1
+//            (reward-uncertainty proxy, App. E, with p = |G_t|/n_t; G_t / B_t the
+//            successful / unsuccessful completions)
+//   w_t    = gbar_t u_t.
+// Each pi_r(.|t) is given by its top-k entries (token id, log-prob); the mass
+// left outside them is one further coordinate shared by every completion.
+//
+// Design.  Per prompt, minimise sum_t w_t / xi_t subject to sum_t xi_t = B and
+// 1 >= xi_1 >= ... >= xi_T > 0 (Eq. design_problem): Pooling Adjacent
+// Violators builds contiguous blocks with non-increasing scores
+// s_m = sqrt(W_m / L_m) (App. F); the optimum is xi = min(1, kappa s_m), the
+// cap saturating a prefix of blocks and kappa spending the rest of the budget
+// on the others.  Variants: Heuristic (the unconstrained closed form
+// B sqrt(w_t) / sum_j sqrt(w_j), capped, then a running minimum), Uniform
+// (H uniform on 1..T) and Time prior (xi_t = exp(-lambda (t-1))).  Every xi is
+// floored at 2^-32, the resolution of the sampler's thresholds.
+//
+// Both kernels work in float64; their cost is negligible next to the proxy's
+// forward pass (a few operations per completion token and per step).
+#include <cmath>
+#include <string>
+
+#include "common.h"
+
+namespace pspo {
+namespace {
+
+constexpr int kDesignMaxEntries = 256;   // K * topk per step
+constexpr double kXiFloor = 0x1p-32;
+
+__device__ __forceinline__ double wave_sum(double v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+
+// One wave per (prompt, step); 4 waves per block.
+__global__ __launch_bounds__(256) void design_weights_kernel(
+    const float* __restrict__ gamma, const int32_t* __restrict__ topk_ids, const float* __restrict__ topk_logp,
+    int topk, const int32_t* __restrict__ lengths, const int32_t* __restrict__ full_off,
+    const float* __restrict__ rewards, const int64_t* __restrict__ xi_off, int P, int K, int64_t total,
+    double* __restrict__ w, double* __restrict__ gbar_out, double* __restrict__ u_out, int32_t* __restrict__ err_flag) {
+  __shared__ int32_t sid[4][kDesignMaxEntries];
+  __shared__ double sval[4][kDesignMaxEntries];
+  const int wv = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int64_t g = (int64_t)blockIdx.x * 4 + wv;
+  const bool live = g < total;   // a wave past the end still takes part in the barrier
+  // prompt of g: the last p with xi_off[p] <= g
+  int lo = 0, hi = P - 1;
+  while (live && lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (xi_off[mid] <= g) lo = mid;
+    else hi = mid - 1;
+  }
+  const int p = lo;
+  const int t = live ? (int)(g - xi_off[p]) + 1 : 0;
+
+  // per-entry signed probabilities of the alive completions (0 for the others)
+  const int ne = live ? K * topk : 0;
+  for (int j = lane; j < ne; j += 64) {
+    const int k = j / topk, r = p * K + k;
+    int32_t id = -1;
+    double v = 0.0;
+    if (lengths[r] >= t) {
+      const int64_t row = (int64_t)full_off[r] + t - 1;
+      id = topk_ids[row * topk + (j - k * topk)];
+      v = exp((double)topk_logp[row * topk + (j - k * topk)]) * (rewards[r] > 0.5f ? 1.0 : -1.0);
+    }
+    sid[wv][j] = id;
+    sval[wv][j] = v;
+  }
+  __syncthreads();
+  // each distinct token id is summed once, by the lane that holds its first occurrence
+  double l1 = 0.0;
+  for (int j = lane; j < ne; j += 64) {
+    const int32_t id = sid[wv][j];
+    if (id < 0) continue;
+    bool first = true;
+    for (int i = 0; i < j && first; ++i) first = sid[wv][i] != id;
+    if (!first) continue;
+    double s = 0.0;
+    for (int i = j; i < ne; ++i)
+      if (sid[wv][i] == id) s += sval[wv][i];
+    l1 += fabs(s);
+  }
+  // per completion: the mass outside its top-k, and its gamma
+  double rest = 0.0, gsum = 0.0, nalive = 0.0, nsucc = 0.0;
+  if (live && lane < K) {
+    const int r = p * K + lane;
+    if (lengths[r] >= t) {
+      const int64_t row = (int64_t)full_off[r] + t - 1;
+      double mass = 0.0;
+      for (int e = 0; e < topk; ++e) mass += exp((double)topk_logp[row * topk + e]);
+      const bool ok = rewards[r] > 0.5f;
+      rest = fmax(0.0, 1.0 - mass) * (ok ? 1.0 : -1.0);
+      gsum = (double)gamma[row];
+      nalive = 1.0;
+      nsucc = ok ? 1.0 : 0.0;
+    }
+  }
+  l1 = wave_sum(l1);
+  rest = wave_sum(rest);
+  gsum = wave_sum(gsum);
+  nalive = wave_sum(nalive);
+  nsucc = wave_sum(nsucc);
+  if (live && lane == 0) {
+    if (nalive == 0.0) {   // the table is longer than every completion of the prompt
+      if (err_flag) atomicOr(err_flag, PSPO_DEVERR_BAD_XI);
+      w[g] = NAN;
+      return;
+    }
+    const double gb = gsum / nalive;
+    // equal rewards among the alive completions: p is 0 or 1 and the norm is exactly 1,
+    // so u = 0 (taken exactly); otherwise ||.||_1 <= 1 by the triangle inequality, so
+    // u >= 0 and rounding below it is clamped
+    const double u = (nsucc == 0.0 || nsucc == nalive) ? 0.0 : fmax(0.0, 0.5 - 0.5 * (l1 + fabs(rest)) / nalive);
+    w[g] = gb * u;
+    if (gbar_out) gbar_out[g] = gb;
+    if (u_out) u_out[g] = u;
+  }
+}
+
+// One block of 64 threads per prompt; lane 0 runs the sequential solve.
+__global__ __launch_bounds__(64) void design_cutoffs_kernel(const double* __restrict__ w,
+                                                            const int64_t* __restrict__ xi_off, double budget,
+                                                            int variant, double lambda, double* __restrict__ xi,
+                                                            int32_t* __restrict__ bstart, int32_t* __restrict__ blen,
+                                                            double* __restrict__ bval, int32_t* __restrict__ err_flag) {
+  const int p = blockIdx.x;
+  const int64_t a = xi_off[p];
+  const int T = (int)(xi_off[p + 1] - a);
+  const double* wp = w + a;
+  double* xp = xi + a;
+  if (variant == PSPO_DESIGN_UNIFORM) {
+    for (int t = threadIdx.x; t < T; t += blockDim.x) xp[t] = (double)(T - t) / (double)T;
+    return;
+  }
+  if (variant == PSPO_DESIGN_TIME_PRIOR) {
+    for (int t = threadIdx.x; t < T; t += blockDim.x) xp[t] = fmax(exp(-lambda * (double)t), kXiFloor);
+    return;
+  }
+  if (threadIdx.x != 0) return;
+  bool bad = false;
+  double root_sum = 0.0;
+  for (int t = 0; t < T; ++t) {
+    const double v = wp[t];
+    if (!(v >= 0.0) || isinf(v)) bad = true;
+    else root_sum += sqrt(v);
+  }
+  if (bad) {
+    if (err_flag) atomicOr(err_flag, PSPO_DEVERR_BAD_XI);
+    for (int t = 0; t < T; ++t) xp[t] = NAN;
+    return;
+  }
+  if (budget >= (double)T) {
+    for (int t = 0; t < T; ++t) xp[t] = 1.0;
+    return;
+  }
+  if (root_sum == 0.0) {   // every weight zero: any feasible table is optimal
+    for (int t = 0; t < T; ++t) xp[t] = budget / (double)T;
+    return;
+  }
+  if (variant == PSPO_DESIGN_HEURISTIC) {
+    double run = 1.0;
+    for (int t = 0; t < T; ++t) {
+      run = fmin(run, fmin(1.0, budget * sqrt(wp[t]) / root_sum));
+      xp[t] = fmax(run, kXiFloor);
+    }
+    return;
+  }
+  // Pooling Adjacent Violators: a stack of blocks (start, length, summed weight)
+  int32_t* st = bstart + a;
+  int32_t* ln = blen + a;
+  double* wv = bval + a;
+  int M = 0;
+  for (int t = 0; t < T; ++t) {
+    int s0 = t, L = 1;
+    double W = wp[t];
+    while (M > 0 && sqrt(wv[M - 1] / (double)ln[M - 1]) < sqrt(W / (double)L)) {
+      --M;
+      s0 = st[M];
+      L += ln[M];
+      W = wv[M] + W;
+    }
+    st[M] = s0;
+    ln[M] = L;
+    wv[M] = W;
+    ++M;
+  }
+  // scores, then suffix sums of L_m s_m (accumulated from the last block)
+  for (int m = 0; m < M; ++m) wv[m] = sqrt(wv[m] / (double)ln[m]);
+  // first unsaturated block: kappa(m) = (B - sum_{j<m} L_j) / sum_{j>=m} L_j s_j, kappa(m) s_m <= 1
+  double* rest = xp;   // scratch: the output table holds the suffix sums until it is written
+  double acc = 0.0;
+  for (int m = M - 1; m >= 0; --m) {
+    acc += (double)ln[m] * wv[m];
+    rest[m] = acc;
+  }
+  int saturated = 0;
+  double kappa = -1.0;   // < 0: only zero-weight blocks remain unsaturated
+  for (int m = 0; m < M; ++m) {
+    if (rest[m] == 0.0) {
+      kappa = -1.0;
+      break;
+    }
+    kappa = (budget - (double)saturated) / rest[m];
+    if (kappa * wv[m] <= 1.0) break;
+    saturated += ln[m];
+  }
+  for (int m = 0; m < M; ++m) {
+    double v;
+    if (kappa < 0.0) v = (st[m] < saturated) ? 1.0 : (budget - (double)saturated) / (double)(T - saturated);
+    else v = fmin(1.0, kappa * wv[m]);
+    v = fmax(v, kXiFloor);
+    for (int t = st[m]; t < st[m] + ln[m]; ++t) xp[t] = v;
+  }
+}
+
+}  // namespace
+}  // namespace pspo
+
+extern "C" {
+
+int pspo_design_weights(const float* gamma, const int32_t* topk_ids, const float* topk_logp, int32_t topk,
+                        const int32_t* lengths, const int32_t* full_off, const float* rewards, const int64_t* xi_off,
+                        int32_t P, int32_t K, int64_t total_T, double* w, double* gamma_bar, double* u,
+                        int32_t* err_flag, hipStream_t stream) {
+  using namespace pspo;
+  clear_last_error();
+  PSPO_REQUIRE(P >= 1 && K >= 1 && total_T >= 0, PSPO_ERR_INVALID_ARG, "need P >= 1, K >= 1, total_T >= 0");
+  PSPO_REQUIRE(K <= 64, PSPO_ERR_UNSUPPORTED, "K must be <= 64");
+  PSPO_REQUIRE(topk >= 1 && (int64_t)K * topk <= kDesignMaxEntries, PSPO_ERR_UNSUPPORTED,
+               "need topk >= 1 and K * topk <= 256");
+  if (total_T == 0) return PSPO_OK;
+  PSPO_REQUIRE(gamma && topk_ids && topk_logp && lengths && full_off && rewards && xi_off && w, PSPO_ERR_INVALID_ARG,
+               "null pointer");
+  PSPO_REQUIRE(aligned(w, 8) && aligned(gamma_bar, 8) && aligned(u, 8) && aligned(xi_off, 8), PSPO_ERR_INVALID_ARG,
+               "misaligned float64 / int64 pointer");
+  if (int rc = require_gfx950()) return rc;
+  const int64_t blocks = (total_T + 3) / 4;
+  PSPO_REQUIRE(blocks <= INT32_MAX, PSPO_ERR_UNSUPPORTED, "problem too large");
+  hipLaunchKernelGGL(design_weights_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, gamma, topk_ids, topk_logp,
+                     topk, lengths, full_off, rewards, xi_off, P, K, total_T, w, gamma_bar, u, err_flag);
+  PSPO_HIP_CHECK(hipGetLastError());
+  return PSPO_OK;
+}
+
+size_t pspo_design_workspace_bytes(int64_t total_T) {
+  using pspo::round_up;
+  if (total_T < 0) return 0;
+  return (size_t)(round_up(total_T * 4, 256) * 2 + round_up(total_T * 8, 256));
+}
+
+int pspo_design_cutoffs(const double* w, const int64_t* xi_off, int32_t P, int64_t total_T, double budget,
+                        int32_t variant, double lambda, double* xi, void* workspace, size_t workspace_bytes,
+                        int32_t* err_flag, hipStream_t stream) {
+  using namespace pspo;
+  clear_last_error();
+  PSPO_REQUIRE(P >= 1 && total_T >= 0, PSPO_ERR_INVALID_ARG, "need P >= 1 and total_T >= 0");
+  PSPO_REQUIRE(variant >= PSPO_DESIGN_OPTIMIZED && variant <= PSPO_DESIGN_TIME_PRIOR, PSPO_ERR_INVALID_ARG,
+               "unknown design variant");
+  PSPO_REQUIRE(std::isfinite(budget) && budget > 0.0, PSPO_ERR_INVALID_ARG, "budget must be finite and > 0");
+  PSPO_REQUIRE(std::isfinite(lambda) && lambda >= 0.0, PSPO_ERR_INVALID_ARG, "lambda must be finite and >= 0");
+  if (total_T == 0) return PSPO_OK;
+  PSPO_REQUIRE(w && xi_off && xi, PSPO_ERR_INVALID_ARG, "null pointer");
+  PSPO_REQUIRE(aligned(w, 8) && aligned(xi_off, 8) && aligned(xi, 8), PSPO_ERR_INVALID_ARG,
+               "misaligned pointer");
+  PSPO_REQUIRE(workspace && aligned(workspace, 256), PSPO_ERR_INVALID_ARG,
+               "workspace must be non-NULL and 256-byte aligned");
+  PSPO_REQUIRE(workspace_bytes >= pspo_design_workspace_bytes(total_T), PSPO_ERR_WORKSPACE,
+               "workspace too small: need " + std::to_string(pspo_design_workspace_bytes(total_T)) + " bytes");
+  if (int rc = require_gfx950()) return rc;
+  char* ws = static_cast<char*>(workspace);
+  int32_t* bstart = reinterpret_cast<int32_t*>(ws);
+  int32_t* blen = reinterpret_cast<int32_t*>(ws + round_up(total_T * 4, 256));
+  double* bval = reinterpret_cast<double*>(ws + 2 * round_up(total_T * 4, 256));
+  hipLaunchKernelGGL(design_cutoffs_kernel, dim3((unsigned)P), dim3(64), 0, stream, w, xi_off, budget, variant,
+                     lambda, xi, bstart, blen, bval, err_flag);
+  PSPO_HIP_CHECK(hipGetLastError());
+  return PSPO_OK;
+}
+
+}  // extern "C"

@@ -33,6 +33,11 @@ _SIGNATURES = {
     "pspo_loss_fwd_bwd": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _I32, _I32, _I32, _I32,
                                          _F32, _F32, _F32, _U32, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
     "pspo_score_proxy_workspace_bytes": (_SZ, [_I32, _I32, _I32]),
+    "pspo_design_weights": (ctypes.c_int, [_P, _P, _P, _I32, _P, _P, _P, _P, _I32, _I32, _I64,
+                                           _P, _P, _P, _P, _P]),
+    "pspo_design_workspace_bytes": (_SZ, [_I64]),
+    "pspo_design_cutoffs": (ctypes.c_int, [_P, _P, _I32, _I64, ctypes.c_double, _I32, ctypes.c_double,
+                                           _P, _P, _SZ, _P, _P]),
     "pspo_score_proxy": (ctypes.c_int, [_P, _P, _P, _I32, _I32, _I32, _P, _P, _P, _P, _P, _SZ, _P]),
 }
 
@@ -241,3 +246,47 @@ def score_proxy(hidden, w_head, target, N: int, want_logp: bool = True, want_p_s
         _ptr(gamma), _ptr(logp), _ptr(p_sq), _ptr(err_flag), _ptr(workspace), workspace.numel(), _stream()))
     return dict(gamma=gamma[:N], logp=None if logp is None else logp[:N],
                 p_sq=None if p_sq is None else p_sq[:N], workspace=workspace)
+
+
+PSPO_DESIGN_OPTIMIZED, PSPO_DESIGN_HEURISTIC, PSPO_DESIGN_UNIFORM, PSPO_DESIGN_TIME_PRIOR = 0, 1, 2, 3
+
+
+def design_weights(gamma, topk_ids, topk_logp, lengths, full_off, rewards, xi_off, P: int, K: int,
+                   total_T: int, want_parts: bool = False, err_flag: Optional[torch.Tensor] = None) -> dict:
+    """Per-step weights w_t = gbar_t u_t of the cutoff design (float64, xi_off layout)."""
+    _dev(gamma, torch.float32, "gamma")
+    _dev(topk_ids, torch.int32, "topk_ids")
+    _dev(topk_logp, torch.float32, "topk_logp")
+    _dev(lengths, torch.int32, "lengths")
+    _dev(full_off, torch.int32, "full_off")
+    _dev(rewards, torch.float32, "rewards")
+    _dev(xi_off, torch.int64, "xi_off")
+    if topk_ids.dim() != 2 or topk_ids.shape != topk_logp.shape:
+        raise ValueError("topk_ids and topk_logp must be [S, k] of the same shape")
+    dev = gamma.device
+    w = torch.empty(max(total_T, 1), dtype=torch.float64, device=dev)
+    gb = torch.empty_like(w) if want_parts else None
+    u = torch.empty_like(w) if want_parts else None
+    if err_flag is not None:
+        _dev(err_flag, torch.int32, "err_flag")
+    _check(load().pspo_design_weights(_ptr(gamma), _ptr(topk_ids), _ptr(topk_logp), topk_ids.shape[1],
+                                      _ptr(lengths), _ptr(full_off), _ptr(rewards), _ptr(xi_off), P, K,
+                                      total_T, _ptr(w), _ptr(gb), _ptr(u), _ptr(err_flag), _stream()))
+    return dict(w=w[:total_T], gamma_bar=None if gb is None else gb[:total_T], u=None if u is None else u[:total_T])
+
+
+def design_cutoffs(w, xi_off, P: int, total_T: int, budget: float, variant: int = PSPO_DESIGN_OPTIMIZED,
+                   lam: float = 0.0, out: Optional[torch.Tensor] = None,
+                   err_flag: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Survival tables xi (float64, xi_off layout) minimising sum w/xi under the budget."""
+    _dev(w, torch.float64, "w")
+    _dev(xi_off, torch.int64, "xi_off")
+    dev = w.device
+    xi = out if out is not None else torch.empty(max(total_T, 1), dtype=torch.float64, device=dev)
+    _dev(xi, torch.float64, "xi")
+    ws = torch.empty(max(int(load().pspo_design_workspace_bytes(total_T)), 256), dtype=torch.uint8, device=dev)
+    if err_flag is not None:
+        _dev(err_flag, torch.int32, "err_flag")
+    _check(load().pspo_design_cutoffs(_ptr(w), _ptr(xi_off), P, total_T, float(budget), int(variant), float(lam),
+                                      _ptr(xi), _ptr(ws), ws.numel(), _ptr(err_flag), _stream()))
+    return xi[:total_T]

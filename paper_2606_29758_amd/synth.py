@@ -255,3 +255,26 @@ def make_workload(cfg, with_matrices: bool = True) -> Workload:
     return Workload(cfg=cfg, lengths=lengths, horizon=horizon, xi=xi, xi_off=xi_off,
                     rewards=rewards, advantage=advantage, target_full=target_full,
                     lp_noise=lp_noise, hidden_bits=hidden_bits, w_bits=w_bits)
+
+
+def make_topk(wl: "Workload", k: int = 16, pool: int = 64, seed: int = 0):
+    """Synthetic top-k next-token lists of every completion token, in the shape a
+    rollout engine reports them: k distinct token ids per row, log-probs sorted in
+    decreasing order, with total mass below one.  The ids of one prompt's rows are
+    drawn from a pool of `pool` ids so that the lists of different completions
+    overlap.  Returns (ids int32 [S, k], logp float32 [S, k])."""
+    cfg = wl.cfg
+    rng = np.random.default_rng(np.random.SeedSequence([cfg.data_seed, 7919, seed]))
+    S = int(wl.total_tokens)
+    ids = np.empty((S, k), dtype=np.int32)
+    pools = [rng.choice(cfg.V, size=pool, replace=False) for _ in range(cfg.P)]
+    off = 0
+    for r, T in enumerate(wl.lengths):
+        p = r // cfg.K
+        for j in range(int(T)):
+            ids[off + j] = pools[p][rng.permutation(pool)[:k]]
+        off += int(T)
+    mass = rng.uniform(0.5, 0.95, S)
+    probs = -np.sort(-rng.dirichlet(np.full(k, 0.3), S), axis=1) * mass[:, None]
+    probs = np.maximum(probs, 1e-30)
+    return ids, np.log(probs).astype(np.float32)

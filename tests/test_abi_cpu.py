@@ -29,14 +29,14 @@ def _declared():
 
 def test_exports_every_declared_symbol(lib):
     names = _declared()
-    assert len(names) == 10
+    assert len(names) == 13
     for name in names:
         assert hasattr(lib, name), name
     assert sorted(pspo.exported_symbols()) == names
 
 
 def test_version_and_status_strings(lib):
-    assert lib.pspo_abi_version() == 3
+    assert lib.pspo_abi_version() == 4
     assert lib.pspo_status_string(0) == b"PSPO_OK"
     assert lib.pspo_status_string(3) == b"PSPO_ERR_WORKSPACE"
     assert lib.pspo_status_string(99) == b"PSPO_ERR_UNKNOWN"
@@ -179,6 +179,43 @@ def test_score_proxy_workspace_bytes(lib):
     # three float32 partials per (256-row vocabulary tile, token) plus two per-token arrays
     b = lib.pspo_score_proxy_workspace_bytes(1000, 3584, 152064)
     assert b >= 3 * 594 * 1024 * 4 + 2 * 1024 * 4
+
+
+def test_design_argument_errors(lib):
+    def weights(**kw):
+        a = dict(g=FAKE, ids=FAKE, lp=FAKE, k=16, len=FAKE, off=FAKE, rew=FAKE, xo=FAKE, P=2, K=8, T=100,
+                 w=FAKE, gb=None, u=None)
+        a.update(kw)
+        return lib.pspo_design_weights(a["g"], a["ids"], a["lp"], a["k"], a["len"], a["off"], a["rew"], a["xo"],
+                                       a["P"], a["K"], a["T"], a["w"], a["gb"], a["u"], None, None)
+    assert weights(T=0, g=None, w=None) == OK          # nothing to do, no device work
+    assert weights(P=0) == INVALID
+    assert weights(K=0) == INVALID
+    assert weights(T=-1) == INVALID
+    assert weights(K=65) == UNSUPPORTED
+    assert weights(k=0) == UNSUPPORTED
+    assert weights(K=16, k=17) == UNSUPPORTED          # K * topk > 256
+    assert weights(w=None) == INVALID
+    assert weights(gb=ctypes.c_void_p((1 << 20) + 4)) == INVALID
+
+    def cutoffs(**kw):
+        T = kw.get("T", 100)
+        a = dict(w=FAKE, xo=FAKE, P=2, T=T, B=128.0, v=0, lam=0.0, xi=FAKE, ws=FAKE,
+                 wsb=lib.pspo_design_workspace_bytes(max(T, 0)))
+        a.update(kw)
+        return lib.pspo_design_cutoffs(a["w"], a["xo"], a["P"], a["T"], a["B"], a["v"], a["lam"], a["xi"], a["ws"],
+                                       a["wsb"], None, None)
+    assert cutoffs(T=0, w=None, xi=None, ws=None) == OK
+    assert cutoffs(P=0) == INVALID
+    assert cutoffs(v=4) == INVALID
+    assert cutoffs(B=0.0) == INVALID
+    assert cutoffs(B=float("nan")) == INVALID
+    assert cutoffs(lam=-1.0) == INVALID
+    assert cutoffs(xi=None) == INVALID
+    assert cutoffs(ws=None) == INVALID
+    assert cutoffs(wsb=64) == WORKSPACE
+    assert lib.pspo_design_workspace_bytes(-1) == 0
+    assert lib.pspo_design_workspace_bytes(1000) >= 16 * 1000
 
 
 def test_binding_refuses_host_tensors():

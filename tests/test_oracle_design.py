@@ -132,7 +132,7 @@ def test_proxy_weights_full_distributions():
             i += 1
     assert i == len(out["w"])
     np.testing.assert_allclose(out["w"], out["gbar"] * out["u"])
-    assert np.all(out["u"] >= -1e-15) and np.all(out["u"] <= 0.5)
+    assert np.all(out["u"] >= 0) and np.all(out["u"] <= 0.5)
 
 
 def test_u_is_zero_for_equal_rewards_and_bounds_the_reward_variance():
