@@ -60,9 +60,9 @@ def parse():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--cpu-tokens", type=int, default=4096)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--pass", dest="which", choices=["update", "proxy"], default="update",
-                    help="update: the policy-update hot path (default); proxy: the forward-only "
-                         "output-head score proxy over every completion token")
+    ap.add_argument("--pass", dest="which", choices=["update", "xi"], default="update",
+                    help="update: the policy-update hot path (default); xi: computing the cutoff "
+                         "tables (score proxy over every completion token + cutoff design)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a device copy of known size (HBM counter calibration) and exit")
     return ap.parse_args()
@@ -104,7 +104,9 @@ def cpu_baseline(wl, logp_old, ntok, seed):
 
 
 def bench_proxy(args):
-    """Forward-only score-proxy pass (gamma, log p(o)) over every completion token."""
+    """The "Computing xi" stage before an update: the output-head score proxy of every
+    completion token on the matrix cores, the per-step weights and the designed survival
+    tables (budget 128, the paper's default)."""
     import torch
     from paper_2606_29758_amd import pipeline, pspo, synth
 
@@ -112,44 +114,81 @@ def bench_proxy(args):
     cfg = wl.cfg
     dw = pipeline.upload(wl, np.zeros(wl.total_tokens, dtype=np.float32))
     N = int(wl.total_tokens)
-    ws = torch.empty(pspo.score_proxy_workspace_bytes(N, cfg.d, cfg.V), dtype=torch.uint8, device="cuda")
-    err = torch.zeros(1, dtype=torch.int32, device="cuda")
-    run = lambda: pspo.score_proxy(dw.hidden_full, dw.w_head, dw.target_full, N, workspace=ws, err_flag=err)
+    ids, logp = synth.make_topk(wl)
+    dev = "cuda"
+    t_ids = torch.from_numpy(ids).to(dev)
+    t_logp = torch.from_numpy(logp).to(dev)
+    full_off = torch.from_numpy(np.concatenate([[0], np.cumsum(wl.lengths)]).astype(np.int32)).to(dev)
+    rewards = torch.from_numpy(wl.rewards.astype(np.float32)).to(dev)
+    total_T = int(wl.xi_off[-1])
+    ws = torch.empty(pspo.score_proxy_workspace_bytes(N, cfg.d, cfg.V), dtype=torch.uint8, device=dev)
+    xi = torch.empty(total_T, dtype=torch.float64, device=dev)
+    err = torch.zeros(1, dtype=torch.int32, device=dev)
+    budget = 128.0
+    stream = torch.cuda.current_stream()
+    ev = lambda: torch.cuda.Event(enable_timing=True)
+
+    def run(marks=None):
+        if marks:
+            marks[0].record(stream)
+        prox = pspo.score_proxy(dw.hidden_full, dw.w_head, dw.target_full, N, want_logp=False,
+                                workspace=ws, err_flag=err)
+        if marks:
+            marks[1].record(stream)
+        wts = pspo.design_weights(prox["gamma"], t_ids, t_logp, dw.lengths, full_off, rewards, dw.xi_off,
+                                  cfg.P, cfg.K, total_T, err_flag=err)
+        pspo.design_cutoffs(wts["w"], dw.xi_off, cfg.P, total_T, budget, out=xi, err_flag=err)
+
     for _ in range(args.warmup):
         run()
     torch.cuda.synchronize()
-    stream = torch.cuda.current_stream()
-    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    s, e = ev(), ev()
+    proxy_ms = []
     s.record(stream)
     for _ in range(args.steps):
-        run()
+        m = (ev(), ev())
+        run(m)
+        proxy_ms.append(m)
     e.record(stream)
     torch.cuda.synchronize()
     ms = s.elapsed_time(e) / args.steps
+    pms = float(np.mean([a.elapsed_time(b) for a, b in proxy_ms]))
     assert int(err.item()) == 0, "device error flag raised"
     flops = 2.0 * N * cfg.V * cfg.d
-    achieved = flops / (ms * 1e-3) / 1e12
+    achieved = flops / (pms * 1e-3) / 1e12
     result = {
-        "metric": "completion tokens/sec for the output-head score proxy pass (forward only); % of bf16 MFMA peak",
+        "metric": "completion tokens/sec for computing xi (score proxy on the matrix cores + cutoff design); "
+                  "% of bf16 MFMA peak",
         "value": N / (ms * 1e-3), "unit": "completion tokens/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
-        "config": {"workload": f"{args.workload}: every completion token, d={cfg.d}, V={cfg.V}", "tokens": N},
+        "config": {"workload": f"{args.workload}: every completion token, d={cfg.d}, V={cfg.V}, top-16 lists, "
+                               f"budget {budget:g}", "tokens": N, "steps_designed": total_T},
+        "score_proxy_ms": pms, "design_ms": ms - pms,
         "roofline": {"bound": "mfma", "kernel": "pspo_score_proxy (forward bf16 MFMA kernel + two-sum epilogue)",
                      "flops": "2 N V d per call", "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None},
     }
     if not args.no_cpu_baseline:
         from threadpoolctl import threadpool_info
+        from oracle import cutoff_design as ocd
         from oracle import score_proxy as osp
         n = min(args.cpu_tokens, N)
         t0 = time.perf_counter()
-        osp.score_proxy(wl.hidden_bits[:n], wl.w_bits, wl.target_full[:n])
+        g = osp.score_proxy(wl.hidden_bits[:n], wl.w_bits, wl.target_full[:n])["gamma"]
+        # the design of the first completion's prompt, on its first n tokens
+        L = np.minimum(wl.lengths[:cfg.K], max(n // cfg.K, 1))
+        off = np.concatenate([[0], np.cumsum(wl.lengths[:cfg.K])])
+        rows = np.concatenate([np.arange(off[k], off[k] + L[k]) for k in range(cfg.K)])
+        gs = np.concatenate([g, np.zeros(max(0, rows.max() + 1 - n))])[rows]
+        w = ocd.proxy_weights(gs, ids[rows], logp[rows], L, wl.rewards[:cfg.K], 1, cfg.K)["w"]
+        ocd.design_xi(w, budget)
         dt = time.perf_counter() - t0
         threads = max([p.get("num_threads", 1) for p in threadpool_info() if p.get("user_api") == "blas"] or [1])
         result["cpu_baseline"] = {"value": n / dt, "unit": "completion tokens/s", "cores": int(threads),
                                   "kind": "oracle",
-                                  "sample": f"gamma of the first {n} completion tokens (float64 numpy, {dt:.1f} s)"}
+                                  "sample": f"score proxy of the first {n} completion tokens and the design of one "
+                                            f"prompt over them (float64 numpy, {dt:.1f} s)"}
     print(json.dumps(result), flush=True)
 
 
@@ -162,7 +201,7 @@ def main():
     if args.copy_calibration:
         copy_calibration()
         return
-    if args.which == "proxy":
+    if args.which == "xi":
         bench_proxy(args)
         return
 
