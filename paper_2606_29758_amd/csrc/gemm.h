@@ -77,6 +77,11 @@ struct GemmShape {
   // Tiles outside the bound exit at once; a shorter K shortens the loop.
   const int32_t* dyn = nullptr;
   int dyn_dim = kDynNone;
+  // K-blocked operands: element (r, k) of a K-blocked operand with row count
+  // R lives at ((k / 32) * R + r) * 32 + k % 32, so each 32-deep K step of a
+  // panel is one contiguous block; its lda / ldb is then R * 32 (elements from
+  // one K step to the next) instead of the row stride.
+  bool a_kb = false, b_kb = false;
 };
 
 // Accumulator (i, j, r) of lane `lane` in wave (wm, wn) holds
@@ -197,9 +202,11 @@ void gemm_nt_kernel(GemmShape g, Epi epi) {
     const int ra = min(tm * kTileM + row, M - 1);
     int rb = min(tn * kTileN + row, N - 1);
     if (g.b_rows != nullptr) rb = g.b_rows[rb];
-    src[0][q] = reinterpret_cast<const unsigned char*>(g.A) + (int64_t)ra * g.lda * 2 + chunk * 16;
-    src[1][q] = reinterpret_cast<const unsigned char*>(g.B) + (int64_t)rb * g.ldb * 2 + chunk * 16;
+    src[0][q] = reinterpret_cast<const unsigned char*>(g.A) + (int64_t)ra * (g.a_kb ? kTileK : g.lda) * 2 + chunk * 16;
+    src[1][q] = reinterpret_cast<const unsigned char*>(g.B) + (int64_t)rb * (g.b_kb ? kTileK : g.ldb) * 2 + chunk * 16;
   }
+  // bytes from one K step of an operand to the next
+  const int64_t kstep_a = (g.a_kb ? g.lda : kTileK) * 2, kstep_b = (g.b_kb ? g.ldb : kTileK) * 2;
   const int wave_lds = wave * 64 * kLdsRow;
 
   // MFMA operand reads: block i of A is rows wm*128 + i*16 + lane%16, K chunk
@@ -244,7 +251,7 @@ void gemm_nt_kernel(GemmShape g, Epi epi) {
   // Load instruction q (0..7) of a step: operand q/4, 16-row group q%4.
   auto issue_load = [&](int kt, int stage, auto q) {
     constexpr int o = decltype(q)::value / 4, r = decltype(q)::value % 4;
-    const int64_t koff = (int64_t)max(min(kt, nk - 1), 0) * (kTileK * 2);
+    const int64_t koff = (int64_t)max(min(kt, nk - 1), 0) * (o == 0 ? kstep_a : kstep_b);
     __builtin_amdgcn_global_load_lds(src[o][r] + koff,
                                      (lds_void*)(lds + stage * kLdsStage + wave_lds + o * kLdsOperand +
                                                  r * 16 * kLdsRow),

@@ -105,8 +105,8 @@ struct EpiForward {
 
 // Backward logit gradient for one vocabulary chunk: rows = vocabulary rows
 // v0 + vl (A = W[v0:]), columns = the compacted tokens that carry gradient
-// (column t is token tok[t], t < *n_dev).  Writes bf16 Delta to dT[vl][t]
-// and dN[t][vl]; zero outside t < *n_dev, v < V.
+// (column t is token tok[t], t < *n_dev).  Writes bf16 Delta in both K-blocked
+// layouts (vocabulary rows for dW, token rows for dH); zero outside t < *n_dev, v < V.
 // The 256 x 256 bf16 tile goes through LDS once per layout so both global
 // layouts are written as whole 512-byte rows (16 bytes per lane).
 struct EpiDelta {
@@ -114,10 +114,10 @@ struct EpiDelta {
   const int32_t* target;
   const float* lse;
   const float* delta;
-  uint16_t* dT;
-  int64_t ldT;
-  uint16_t* dN;
-  int64_t ldN;
+  uint16_t* dT;          // K-blocked [Npad/32][rT][32]: rows = vocabulary entries of the chunk, K = tokens
+  int64_t rT;
+  uint16_t* dN;          // K-blocked [Vc/32][rN][32]: rows = tokens, K = vocabulary entries of the chunk
+  int64_t rN;
   const int32_t* tok;    // column t of the tile is token tok[t] (columns t < *n_dev)
   const int32_t* n_dev;
 
@@ -126,12 +126,15 @@ struct EpiDelta {
     return row * 512 + ((((col >> 3) ^ (row & 31)) << 4) | ((col & 7) << 1));
   }
 
-  // Copies the LDS tile (256 rows of 256 bf16) to rows of `dst` with stride `ld`.
-  __device__ static __forceinline__ void copy_out(const unsigned char* tile, uint16_t* dst, int64_t ld) {
+  // Copies the LDS tile (256 rows of 256 bf16) into a K-blocked matrix with R
+  // rows per K block, `dst` pointing at the tile's first row in its first K
+  // block: the tile's 8 column blocks of 32 become 8 runs of 256 x 64 bytes,
+  // each contiguous (16 KB), written 16 bytes per lane.
+  __device__ static __forceinline__ void copy_out_kb(const unsigned char* tile, uint16_t* dst, int64_t R) {
     for (int c = threadIdx.x; c < 256 * 32; c += kGemmThreads) {
-      const int row = c >> 5, chunk = c & 31;
-      const u32x4 v = *reinterpret_cast<const u32x4*>(tile + row * 512 + ((chunk ^ (row & 31)) << 4));
-      *reinterpret_cast<u32x4*>(dst + (int64_t)row * ld + chunk * 8) = v;
+      const int blk = c >> 10, row = (c >> 2) & 255, q = c & 3;
+      const u32x4 v = *reinterpret_cast<const u32x4*>(tile + row * 512 + (((blk * 4 + q) ^ (row & 31)) << 4));
+      *reinterpret_cast<u32x4*>(dst + ((int64_t)blk * R + row) * kTileK + q * 8) = v;
     }
   }
 
@@ -172,7 +175,8 @@ struct EpiDelta {
       }
     }
     __syncthreads();
-    copy_out(tile, dN + (int64_t)(tn * kTileN) * ldN + tm * kTileM, ldN);
+    // token-major tile: rows tn*256.., K blocks (tm*256)/32..
+    copy_out_kb(tile, dN + ((int64_t)(tm * (kTileM / kTileK)) * rN + tn * kTileN) * kTileK, rN);
     __syncthreads();
     // vocabulary-major layout: LDS row = vocabulary entry
 #pragma unroll
@@ -187,7 +191,8 @@ struct EpiDelta {
         }
     }
     __syncthreads();
-    copy_out(tile, dT + (int64_t)(tm * kTileM) * ldT + tn * kTileN, ldT);
+    // vocabulary-major tile: rows tm*256.., K blocks (tn*256)/32..
+    copy_out_kb(tile, dT + ((int64_t)(tn * (kTileN / kTileK)) * rT + tm * kTileM) * kTileK, rT);
   }
 };
 
@@ -251,18 +256,18 @@ struct EpiDH {
 // ---------------------------------------------------------------------------
 
 // Transposed, zero-padded copy of a bf16 [rows x cols] matrix, in blocks of
-// `chunk` source rows: source row r, column c goes to
-//   dst[(r / chunk) * cols * ld + c * ld + r % chunk]   (0 for r >= rows),
-// i.e. block b is the [cols x chunk] transpose of rows [b*chunk, (b+1)*chunk)
-// with row stride ld >= chunk.  64 x 64 tiles through LDS; cols, chunk and the
-// padded row count are multiples of 64.
+// `chunk` source rows, each block K-blocked: source row r, column c goes to
+//   dst[(r / chunk) * cols * chunk + (((r % chunk) / 32) * cols + c) * 32 + r % 32]
+// (0 for r >= rows), i.e. block b is the [cols x chunk] transpose of rows
+// [b*chunk, (b+1)*chunk) with each 32-deep K step of its cols rows contiguous.
+// 64 x 64 tiles through LDS; cols, chunk and the padded row count are
+// multiples of 64.
 // Optionally, row r of the source is row rmap[r] of `src` and only the first
 // min(rows, *n_dev) rows are present; 64-row blocks wholly past that count are
 // not written (no product reads them).
 __global__ __launch_bounds__(256) void transpose_pad_kernel(const uint16_t* __restrict__ src, int rows, int cols,
                                                             int64_t ld_src, uint16_t* __restrict__ dst,
-                                                            int64_t chunk, int64_t ld,
-                                                            const int32_t* __restrict__ rmap,
+                                                            int64_t chunk, const int32_t* __restrict__ rmap,
                                                             const int32_t* __restrict__ n_dev) {
   __shared__ uint16_t tile[64][66];
   const int c0 = blockIdx.x * 64, r0 = blockIdx.y * 64;
@@ -276,9 +281,9 @@ __global__ __launch_bounds__(256) void transpose_pad_kernel(const uint16_t* __re
     tile[rr][tx] = (r < rows) ? src[(int64_t)(rmap ? rmap[r] : r) * ld_src + c0 + tx] : (uint16_t)0;
   }
   __syncthreads();
-  const int64_t block = r0 / chunk, rin = r0 % chunk;
-  uint16_t* out = dst + block * cols * ld + rin;
-  for (int cc = ty; cc < 64; cc += 4) out[(int64_t)(c0 + cc) * ld + tx] = tile[tx][cc];
+  const int64_t block = r0 / chunk, rin = r0 % chunk + tx;
+  uint16_t* out = dst + block * cols * chunk + ((rin / kTileK) * cols) * kTileK + rin % kTileK;
+  for (int cc = ty; cc < 64; cc += 4) out[(int64_t)(c0 + cc) * kTileK] = tile[tx][cc];
 }
 
 __global__ void fill_f32_kernel(float* __restrict__ p, int64_t n, float v) {
@@ -487,14 +492,9 @@ __global__ __launch_bounds__(kFinThreads) void reduce_loss_kernel(int nblk, cons
 // Workspace plan
 // ---------------------------------------------------------------------------
 
-// Row strides of the workspace matrices are padded by kStridePad elements
-// (128 bytes): power-of-two strides would send every row of a tile to the same
-// memory channels.
-constexpr int64_t kStridePad = 64;
 
 struct Plan {
   int64_t Npad, Vpad, Vc, ntv, nfin;
-  int64_t ldH, ldW, ldN, ldT;   // row strides of H^T, W^T blocks, Delta [t][v], Delta^T [v][t]
   int64_t off_pm, off_pl, off_zt, off_lse, off_delta, off_fidx, off_fpos, off_nfwd, off_idx, off_nact, off_blk, off_ht,
       off_wt, off_dn, off_dt, total;
 };
@@ -506,10 +506,6 @@ Plan make_plan(int64_t N, int64_t d, int64_t V) {
   p.Vc = p.Vpad < kVocabChunk ? p.Vpad : kVocabChunk;
   p.ntv = p.Vpad / kTileM;
   p.nfin = (N + kFinThreads - 1) / kFinThreads;
-  p.ldH = p.Npad + kStridePad;
-  p.ldW = p.Vc + kStridePad;
-  p.ldN = p.Vc + kStridePad;
-  p.ldT = p.Npad + kStridePad;
   int64_t o = 0;
   auto take = [&](int64_t bytes) {
     const int64_t at = o;
@@ -527,10 +523,10 @@ Plan make_plan(int64_t N, int64_t d, int64_t V) {
   p.off_idx = take(p.Npad * 4);
   p.off_nact = take(4);
   p.off_blk = take((p.nfin > 0 ? p.nfin : 1) * 5 * 8);
-  p.off_ht = take(d * p.ldH * 2);
-  p.off_wt = take(d * ((p.Vpad + p.Vc - 1) / p.Vc) * p.ldW * 2);   // [V/Vc][d][ldW] blocks
-  p.off_dn = take(p.Npad * p.ldN * 2);
-  p.off_dt = take(p.Vc * p.ldT * 2);
+  p.off_ht = take(d * p.Npad * 2);                                  // K-blocked [Npad/32][d][32]
+  p.off_wt = take(d * ((p.Vpad + p.Vc - 1) / p.Vc) * p.Vc * 2);     // per chunk: K-blocked [Vc/32][d][32]
+  p.off_dn = take(p.Npad * p.Vc * 2);                               // K-blocked [Vc/32][Npad][32]
+  p.off_dt = take(p.Vc * p.Npad * 2);                               // K-blocked [Npad/32][Vc][32]
   p.total = o;
   return p;
 }
@@ -651,10 +647,10 @@ int pspo_loss_fwd_bwd(const uint16_t* hidden, const uint16_t* w_head, const int3
   PSPO_HIP_CHECK(hipGetLastError());
   // 5. K-contiguous copies for the gradient products
   hipLaunchKernelGGL(transpose_pad_kernel, dim3(d / 64, (unsigned)(pl.Npad / 64)), dim3(256), 0, stream, hidden, N,
-                     d, (int64_t)d, hT, pl.Npad, pl.ldH, act_idx, n_act);   // H[active]^T [d x Npad]
+                     d, (int64_t)d, hT, pl.Npad, act_idx, n_act);   // H[active]^T [d x Npad]
   PSPO_HIP_CHECK(hipGetLastError());
   hipLaunchKernelGGL(transpose_pad_kernel, dim3(d / 64, (unsigned)(pl.Vpad / 64)), dim3(256), 0, stream, w_head, V,
-                     d, (int64_t)d, wT, pl.Vc, pl.ldW, nullptr, nullptr);  // per chunk: W[chunk]^T [d x Vc]
+                     d, (int64_t)d, wT, pl.Vc, nullptr, nullptr);  // per chunk: W[chunk]^T [d x Vc]
   PSPO_HIP_CHECK(hipGetLastError());
   // 6. backward, one vocabulary chunk at a time; every product is bounded by
   //    the active-token count in device memory
@@ -663,17 +659,18 @@ int pspo_loss_fwd_bwd(const uint16_t* hidden, const uint16_t* w_head, const int3
     const int ctiles = (int)(vc / kTileM);
     {
       GemmShape g{w_head + v0 * d, d, (int)(V - v0), hidden, d, N, d, ctiles, tiles_tok, act_idx, n_act, kDynN};
-      EpiDelta e{V, N, (int)v0, target, lse, delta, dT, pl.ldT, dN, pl.ldN, act_idx, n_act};
+      EpiDelta e{V, N, (int)v0, target, lse, delta, dT, pl.Vc, dN, pl.Npad, act_idx, n_act};
       if (int rc = launch_gemm(g, e, stream)) return rc;
     }
     {
-      GemmShape g{dT, pl.ldT, (int)vc, hT, pl.ldH, d, (int)pl.Npad, ctiles, tiles_d, nullptr, n_act, kDynK};
+      GemmShape g{dT,      pl.Vc * kTileK, (int)vc, hT, (int64_t)d * kTileK, d, (int)pl.Npad, ctiles, tiles_d,
+                  nullptr, n_act, kDynK,     true,     true};
       EpiDW e{V, d, (int)v0, d_w_head, accumulate};
       if (int rc = launch_gemm(g, e, stream)) return rc;
     }
     {
-      GemmShape g{dN,       pl.ldN,   (int)pl.Npad, wT + (v0 / pl.Vc) * d * pl.ldW, pl.ldW, d, (int)vc, tiles_tok,
-                  tiles_d, nullptr, n_act, kDynM};
+      GemmShape g{dN,      pl.Npad * kTileK, (int)pl.Npad, wT + (v0 / pl.Vc) * d * pl.Vc, (int64_t)d * kTileK, d,
+                  (int)vc, tiles_tok, tiles_d, nullptr, n_act, kDynM, true, true};
       EpiDH e{N, d, d_hidden, v0 == 0, act_idx, n_act};
       if (int rc = launch_gemm(g, e, stream)) return rc;
     }
