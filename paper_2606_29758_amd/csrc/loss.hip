@@ -28,7 +28,6 @@
 namespace pspo {
 namespace {
 
-constexpr int64_t kVocabChunk = 16384;   // rows of W per backward chunk
 constexpr float kNegInf = -INFINITY;
 
 // ---------------------------------------------------------------------------
@@ -503,7 +502,20 @@ Plan make_plan(int64_t N, int64_t d, int64_t V) {
   Plan p{};
   p.Npad = round_up(N > 0 ? N : 1, kTileN);
   p.Vpad = round_up(V, kTileM);
-  p.Vc = p.Vpad < kVocabChunk ? p.Vpad : kVocabChunk;
+  // Vocabulary rows per backward chunk: a multiple of 256 tiles such that the
+  // dW product of a chunk ((Vc / 256) x ceil(d / 256) tiles of very long K) fills
+  // whole rounds of the 256 CUs (d = 3584: 14 column tiles, 128 row tiles,
+  // exactly 7 rounds); whole vocabulary if smaller.
+  {
+    int64_t td = (d + kTileN - 1) / kTileN, a = td, b = 256;
+    while (b) {
+      const int64_t r = a % b;
+      a = b;
+      b = r;
+    }
+    const int64_t rows = 256 / a * kTileM;
+    p.Vc = p.Vpad < rows ? p.Vpad : rows;
+  }
   p.ntv = p.Vpad / kTileM;
   p.nfin = (N + kFinThreads - 1) / kFinThreads;
   int64_t o = 0;
