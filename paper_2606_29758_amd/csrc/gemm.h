@@ -95,6 +95,25 @@ __device__ __forceinline__ int acc_row(int wm, int i, int r, int lane) {
 }
 __device__ __forceinline__ int acc_col(int wn, int j, int lane) { return wn * 128 + j * 16 + (lane & 15); }
 
+// The accumulator of column block j that sits in row `rel` of this lane's rows
+// (rel = row - (wm * 128 + (lane / 16) * 4); the lane holds rows i * 16 + r,
+// i < 8, r < 4), picked with selects only (no divergent branch per value).
+// Returns whether the lane holds that row.
+__device__ __forceinline__ bool acc_pick(const AccTile& acc, int j, int rel, float& value) {
+  float z = 0.f;
+  bool has = false;
+#pragma unroll
+  for (int i = 0; i < kBlocks; ++i)
+#pragma unroll
+    for (int r = 0; r < kAccPerBlock; ++r) {
+      const bool hit = rel == i * 16 + r;
+      z = hit ? acc.c[i][j][r] : z;
+      has = has || hit;
+    }
+  value = z;
+  return has;
+}
+
 __device__ __forceinline__ int chunk_swizzle(int row) { return ((row >> 1) ^ (row >> 2)) & 3; }
 
 // Tile of work-group blockIdx.x among the tiles_m x tiles_n tiles that cover

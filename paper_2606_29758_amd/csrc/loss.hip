@@ -50,23 +50,21 @@ struct EpiForward {
   __device__ __forceinline__ void apply(const AccTile& acc, int tm, int tn, int wm, int wn, int lane, float* smem) const {
     float* red = smem;  // [2 wave rows][256 columns][m, l]
     const int n = min(N, __builtin_amdgcn_readfirstlane(*n_dev));
+    const int vbase = tm * kTileM + acc_row(wm, 0, 0, lane);   // this lane's rows: vbase + i*16 + r
+    const bool full = (tm + 1) * kTileM <= V;                   // every row of the tile is a token id
 #pragma unroll
     for (int j = 0; j < kBlocks; ++j) {
       const int cl = acc_col(wn, j, lane);
       const int t = tn * kTileN + cl;
       const int tgt = (t < n) ? target[tok[t]] : -1;
+      float zv;
+      if (acc_pick(acc, j, tgt - vbase, zv)) zt[t] = zv;
       float m = kNegInf;
 #pragma unroll
       for (int i = 0; i < kBlocks; ++i)
 #pragma unroll
-        for (int r = 0; r < kAccPerBlock; ++r) {
-          const int v = tm * kTileM + acc_row(wm, i, r, lane);
-          const float x = acc.c[i][j][r];
-          if (v < V) {
-            m = fmaxf(m, x);
-            if (v == tgt) zt[t] = x;
-          }
-        }
+        for (int r = 0; r < kAccPerBlock; ++r)
+          if (full || vbase + i * 16 + r < V) m = fmaxf(m, acc.c[i][j][r]);
       m = fmaxf(m, __shfl_xor(m, 16));
       m = fmaxf(m, __shfl_xor(m, 32));
       float l = 0.f;
@@ -74,10 +72,8 @@ struct EpiForward {
 #pragma unroll
         for (int i = 0; i < kBlocks; ++i)
 #pragma unroll
-          for (int r = 0; r < kAccPerBlock; ++r) {
-            const int v = tm * kTileM + acc_row(wm, i, r, lane);
-            if (v < V) l += __expf(acc.c[i][j][r] - m);
-          }
+          for (int r = 0; r < kAccPerBlock; ++r)
+            if (full || vbase + i * 16 + r < V) l += __expf(acc.c[i][j][r] - m);
       }
       l += __shfl_xor(l, 16);
       l += __shfl_xor(l, 32);
@@ -140,7 +136,11 @@ struct EpiDelta {
   __device__ __forceinline__ void apply(AccTile& acc, int tm, int tn, int wm, int wn, int lane, float* smem) const {
     unsigned char* tile = reinterpret_cast<unsigned char*>(smem);
     const int n = min(N, __builtin_amdgcn_readfirstlane(*n_dev));
-    // Delta in place of the logits
+    const int vbase = v0 + tm * kTileM + acc_row(wm, 0, 0, lane);   // this lane's rows: vbase + i*16 + r
+    const bool full = v0 + (tm + 1) * kTileM <= V;                   // every row of the tile is a token id
+    // Delta in place of the logits, without a branch per value: columns past n
+    // have delta 0, and exp(min(z - lse, 0)) equals exp(z - lse) for the others
+    // (lse >= every logit) while staying finite for them
 #pragma unroll
     for (int j = 0; j < kBlocks; ++j) {
       const int t = tn * kTileN + acc_col(wn, j, lane);
@@ -153,9 +153,9 @@ struct EpiDelta {
       for (int i = 0; i < kBlocks; ++i)
 #pragma unroll
         for (int r = 0; r < kAccPerBlock; ++r) {
-          const int v = v0 + tm * kTileM + acc_row(wm, i, r, lane);
-          float dv = 0.f;
-          if (dl != 0.f && v < V) dv = dl * ((v == tgt ? 1.f : 0.f) - __expf(acc.c[i][j][r] - ls));
+          const int v = vbase + i * 16 + r;
+          float dv = dl * ((v == tgt ? 1.f : 0.f) - __expf(fminf(acc.c[i][j][r] - ls, 0.f)));
+          if (!full) dv = (v < V) ? dv : 0.f;
           acc.c[i][j][r] = dv;
         }
     }

@@ -43,23 +43,21 @@ struct EpiProxy {
 
   __device__ __forceinline__ void apply(const AccTile& acc, int tm, int tn, int wm, int wn, int lane, float* smem) const {
     float* red = smem;  // [2 wave rows][256 columns][m, S1, S2]
+    const int vbase = tm * kTileM + acc_row(wm, 0, 0, lane);   // this lane's rows: vbase + i*16 + r
+    const bool full = (tm + 1) * kTileM <= V;                   // every row of the tile is a token id
 #pragma unroll
     for (int j = 0; j < kBlocks; ++j) {
       const int cl = acc_col(wn, j, lane);
       const int t = tn * kTileN + cl;
       const int tgt = (t < N) ? target[t] : -1;
+      float zv;
+      if (acc_pick(acc, j, tgt - vbase, zv)) zt[t] = zv;
       float m = kNegInf;
 #pragma unroll
       for (int i = 0; i < kBlocks; ++i)
 #pragma unroll
-        for (int r = 0; r < kAccPerBlock; ++r) {
-          const int v = tm * kTileM + acc_row(wm, i, r, lane);
-          const float x = acc.c[i][j][r];
-          if (v < V) {
-            m = fmaxf(m, x);
-            if (v == tgt) zt[t] = x;
-          }
-        }
+        for (int r = 0; r < kAccPerBlock; ++r)
+          if (full || vbase + i * 16 + r < V) m = fmaxf(m, acc.c[i][j][r]);
       m = fmaxf(m, __shfl_xor(m, 16));
       m = fmaxf(m, __shfl_xor(m, 32));
       float s1 = 0.f, s2 = 0.f;
@@ -68,12 +66,11 @@ struct EpiProxy {
         for (int i = 0; i < kBlocks; ++i)
 #pragma unroll
           for (int r = 0; r < kAccPerBlock; ++r) {
-            const int v = tm * kTileM + acc_row(wm, i, r, lane);
-            if (v < V && v != tgt) {
-              const float e = __expf(acc.c[i][j][r] - m);
-              s1 += e;
-              s2 += e * e;
-            }
+            const int v = vbase + i * 16 + r;
+            // the target's own entry is left out (selected away, not subtracted)
+            const float e = ((full || v < V) && v != tgt) ? __expf(acc.c[i][j][r] - m) : 0.f;
+            s1 += e;
+            s2 += e * e;
           }
       }
       s1 += __shfl_xor(s1, 16);
