@@ -52,11 +52,24 @@ struct EpiForward {
     const int n = min(N, __builtin_amdgcn_readfirstlane(*n_dev));
     const int vbase = tm * kTileM + acc_row(wm, 0, 0, lane);   // this lane's rows: vbase + i*16 + r
     const bool full = (tm + 1) * kTileM <= V;                   // every row of the tile is a token id
+    // the targets of the lane's 8 columns, fetched together (two round trips, not 16)
+    int tgts[kBlocks];
+#pragma unroll
+    for (int j = 0; j < kBlocks; ++j) {
+      const int t = tn * kTileN + acc_col(wn, j, lane);
+      tgts[j] = t < n ? tok[t] : -1;
+    }
+#pragma unroll
+    for (int j = 0; j < kBlocks; ++j) asm volatile("" ::"v"(tgts[j]));   // keep the batch: no sinking
+#pragma unroll
+    for (int j = 0; j < kBlocks; ++j) tgts[j] = tgts[j] >= 0 ? target[tgts[j]] : -1;
+#pragma unroll
+    for (int j = 0; j < kBlocks; ++j) asm volatile("" ::"v"(tgts[j]));
 #pragma unroll
     for (int j = 0; j < kBlocks; ++j) {
       const int cl = acc_col(wn, j, lane);
       const int t = tn * kTileN + cl;
-      const int tgt = (t < n) ? target[tok[t]] : -1;
+      const int tgt = tgts[j];
       float zv;
       if (acc_pick(acc, j, tgt - vbase, zv)) zt[t] = zv;
       float m = kNegInf;
@@ -141,14 +154,27 @@ struct EpiDelta {
     // Delta in place of the logits, without a branch per value: columns past n
     // have delta 0, and exp(min(z - lse, 0)) equals exp(z - lse) for the others
     // (lse >= every logit) while staying finite for them
+    // per-column token data of the lane's 8 columns, fetched together
+    int tos[kBlocks];
+    float dls[kBlocks], lss[kBlocks];
+    int tgs[kBlocks];
 #pragma unroll
     for (int j = 0; j < kBlocks; ++j) {
       const int t = tn * kTileN + acc_col(wn, j, lane);
-      const bool tv = t < n;
-      const int to = tv ? tok[t] : 0;
-      const float dl = tv ? delta[to] : 0.f;
-      const float ls = tv ? lse[to] : 0.f;
-      const int tgt = tv ? target[to] : -1;
+      tos[j] = t < n ? tok[t] : -1;
+    }
+#pragma unroll
+    for (int j = 0; j < kBlocks; ++j) {
+      const bool tv = tos[j] >= 0;
+      dls[j] = tv ? delta[tos[j]] : 0.f;
+      lss[j] = tv ? lse[tos[j]] : 0.f;
+      tgs[j] = tv ? target[tos[j]] : -1;
+    }
+#pragma unroll
+    for (int j = 0; j < kBlocks; ++j) {
+      const float dl = dls[j];
+      const float ls = lss[j];
+      const int tgt = tgs[j];
 #pragma unroll
       for (int i = 0; i < kBlocks; ++i)
 #pragma unroll

@@ -45,11 +45,20 @@ struct EpiProxy {
     float* red = smem;  // [2 wave rows][256 columns][m, S1, S2]
     const int vbase = tm * kTileM + acc_row(wm, 0, 0, lane);   // this lane's rows: vbase + i*16 + r
     const bool full = (tm + 1) * kTileM <= V;                   // every row of the tile is a token id
+    // the targets of the lane's 8 columns, fetched together
+    int tgts[kBlocks];
+#pragma unroll
+    for (int j = 0; j < kBlocks; ++j) {
+      const int t = tn * kTileN + acc_col(wn, j, lane);
+      tgts[j] = t < N ? target[t] : -1;
+    }
+#pragma unroll
+    for (int j = 0; j < kBlocks; ++j) asm volatile("" ::"v"(tgts[j]));   // keep the batch: no sinking
 #pragma unroll
     for (int j = 0; j < kBlocks; ++j) {
       const int cl = acc_col(wn, j, lane);
       const int t = tn * kTileN + cl;
-      const int tgt = (t < N) ? target[t] : -1;
+      const int tgt = tgts[j];
       float zv;
       if (acc_pick(acc, j, tgt - vbase, zv)) zt[t] = zv;
       float m = kNegInf;
