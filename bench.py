@@ -60,6 +60,8 @@ def parse():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--cpu-tokens", type=int, default=4096)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-full-control", action="store_true",
+                    help="skip timing the full-trajectory control (every xi = 1) on the same batch")
     ap.add_argument("--pass", dest="which", choices=["update", "xi"], default="update",
                     help="update: the policy-update hot path (default); xi: computing the cutoff "
                          "tables (score proxy over every completion token + cutoff design)")
@@ -220,15 +222,21 @@ def main():
     for _ in range(args.warmup):
         step(args.seed, want_logp=False)
     torch.cuda.synchronize()
+    torch.cuda.reset_peak_memory_stats()
 
     loss_ms = []
-    starts, ends = [], []
+    starts, ends, pack_marks = [], [], []
     t_start, t_end = ev(), ev()
     torch.cuda.synchronize()
     t_start.record(stream)
     N = 0
     for _ in range(args.steps):
+        p0 = ev()
+        p0.record(stream)
         pk = step.sample_and_pack(args.seed)
+        p1 = ev()
+        p1.record(stream)
+        pack_marks.append((p0, p1))
         N = int(pk["n_tokens"].item())
         s, e = ev(), ev()
         s.record(stream)
@@ -241,7 +249,31 @@ def main():
     ms_step = t_start.elapsed_time(t_end) / args.steps
     loss_ms = [s.elapsed_time(e) for s, e in zip(starts, ends)]
     loss_avg = float(np.mean(loss_ms))
+    pack_avg = float(np.mean([a.elapsed_time(b) for a, b in pack_marks]))
     assert int(step.err.item()) == 0, "device error flag raised"
+    peak_bytes = torch.cuda.max_memory_allocated()
+
+    # the full-trajectory control on the same batch (every xi = 1: the standard, untruncated
+    # update): its loss-call time against the truncated one
+    full = None
+    if not args.no_full_control:
+        import dataclasses
+        dw_full = dataclasses.replace(dw, xi=torch.ones_like(dw.xi))
+        step_full = pipeline.Step(dw_full)
+        for _ in range(2):
+            step_full(args.seed, want_logp=False)
+        torch.cuda.synchronize()
+        pkf = step_full.sample_and_pack(args.seed)
+        Nf = int(pkf["n_tokens"].item())
+        fs, fe = ev(), ev()
+        fs.record(stream)
+        nrep = max(3, args.steps // 2)
+        for _ in range(nrep):
+            step_full.loss(pkf, Nf, want_logp=False)
+        fe.record(stream)
+        torch.cuda.synchronize()
+        full = {"tokens": Nf, "loss_call_ms": fs.elapsed_time(fe) / nrep}
+        del step_full, dw_full
     st = out["stats"].cpu().numpy()
     n_fwd = N - int(st[2])   # tokens of completions with A != 0: the forward's columns
     n_bwd = int(st[4])       # tokens with a nonzero logit-gradient row
@@ -288,6 +320,10 @@ def main():
             "parallelism": "single GPU",
         },
         "loss_call_ms": loss_avg,
+        "sample_pack_ms": pack_avg,
+        "memory": {"peak_device_bytes": int(peak_bytes),
+                   "loss_workspace_bytes": int(step.workspace.numel()),
+                   "logits_fp32_bytes_avoided": int(N) * int(cfg.V) * 4},
         "pct_bf16_peak": 100.0 * achieved / PEAK_BF16_TFLOPS,
         "dense_equivalent_tflops": dense_equiv,
         "roofline": {
@@ -302,6 +338,8 @@ def main():
             "traffic": traffic,
         },
     }
+    if full is not None:
+        result["full_trajectory_control"] = dict(full, prefix_vs_full_ratio=loss_avg / full["loss_call_ms"])
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(wl, logp_old, args.cpu_tokens, args.seed)
     print(json.dumps(result), flush=True)
