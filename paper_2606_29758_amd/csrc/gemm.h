@@ -2,112 +2,127 @@
 // with a pluggable epilogue.  Every contraction of the LM-head loss is one of
 // these "NT" products:
 //
-//   C[m][n] = sum_k A[m][k] * B[n][k],  A: [M x K], B: [N x K], both row-major
-//   with K contiguous (row strides lda / ldb in elements), K % 32 == 0, K > 0.
+//   C[m][n] = sum_k A[m][k] * B[n][k],  A: [M x K], B: [N x K].
 //
-// Tiling: a 256-thread work-group (4 wave64s in a 2 x 2 arrangement) owns a
-// 256 x 256 C tile; each wave owns 128 x 128 = 8 x 8 blocks of the
-// v_mfma_f32_16x16x32_bf16 instruction, i.e. 256 fp32 accumulators per lane
-// (the whole AGPR file).  On real (random) bf16 operands this instruction
-// sustains a markedly higher rate than the 32x32x16 form at the same LDS
-// traffic per flop (measured on MI355X: ~86% vs ~77% of peak in a pure MFMA
-// loop), so it is the one used.
+// Operands are K-blocked: element (r, k) of an operand with R rows per K block
+// sits at ((k / 32) * R + r) * 32 + k % 32, so the 32-deep K step of a panel of
+// consecutive rows is one contiguous block of 64-byte rows.  The caller pads
+// every operand: rows [0, tiles_m * 384) of A and [0, tiles_n * 256) of B must
+// be readable (their content only reaches output rows / columns the epilogue
+// masks), K % 32 == 0, and K-padding entries must be zero in both operands.
+//
+// Tiling: a 256-thread work-group (4 wave64s, 2 x 2) owns a 384 x 256 C tile;
+// each wave owns 192 x 128 = 12 x 8 blocks of v_mfma_f32_16x16x32_bf16, i.e.
+// 384 fp32 accumulators per lane: row blocks 0..7 in the 256 AGPRs, row blocks
+// 8..11 in 128 VGPRs.  A 384 x 256 tile moves 40 KB of operands per 32-deep K
+// step for 6.3 MFLOP (154 flop/byte, against 128 for a 256 x 256 tile): the
+// products are bound by the rate at which the CU's load path delivers operand
+// bytes while the matrix cores run, so fewer bytes per flop is what counts.
+// On random bf16 operands this tile runs 5-20% faster than 256 x 256 on the
+// loss call's shapes (measured on MI355X).
 //
 // Pipeline: K advances in steps of 32 (one MFMA depth) through a ring of
-// kStages LDS stages (32 KB each: 256 rows x 64 bytes of A and of B).
-// Operands go from global memory straight into LDS (global_load_lds_dwordx4:
-// no staging registers, no LDS-write instructions); each wave loads 64 rows of
-// A and 64 rows of B per step.  Step kt:
-//   1. 64 MFMAs on the register slot holding step kt's operands, interleaved
-//      with the 16 LDS reads of step kt+1's operands (into the other slot) and
-//      the 8 loads of step kt+kStages-1 into the stage step kt-1 used;
-//   2. wait until this wave's loads of step kt+2 have landed and its LDS reads
-//      are done, then one work-group barrier: step kt+2 is visible to all and
-//      every wave is done with the stage step kt used.
-// A load therefore has kStages-3 whole steps (about 1000 MFMA cycles each) to
-// land.  Each group of four MFMAs and its memory ops is fenced with
-// sched_barrier so the compiler keeps the interleave.  LDS rows are 64 bytes;
-// the four 16-byte chunks of row r are stored XOR-ed with ((r>>1) ^ (r>>2)) & 3,
-// which is bank-conflict free for the 16-row operand reads and repeats every
-// 16 rows, so all reads of a step use one per-lane base plus fixed offsets.
+// kStages = 4 LDS stages of 40 KB, filled by global_load_lds_dwordx4 (no
+// staging registers).  Step kt runs 12 groups of 8 MFMAs (row block g times
+// the 8 column blocks); interleaved with them:
+//   * A operands are single-buffered and rolling: row block g of step kt+1 is
+//     read into its registers two groups after row block g of step kt is used
+//     (blocks 10 and 11 of a step are read in groups 0 and 1 of that step);
+//   * B operands are double-buffered: the 8 blocks of step kt+1 are read in
+//     groups 2..9;
+//   * the 10 loads of step kt+3 (6 x 16 rows of A, 4 x 16 rows of B per wave)
+//     go one per group in groups 1..10, into the stage step kt-1 used;
+//   * at the end of the step, wait until this wave's loads of step kt+2 have
+//     landed and its LDS reads are done, then one work-group barrier.
+// Each group is fenced with sched_barrier so the compiler keeps the interleave.
+// LDS rows are 64 bytes; the four 16-byte chunks of row r are stored XOR-ed
+// with ((r >> 1) ^ (r >> 2)) & 3 (bank-conflict free for the 16-row operand
+// reads, period 16 rows).
 //
-// Rows past M (or N) are clamped to the last valid row when loading; the
-// epilogue masks them.  B rows can be gathered through an index map, and one
-// dimension can be bounded by a count that lives in device memory (so a
-// product over a data-dependent subset of tokens needs no host round trip).  Work-group -> tile mapping is XCD-aware: work-groups
-// are dispatched round-robin over the 8 XCDs, so consecutive tile ids are
-// handed to the same XCD, in a grouped order that keeps 8 A-tiles resident
-// while B-tiles stream (L2 reuse inside each XCD's private cache).
+// One dimension can be bounded by a count that lives in device memory (a
+// product over a data-dependent subset of tokens needs no host round trip).
+// Work-group -> tile mapping is XCD-aware: work-groups are dispatched
+// round-robin over the 8 XCDs, so consecutive tile ids go to the same XCD, in
+// a grouped order (4 A-tiles x 8 B-tiles resident per XCD round) for reuse
+// inside each XCD's private L2.
 #pragma once
 
 #include "common.h"
 
 namespace pspo {
 
-constexpr int kTileM = 256, kTileN = 256, kTileK = 32;
+constexpr int kTileM = 384, kTileN = 256, kTileK = 32;
 constexpr int kGemmThreads = 256;
 constexpr int kNumXcd = 8;
-constexpr int kGroupM = 8;
-constexpr int kStages = 5;
+constexpr int kGroupM = 4;
+constexpr int kStages = 4;
 constexpr int kLdsRow = kTileK * 2;                // 64 bytes
-constexpr int kLdsOperand = kTileM * kLdsRow;      // 16 KB
-constexpr int kLdsStage = 2 * kLdsOperand;         // A + B: 32 KB
+constexpr int kLdsA = kTileM * kLdsRow;            // 24 KB
+constexpr int kLdsB = kTileN * kLdsRow;            // 16 KB
+constexpr int kLdsStage = kLdsA + kLdsB;           // 40 KB
 constexpr int kLdsBytes = kStages * kLdsStage;     // 160 KB
+// both tile sizes divide this: padded token counts are multiples of it
+constexpr int kTileLcm = 768;
 
-// Accumulator layout: per wave 8 x 8 blocks of 16 x 16, four fp32 per lane each.
-constexpr int kBlocks = 8;
+// Accumulator layout: per wave 12 x 8 blocks of 16 x 16, four fp32 per lane each.
+constexpr int kBlocksM = 12, kBlocksN = 8, kBlocksAgpr = 8;
+constexpr int kWaveM = kBlocksM * 16, kWaveN = kBlocksN * 16;   // 192 x 128
 constexpr int kAccPerBlock = 4;
+constexpr int kLoadsA = kTileM / 4 / 16, kLoadsB = kTileN / 4 / 16;   // 6 + 4 per wave per step
 
 // Which dimension of a product a device-resident bound applies to.
 constexpr int kDynNone = 0, kDynM = 1, kDynN = 2, kDynK = 3;
 
 struct GemmShape {
   const uint16_t* A;
-  int64_t lda;
+  int64_t rows_a;            // rows per K block of A (>= tiles_m * kTileM)
   int M;
   const uint16_t* B;
-  int64_t ldb;
+  int64_t rows_b;            // rows per K block of B (>= tiles_n * kTileN)
   int N;
   int K;
   int tiles_m, tiles_n;      // grid extent (host-side upper bound)
-  // Optional gather: row r of the B operand is row b_rows[r] of B.
-  const int32_t* b_rows = nullptr;
   // Optional bound read from device memory when the kernel starts: limits M
   // (kDynM) or N (kDynN) to *dyn, or K (kDynK) to *dyn rounded up to kTileK.
   // Tiles outside the bound exit at once; a shorter K shortens the loop.
   const int32_t* dyn = nullptr;
   int dyn_dim = kDynNone;
-  // K-blocked operands: element (r, k) of a K-blocked operand with row count
-  // R lives at ((k / 32) * R + r) * 32 + k % 32, so each 32-deep K step of a
-  // panel is one contiguous block; its lda / ldb is then R * 32 (elements from
-  // one K step to the next) instead of the row stride.
-  bool a_kb = false, b_kb = false;
 };
 
 // Accumulator (i, j, r) of lane `lane` in wave (wm, wn) holds
-//   C[row0 + wm*128 + i*16 + (lane/16)*4 + r][col0 + wn*128 + j*16 + lane%16].
+//   C[row0 + wm*192 + i*16 + (lane/16)*4 + r][col0 + wn*128 + j*16 + lane%16].
 struct AccTile {
-  f32x4 c[kBlocks][kBlocks];
+  f32x4 a[kBlocksAgpr][kBlocksN];              // row blocks 0..7
+  f32x4 v[kBlocksM - kBlocksAgpr][kBlocksN];   // row blocks 8..11
 };
 
-__device__ __forceinline__ int acc_row(int wm, int i, int r, int lane) {
-  return wm * 128 + i * 16 + (lane >> 4) * 4 + r;
+// Element access with (after unrolling) constant indices.
+__device__ __forceinline__ float acc_get(const AccTile& t, int i, int j, int r) {
+  return i < kBlocksAgpr ? t.a[i][j][r] : t.v[i - kBlocksAgpr][j][r];
 }
-__device__ __forceinline__ int acc_col(int wn, int j, int lane) { return wn * 128 + j * 16 + (lane & 15); }
+__device__ __forceinline__ void acc_set(AccTile& t, int i, int j, int r, float x) {
+  if (i < kBlocksAgpr) t.a[i][j][r] = x;
+  else t.v[i - kBlocksAgpr][j][r] = x;
+}
+
+__device__ __forceinline__ int acc_row(int wm, int i, int r, int lane) {
+  return wm * kWaveM + i * 16 + (lane >> 4) * 4 + r;
+}
+__device__ __forceinline__ int acc_col(int wn, int j, int lane) { return wn * kWaveN + j * 16 + (lane & 15); }
 
 // The accumulator of column block j that sits in row `rel` of this lane's rows
-// (rel = row - (wm * 128 + (lane / 16) * 4); the lane holds rows i * 16 + r,
-// i < 8, r < 4), picked with selects only (no divergent branch per value).
+// (rel = row - (wm * 192 + (lane / 16) * 4); the lane holds rows i * 16 + r,
+// i < 12, r < 4), picked with selects only (no divergent branch per value).
 // Returns whether the lane holds that row.
 __device__ __forceinline__ bool acc_pick(const AccTile& acc, int j, int rel, float& value) {
   float z = 0.f;
   bool has = false;
 #pragma unroll
-  for (int i = 0; i < kBlocks; ++i)
+  for (int i = 0; i < kBlocksM; ++i)
 #pragma unroll
     for (int r = 0; r < kAccPerBlock; ++r) {
       const bool hit = rel == i * 16 + r;
-      z = hit ? acc.c[i][j][r] : z;
+      z = hit ? acc_get(acc, i, j, r) : z;
       has = has || hit;
     }
   value = z;
@@ -151,17 +166,22 @@ struct Const {
 
 typedef __attribute__((address_space(3))) void lds_void;
 
-// c += a * b on one 16 x 16 x 32 bf16 block, accumulating in place in AGPRs.
-// Written as inline asm with the accumulator tied in/out: through the builtin,
-// the register allocator is free to give the result a different AGPR quadruple
-// than the addend, and with all 256 AGPRs live it then rotates accumulators
-// through VGPRs with accvgpr read/write/mov copies on every loop trip (each of
-// which waits for the MFMA producing it).  The compiler's hazard tracking does
-// not see inline asm as an MFMA, so the kernel pads the MFMA -> VALU hazard
-// itself before its epilogue reads the accumulators (mfma_drain below); inside
-// the loop no instruction reads an accumulator within 64 MFMAs of its write.
-__device__ __forceinline__ void mfma_16x16x32(f32x4& c, const bf16x8& a, const bf16x8& b) {
+// c += a * b on one 16 x 16 x 32 bf16 block, accumulating in place (AGPRs or
+// VGPRs).  Written as inline asm with the accumulator tied in/out: through the
+// builtin, the register allocator is free to give the result a different
+// register quadruple than the addend, and with every accumulator register live
+// it then rotates accumulators through other registers with copies on every
+// loop trip (each of which waits for the MFMA producing it).  The compiler's
+// hazard tracking does not see inline asm as an MFMA, so the kernel pads the
+// MFMA -> VALU hazard itself before its epilogue reads the accumulators
+// (mfma_drain below); inside the loop no instruction reads or writes an
+// accumulator register between the MFMAs that update it (the write-after-read
+// hazard rules of the MFMA unit concern its accumulator input only).
+__device__ __forceinline__ void mfma_agpr(f32x4& c, const bf16x8& a, const bf16x8& b) {
   asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+a"(c) : "v"(a), "v"(b));
+}
+__device__ __forceinline__ void mfma_vgpr(f32x4& c, const bf16x8& a, const bf16x8& b) {
+  asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+v"(c) : "v"(a), "v"(b));
 }
 
 // Enough independent wait states for any MFMA result to be readable by VALU,
@@ -210,123 +230,98 @@ void gemm_nt_kernel(GemmShape g, Epi epi) {
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave >> 1, wn = wave & 1;
 
-  // Direct-to-LDS loads: instruction q (0..3) of operand o writes 1 KB = rows
-  // wave*64 + q*16 + lane/4 of the stage, physical chunk lane%4, holding the
-  // logical chunk (lane%4) ^ swizzle(row) of that row's 64-byte K slice.
-  const unsigned char* src[2][4];
-#pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const int row = wave * 64 + q * 16 + (lane >> 2);
-    const int chunk = (lane & 3) ^ chunk_swizzle(row);
-    const int ra = min(tm * kTileM + row, M - 1);
-    int rb = min(tn * kTileN + row, N - 1);
-    if (g.b_rows != nullptr) rb = g.b_rows[rb];
-    src[0][q] = reinterpret_cast<const unsigned char*>(g.A) + (int64_t)ra * (g.a_kb ? kTileK : g.lda) * 2 + chunk * 16;
-    src[1][q] = reinterpret_cast<const unsigned char*>(g.B) + (int64_t)rb * (g.b_kb ? kTileK : g.ldb) * 2 + chunk * 16;
-  }
-  // bytes from one K step of an operand to the next
-  const int64_t kstep_a = (g.a_kb ? g.lda : kTileK) * 2, kstep_b = (g.b_kb ? g.ldb : kTileK) * 2;
-  const int wave_lds = wave * 64 * kLdsRow;
+  // Direct-to-LDS loads: a load instruction writes 16 rows (1 KB) of a stage;
+  // lane l writes physical chunk l % 4 of row l / 4 and therefore fetches the
+  // logical chunk (l % 4) ^ swizzle(row) of that row's 64-byte K slice.  Wave w
+  // loads A rows w*96 + q*16 (q < 6) and B rows w*64 + q*16 (q < 4).
+  const uint32_t lane_off = (uint32_t)((lane >> 2) * kLdsRow + (((lane & 3) ^ chunk_swizzle(lane >> 2)) << 4));
+  const unsigned char* gA =
+      reinterpret_cast<const unsigned char*>(g.A) + ((int64_t)tm * kTileM + wave * (kTileM / 4)) * kLdsRow;
+  const unsigned char* gB =
+      reinterpret_cast<const unsigned char*>(g.B) + ((int64_t)tn * kTileN + wave * (kTileN / 4)) * kLdsRow;
+  const int64_t kstep_a = g.rows_a * kLdsRow, kstep_b = g.rows_b * kLdsRow;   // bytes per K step
 
-  // MFMA operand reads: block i of A is rows wm*128 + i*16 + lane%16, K chunk
+  // MFMA operand reads: block i of A is rows wm*192 + i*16 + lane%16, K chunk
   // lane/16 (8 bf16 of the 32-deep step).  The swizzle of row r + 16 i equals
   // that of row r, so block i is the lane's base plus i * 16 rows.
-  const int ra0 = wm * 128 + (lane & 15), rb0 = wn * 128 + (lane & 15);
-  const int rdA = ra0 * kLdsRow + (((lane >> 4) ^ chunk_swizzle(ra0)) << 4);
-  const int rdB = kLdsOperand + rb0 * kLdsRow + (((lane >> 4) ^ chunk_swizzle(rb0)) << 4);
+  const int rdA = (wm * kWaveM + (lane & 15)) * kLdsRow + (((lane >> 4) ^ chunk_swizzle(lane & 15)) << 4);
+  const int rdB = kLdsA + (wn * kWaveN + (lane & 15)) * kLdsRow + (((lane >> 4) ^ chunk_swizzle(lane & 15)) << 4);
 
-  bf16x8 fa[2][kBlocks], fb[2][kBlocks];
+  bf16x8 fa[kBlocksM], fb[2][kBlocksN];
   AccTile acc;
 #pragma unroll
-  for (int i = 0; i < kBlocks; ++i)
+  for (int i = 0; i < kBlocksAgpr; ++i)
 #pragma unroll
-    for (int j = 0; j < kBlocks; ++j) acc.c[i][j] = f32x4{};
+    for (int j = 0; j < kBlocksN; ++j) acc.a[i][j] = f32x4{};
+#pragma unroll
+  for (int i = 0; i < kBlocksM - kBlocksAgpr; ++i)
+#pragma unroll
+    for (int j = 0; j < kBlocksN; ++j) acc.v[i][j] = f32x4{};
 
   const int nk = K / kTileK;
 
-  // Operand n (0..15) of a step, in the order the MFMAs consume them:
-  // A0, B0..B7, A1..A7.
-  auto read_frag = [&](int stage, auto slot, auto n) {
-    constexpr int s = decltype(slot)::value, q = decltype(n)::value;
-    const unsigned char* base = lds + stage * kLdsStage;
-    if constexpr (q == 0) {
-      fa[s][0] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(base + rdA));
-    } else if constexpr (q <= 8) {
-      fb[s][q - 1] =
-          __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(base + rdB + (q - 1) * 16 * kLdsRow));
+  auto read_a = [&](int stage, int i) -> bf16x8 {
+    return __builtin_bit_cast(bf16x8,
+                              *reinterpret_cast<const u32x4*>(lds + stage * kLdsStage + rdA + i * 16 * kLdsRow));
+  };
+  auto read_b = [&](int stage, int j) -> bf16x8 {
+    return __builtin_bit_cast(bf16x8,
+                              *reinterpret_cast<const u32x4*>(lds + stage * kLdsStage + rdB + j * 16 * kLdsRow));
+  };
+  // Load q (0..9) of step kt into `stage`; steps past the last reload the last
+  // one (in bounds, never consumed), so every step issues the same count.
+  auto issue_load = [&](int kt, int stage, int q) {
+    const int64_t kk = max(min(kt, nk - 1), 0);
+    if (q < kLoadsA) {
+      __builtin_amdgcn_global_load_lds(
+          gA + kk * kstep_a + q * 16 * kLdsRow + lane_off,
+          (lds_void*)(lds + stage * kLdsStage + (wave * (kTileM / 4) + q * 16) * kLdsRow), 16, 0, 0);
     } else {
-      fa[s][q - 8] =
-          __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(base + rdA + (q - 8) * 16 * kLdsRow));
+      __builtin_amdgcn_global_load_lds(
+          gB + kk * kstep_b + (q - kLoadsA) * 16 * kLdsRow + lane_off,
+          (lds_void*)(lds + stage * kLdsStage + kLdsA + (wave * (kTileN / 4) + (q - kLoadsA) * 16) * kLdsRow), 16,
+          0, 0);
     }
   };
-  // MFMA group q (0..15): blocks (q/2, 4*(q%2) .. 4*(q%2)+3).
-  auto mfma_group = [&](auto slot, auto q) {
-    constexpr int s = decltype(slot)::value;
-    constexpr int i = decltype(q)::value / 2, j = 4 * (decltype(q)::value % 2);
+
+  // Group g of step kt: 8 MFMAs of row block g on B slot s, then its memory ops.
+  auto group = [&](auto slot, int kt, int cur, int nxt, int refill, auto gq) {
+    constexpr int s = decltype(slot)::value, gi = decltype(gq)::value;
 #pragma unroll
-    for (int jj = 0; jj < 4; ++jj)
-      mfma_16x16x32(acc.c[i][j + jj], fa[s][i], fb[s][j + jj]);
-  };
-  // Load instruction q (0..7) of a step: operand q/4, 16-row group q%4.
-  auto issue_load = [&](int kt, int stage, auto q) {
-    constexpr int o = decltype(q)::value / 4, r = decltype(q)::value % 4;
-    const int64_t koff = (int64_t)max(min(kt, nk - 1), 0) * (o == 0 ? kstep_a : kstep_b);
-    __builtin_amdgcn_global_load_lds(src[o][r] + koff,
-                                     (lds_void*)(lds + stage * kLdsStage + wave_lds + o * kLdsOperand +
-                                                 r * 16 * kLdsRow),
-                                     16, 0, 0);
-  };
-  auto issue_loads = [&](int kt, int stage) {
-    issue_load(kt, stage, Const<0>{}); issue_load(kt, stage, Const<1>{});
-    issue_load(kt, stage, Const<2>{}); issue_load(kt, stage, Const<3>{});
-    issue_load(kt, stage, Const<4>{}); issue_load(kt, stage, Const<5>{});
-    issue_load(kt, stage, Const<6>{}); issue_load(kt, stage, Const<7>{});
-  };
-  // Group q of a step: 4 MFMAs on `slot`; the next step's 16 operands are read
-  // two per group in groups 0..7 (the last one 32 MFMAs before it is needed)
-  // and the 8 loads of step kt+kStages-1 go one per group in groups 8..15.
-  auto group = [&](auto slot, int next_stage, int kt_load, int refill, auto q) {
-    constexpr int n = decltype(q)::value;
-    constexpr int other = 1 - decltype(slot)::value;
-    mfma_group(slot, q);
-    if constexpr (n < 8) {
-      read_frag(next_stage, Const<other>{}, Const<2 * n>{});
-      read_frag(next_stage, Const<other>{}, Const<2 * n + 1>{});
-    } else {
-      issue_load(kt_load, refill, Const<n - 8>{});
+    for (int j = 0; j < kBlocksN; ++j) {
+      if constexpr (gi < kBlocksAgpr) mfma_agpr(acc.a[gi][j], fa[gi], fb[s][j]);
+      else mfma_vgpr(acc.v[gi - kBlocksAgpr][j], fa[gi], fb[s][j]);
     }
+    if constexpr (gi < 2) fa[kBlocksM - 2 + gi] = read_a(cur, kBlocksM - 2 + gi);
+    else fa[gi - 2] = read_a(nxt, gi - 2);
+    if constexpr (gi >= 2 && gi < 2 + kBlocksN) fb[1 - s][gi - 2] = read_b(nxt, gi - 2);
+    if constexpr (gi >= 1 && gi <= kLoadsA + kLoadsB) issue_load(kt + kStages - 1, refill, gi - 1);
     __builtin_amdgcn_sched_barrier(0);
   };
   auto step = [&](auto slot, int kt) {
-    const int next_stage = (kt + 1) % kStages;
-    const int refill = (kt + kStages - 1) % kStages;  // the stage step kt-1 used
-    const int kl = kt + kStages - 1;
-    group(slot, next_stage, kl, refill, Const<0>{}); group(slot, next_stage, kl, refill, Const<1>{});
-    group(slot, next_stage, kl, refill, Const<2>{}); group(slot, next_stage, kl, refill, Const<3>{});
-    group(slot, next_stage, kl, refill, Const<4>{}); group(slot, next_stage, kl, refill, Const<5>{});
-    group(slot, next_stage, kl, refill, Const<6>{}); group(slot, next_stage, kl, refill, Const<7>{});
-    group(slot, next_stage, kl, refill, Const<8>{}); group(slot, next_stage, kl, refill, Const<9>{});
-    group(slot, next_stage, kl, refill, Const<10>{}); group(slot, next_stage, kl, refill, Const<11>{});
-    group(slot, next_stage, kl, refill, Const<12>{}); group(slot, next_stage, kl, refill, Const<13>{});
-    group(slot, next_stage, kl, refill, Const<14>{}); group(slot, next_stage, kl, refill, Const<15>{});
-    stage_barrier<(kStages - 3) * 8>();
+    const int cur = kt % kStages, nxt = (kt + 1) % kStages;
+    const int refill = (kt + kStages - 1) % kStages;   // the stage step kt-1 used
+    group(slot, kt, cur, nxt, refill, Const<0>{}); group(slot, kt, cur, nxt, refill, Const<1>{});
+    group(slot, kt, cur, nxt, refill, Const<2>{}); group(slot, kt, cur, nxt, refill, Const<3>{});
+    group(slot, kt, cur, nxt, refill, Const<4>{}); group(slot, kt, cur, nxt, refill, Const<5>{});
+    group(slot, kt, cur, nxt, refill, Const<6>{}); group(slot, kt, cur, nxt, refill, Const<7>{});
+    group(slot, kt, cur, nxt, refill, Const<8>{}); group(slot, kt, cur, nxt, refill, Const<9>{});
+    group(slot, kt, cur, nxt, refill, Const<10>{}); group(slot, kt, cur, nxt, refill, Const<11>{});
+    stage_barrier<kLoadsA + kLoadsB>();
   };
 
-  // prologue: steps 0 .. kStages-2 in flight; step 0 visible, its operands in
-  // slot 0; then step 1 visible (read during step 0).  With nk == 0 (a
-  // device-side K bound of 0) the loads and reads still happen, at K offset 0,
-  // but no MFMA consumes them and the accumulators stay zero.
-  for (int s = 0; s < kStages - 1; ++s) issue_loads(s, s);
-  stage_barrier<(kStages - 2) * 8>();
-  read_frag(0, Const<0>{}, Const<0>{}); read_frag(0, Const<0>{}, Const<1>{});
-  read_frag(0, Const<0>{}, Const<2>{}); read_frag(0, Const<0>{}, Const<3>{});
-  read_frag(0, Const<0>{}, Const<4>{}); read_frag(0, Const<0>{}, Const<5>{});
-  read_frag(0, Const<0>{}, Const<6>{}); read_frag(0, Const<0>{}, Const<7>{});
-  read_frag(0, Const<0>{}, Const<8>{}); read_frag(0, Const<0>{}, Const<9>{});
-  read_frag(0, Const<0>{}, Const<10>{}); read_frag(0, Const<0>{}, Const<11>{});
-  read_frag(0, Const<0>{}, Const<12>{}); read_frag(0, Const<0>{}, Const<13>{});
-  read_frag(0, Const<0>{}, Const<14>{}); read_frag(0, Const<0>{}, Const<15>{});
-  stage_barrier<(kStages - 3) * 8>();
+  // Prologue: steps 0 .. kStages-2 in flight; steps 0 and 1 visible; step 0's
+  // B blocks and A blocks 0..9 in registers (blocks 10, 11 are read in groups
+  // 0, 1 of step 0).  With nk == 0 (a device-side K bound of 0) the loads and
+  // reads still happen, at K offset 0, but no MFMA consumes them and the
+  // accumulators stay zero.
+  for (int s = 0; s < kStages - 1; ++s)
+    for (int q = 0; q < kLoadsA + kLoadsB; ++q) issue_load(s, s, q);
+  stage_barrier<kLoadsA + kLoadsB>();
+#pragma unroll
+  for (int i = 0; i < kBlocksM - 2; ++i) fa[i] = read_a(0, i);
+#pragma unroll
+  for (int j = 0; j < kBlocksN; ++j) fb[0][j] = read_b(0, j);
 
   int kt = 0;
   for (; kt + 1 < nk; kt += 2) {
@@ -336,7 +331,7 @@ void gemm_nt_kernel(GemmShape g, Epi epi) {
   if (kt < nk) step(Const<0>{}, kt);
 
   // drain the (clamped, unused) loads still in flight before LDS is reused
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
   mfma_drain();
   __syncthreads();
 

@@ -9,14 +9,17 @@
 //   dH_i = G_i W,  dW = sum_i G_i^T h_i.
 //
 // Schedule (the [N, V] logits never reach memory):
-//   1. forward product z^T = W H^T in 256x256 tiles; the epilogue reduces each
-//      tile column (one token) to a partial (max, sum exp) over the tile's 256
-//      vocabulary rows and picks up the target logit;
-//   2. finalize: merge the partials into lse, then l, rho, the clip mask, delta
+//   1. K-blocked bf16 copies of W and of the hidden rows of the tokens whose
+//      logits are needed (the operand layout of the matrix-core products);
+//   2. forward product z^T = W H^T in 384 x 256 tiles; the epilogue reduces
+//      each tile column (one token) to a partial (max, sum exp) over the tile's
+//      384 vocabulary rows and picks up the target logit;
+//   3. finalize: merge the partials into lse, then l, rho, the clip mask, delta
 //      and a deterministic float64 loss reduction;
-//   3. transposed bf16 copies H^T [d x Npad] and, per vocabulary chunk,
-//      W[chunk]^T [d x Vc] (K-contiguous operands of the two gradient products);
-//   4. per vocabulary chunk of Vc rows: recompute the chunk's logit tiles and
+//   4. K-blocked copies of the backward tokens' hidden rows, of their
+//      transpose H^T [d x Npad] and, per vocabulary chunk, of W[chunk]^T
+//      [d x Vc] (K-contiguous operands of the gradient products);
+//   5. per vocabulary chunk of Vc rows: recompute the chunk's logit tiles and
 //      write the bf16 logit gradient Delta = delta (e_o - exp(z - lse)) in both
 //      layouts ([Npad x Vc] and [Vc x Npad]); then dW[chunk] = Delta^T H and
 //      dH += Delta W[chunk] as two more matrix-core products.
@@ -24,6 +27,7 @@
 
 #include "common.h"
 #include "gemm.h"
+#include "layout.h"
 
 namespace pspo {
 namespace {
@@ -35,8 +39,9 @@ constexpr float kNegInf = -INFINITY;
 // ---------------------------------------------------------------------------
 
 // Forward: rows = vocabulary (A = W), columns = the tokens whose logits are
-// needed (B = H rows gathered through tok); writes per-column softmax
-// partials of each 256-row vocabulary tile and the target logit.
+// needed (B = their hidden rows, gathered; column t is token tok[t]); writes
+// per-column softmax partials of each 384-row vocabulary tile and the target
+// logit.
 struct EpiForward {
   int V, N;
   int64_t ldp;  // stride between vocabulary tiles in the partial arrays (= Npad)
@@ -53,52 +58,57 @@ struct EpiForward {
     const int vbase = tm * kTileM + acc_row(wm, 0, 0, lane);   // this lane's rows: vbase + i*16 + r
     const bool full = (tm + 1) * kTileM <= V;                   // every row of the tile is a token id
     // the targets of the lane's 8 columns, fetched together (two round trips, not 16)
-    int tgts[kBlocks];
+    int tgts[kBlocksN];
 #pragma unroll
-    for (int j = 0; j < kBlocks; ++j) {
+    for (int j = 0; j < kBlocksN; ++j) {
       const int t = tn * kTileN + acc_col(wn, j, lane);
       tgts[j] = t < n ? tok[t] : -1;
     }
 #pragma unroll
-    for (int j = 0; j < kBlocks; ++j) asm volatile("" ::"v"(tgts[j]));   // keep the batch: no sinking
+    for (int j = 0; j < kBlocksN; ++j) asm volatile("" ::"v"(tgts[j]));   // keep the batch: no sinking
 #pragma unroll
-    for (int j = 0; j < kBlocks; ++j) tgts[j] = tgts[j] >= 0 ? target[tgts[j]] : -1;
+    for (int j = 0; j < kBlocksN; ++j) tgts[j] = tgts[j] >= 0 ? target[tgts[j]] : -1;
 #pragma unroll
-    for (int j = 0; j < kBlocks; ++j) asm volatile("" ::"v"(tgts[j]));
+    for (int j = 0; j < kBlocksN; ++j) asm volatile("" ::"v"(tgts[j]));
+    // the target logits are stored after the column loop: a conditional store
+    // inside it makes the compiler keep far more accumulator copies live
+    float zvs[kBlocksN];
+    bool has[kBlocksN];
 #pragma unroll
-    for (int j = 0; j < kBlocks; ++j) {
+    for (int j = 0; j < kBlocksN; ++j) {
       const int cl = acc_col(wn, j, lane);
-      const int t = tn * kTileN + cl;
       const int tgt = tgts[j];
-      float zv;
-      if (acc_pick(acc, j, tgt - vbase, zv)) zt[t] = zv;
+      has[j] = acc_pick(acc, j, tgt - vbase, zvs[j]);
       float m = kNegInf;
 #pragma unroll
-      for (int i = 0; i < kBlocks; ++i)
+      for (int i = 0; i < kBlocksM; ++i)
 #pragma unroll
         for (int r = 0; r < kAccPerBlock; ++r)
-          if (full || vbase + i * 16 + r < V) m = fmaxf(m, acc.c[i][j][r]);
+          if (full || vbase + i * 16 + r < V) m = fmaxf(m, acc_get(acc, i, j, r));
       m = fmaxf(m, __shfl_xor(m, 16));
       m = fmaxf(m, __shfl_xor(m, 32));
       float l = 0.f;
       if (m != kNegInf) {
 #pragma unroll
-        for (int i = 0; i < kBlocks; ++i)
+        for (int i = 0; i < kBlocksM; ++i)
 #pragma unroll
           for (int r = 0; r < kAccPerBlock; ++r)
-            if (full || vbase + i * 16 + r < V) l += __expf(acc.c[i][j][r] - m);
+            if (full || vbase + i * 16 + r < V) l += __expf(acc_get(acc, i, j, r) - m);
       }
       l += __shfl_xor(l, 16);
       l += __shfl_xor(l, 32);
       if (lane < 16) {
-        red[(wm * 256 + cl) * 2 + 0] = m;
-        red[(wm * 256 + cl) * 2 + 1] = l;
+        red[(wm * kTileN + cl) * 2 + 0] = m;
+        red[(wm * kTileN + cl) * 2 + 1] = l;
       }
     }
+#pragma unroll
+    for (int j = 0; j < kBlocksN; ++j)
+      if (has[j]) zt[tn * kTileN + acc_col(wn, j, lane)] = zvs[j];
     __syncthreads();
     const int c = threadIdx.x;
     const float m0 = red[c * 2], l0 = red[c * 2 + 1];
-    const float m1 = red[(256 + c) * 2], l1 = red[(256 + c) * 2 + 1];
+    const float m1 = red[(kTileN + c) * 2], l1 = red[(kTileN + c) * 2 + 1];
     const float M = fmaxf(m0, m1);
     float L = 0.f;
     if (m0 != kNegInf) L += l0 * __expf(m0 - M);
@@ -111,12 +121,23 @@ struct EpiForward {
   }
 };
 
+// Lane exchange inside a quad of lanes (DPP quad_perm): value of lane l ^ 1 / l ^ 2.
+__device__ __forceinline__ uint32_t quad_xor1(uint32_t x) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0xB1, 0xF, 0xF, false);
+}
+__device__ __forceinline__ uint32_t quad_xor2(uint32_t x) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x4E, 0xF, 0xF, false);
+}
+
 // Backward logit gradient for one vocabulary chunk: rows = vocabulary rows
 // v0 + vl (A = W[v0:]), columns = the compacted tokens that carry gradient
 // (column t is token tok[t], t < *n_dev).  Writes bf16 Delta in both K-blocked
-// layouts (vocabulary rows for dW, token rows for dH); zero outside t < *n_dev, v < V.
-// The 256 x 256 bf16 tile goes through LDS once per layout so both global
-// layouts are written as whole 512-byte rows (16 bytes per lane).
+// layouts (vocabulary rows for dW, token rows for dH); zero outside t < *n_dev,
+// v < V.  Straight from registers: a lane's 4 consecutive rows of a block are
+// 4 consecutive K entries of the token-major layout (one 8-byte store); for the
+// vocabulary-major layout the 4 x 4 (rows x tokens) blocks of a quad of lanes
+// are transposed with two quad exchanges, so each lane stores 4 consecutive
+// tokens of one row.
 struct EpiDelta {
   int V, N, v0;
   const int32_t* target;
@@ -129,125 +150,132 @@ struct EpiDelta {
   const int32_t* tok;    // column t of the tile is token tok[t] (columns t < *n_dev)
   const int32_t* n_dev;
 
-  // LDS tile: 256 rows x 512 bytes; 16-byte chunk c of row r stored at chunk c ^ (r & 31).
-  __device__ static __forceinline__ int tile_off(int row, int col) {
-    return row * 512 + ((((col >> 3) ^ (row & 31)) << 4) | ((col & 7) << 1));
-  }
-
-  // Copies the LDS tile (256 rows of 256 bf16) into a K-blocked matrix with R
-  // rows per K block, `dst` pointing at the tile's first row in its first K
-  // block: the tile's 8 column blocks of 32 become 8 runs of 256 x 64 bytes,
-  // each contiguous (16 KB), written 16 bytes per lane.
-  __device__ static __forceinline__ void copy_out_kb(const unsigned char* tile, uint16_t* dst, int64_t R) {
-    for (int c = threadIdx.x; c < 256 * 32; c += kGemmThreads) {
-      const int blk = c >> 10, row = (c >> 2) & 255, q = c & 3;
-      const u32x4 v = *reinterpret_cast<const u32x4*>(tile + row * 512 + (((blk * 4 + q) ^ (row & 31)) << 4));
-      *reinterpret_cast<u32x4*>(dst + ((int64_t)blk * R + row) * kTileK + q * 8) = v;
-    }
-  }
-
-  __device__ __forceinline__ void apply(AccTile& acc, int tm, int tn, int wm, int wn, int lane, float* smem) const {
-    unsigned char* tile = reinterpret_cast<unsigned char*>(smem);
+  __device__ __forceinline__ void apply(AccTile& acc, int tm, int tn, int wm, int wn, int lane, float*) const {
     const int n = min(N, __builtin_amdgcn_readfirstlane(*n_dev));
-    const int vbase = v0 + tm * kTileM + acc_row(wm, 0, 0, lane);   // this lane's rows: vbase + i*16 + r
-    const bool full = v0 + (tm + 1) * kTileM <= V;                   // every row of the tile is a token id
-    // Delta in place of the logits, without a branch per value: columns past n
-    // have delta 0, and exp(min(z - lse, 0)) equals exp(z - lse) for the others
-    // (lse >= every logit) while staying finite for them
+    const int vl0 = tm * kTileM + acc_row(wm, 0, 0, lane);   // chunk rows of this lane: vl0 + i*16 + r
+    const int vbase = v0 + vl0;
+    const bool full = v0 + (tm + 1) * kTileM <= V;            // every row of the tile is a token id
     // per-column token data of the lane's 8 columns, fetched together
-    int tos[kBlocks];
-    float dls[kBlocks], lss[kBlocks];
-    int tgs[kBlocks];
+    int tos[kBlocksN];
+    float dls[kBlocksN], lss[kBlocksN];
+    int tgs[kBlocksN];
 #pragma unroll
-    for (int j = 0; j < kBlocks; ++j) {
+    for (int j = 0; j < kBlocksN; ++j) {
       const int t = tn * kTileN + acc_col(wn, j, lane);
       tos[j] = t < n ? tok[t] : -1;
     }
 #pragma unroll
-    for (int j = 0; j < kBlocks; ++j) {
+    for (int j = 0; j < kBlocksN; ++j) {
       const bool tv = tos[j] >= 0;
       dls[j] = tv ? delta[tos[j]] : 0.f;
       lss[j] = tv ? lse[tos[j]] : 0.f;
       tgs[j] = tv ? target[tos[j]] : -1;
     }
+    // Delta without a branch per value: columns past n have delta 0, and
+    // exp(min(z - lse, 0)) equals exp(z - lse) for the others (lse >= every
+    // logit) while staying finite for them.
+    // Store addresses: a per-tile base (uniform) plus a 32-bit byte offset per
+    // lane and block (a tile spans 12 K blocks of the token-major layout and 8
+    // of the vocabulary-major one, far below 4 GB); 64-bit addresses for all
+    // 96 blocks would not fit in the registers left beside the accumulators.
+    const int k = lane & 3;
+    unsigned char* nbase = reinterpret_cast<unsigned char*>(
+        dN + ((int64_t)(tm * (kTileM / kTileK)) * rN + tn * kTileN) * kTileK);
+    unsigned char* tbase = reinterpret_cast<unsigned char*>(
+        dT + ((int64_t)(tn * (kTileN / kTileK)) * rT + tm * kTileM) * kTileK);
+    const uint32_t kstepN = (uint32_t)rN * (kTileK * 2), kstepT = (uint32_t)rT * (kTileK * 2);
+    // token-major: lane holds chunk rows wm*192 + (lane/16)*4 + i*16 + r of token
+    // wn*128 + j*16 + lane%16 (tile-local); K block (row / 32), entry row % 32
+    const uint32_t noff = (uint32_t)(wm * (kWaveM / kTileK)) * kstepN +
+                          (uint32_t)(wn * kWaveN + (lane & 15)) * (kTileK * 2) + (uint32_t)(lane >> 4) * 8;
+    // vocabulary-major: after the exchanges lane k holds row wm*192 + (lane/16)*4
+    // + i*16 + k for tokens wn*128 + j*16 + (lane & 12) .. +3
+    const uint32_t toff = (uint32_t)(wn * (kWaveN / kTileK)) * kstepT +
+                          (uint32_t)(wm * kWaveM + (lane >> 4) * 4 + k) * (kTileK * 2) + (uint32_t)(lane & 12) * 2;
 #pragma unroll
-    for (int j = 0; j < kBlocks; ++j) {
+    for (int j = 0; j < kBlocksN; ++j) {
       const float dl = dls[j];
       const float ls = lss[j];
       const int tgt = tgs[j];
 #pragma unroll
-      for (int i = 0; i < kBlocks; ++i)
+      for (int i = 0; i < kBlocksM; ++i) {
+        uint32_t x[kAccPerBlock];
 #pragma unroll
         for (int r = 0; r < kAccPerBlock; ++r) {
           const int v = vbase + i * 16 + r;
-          float dv = dl * ((v == tgt ? 1.f : 0.f) - __expf(fminf(acc.c[i][j][r] - ls, 0.f)));
+          float dv = dl * ((v == tgt ? 1.f : 0.f) - __expf(fminf(acc_get(acc, i, j, r) - ls, 0.f)));
           if (!full) dv = (v < V) ? dv : 0.f;
-          acc.c[i][j][r] = dv;
+          x[r] = f32_to_bf16_bits(dv);
         }
-    }
-    // token-major layout: LDS row = token, the lane's 4 consecutive vocabulary
-    // entries of a block in one 8-byte write
-#pragma unroll
-    for (int j = 0; j < kBlocks; ++j) {
-      const int tl = acc_col(wn, j, lane);
-#pragma unroll
-      for (int i = 0; i < kBlocks; ++i) {
-        const int vl = acc_row(wm, i, 0, lane);
-        u32x2 packed;
-        packed.x = f32_to_bf16_bits(acc.c[i][j][0]) | (f32_to_bf16_bits(acc.c[i][j][1]) << 16);
-        packed.y = f32_to_bf16_bits(acc.c[i][j][2]) | (f32_to_bf16_bits(acc.c[i][j][3]) << 16);
-        *reinterpret_cast<u32x2*>(tile + tile_off(tl, vl)) = packed;
+        const uint32_t p0 = x[0] | (x[1] << 16), p1 = x[2] | (x[3] << 16);
+        u32x2 tokmaj;
+        tokmaj.x = p0;
+        tokmaj.y = p1;
+        *reinterpret_cast<u32x2*>(nbase + (noff + (uint32_t)(i >> 1) * kstepN + (uint32_t)(j * 16 * kTileK * 2 +
+                                                                                         (i & 1) * 32))) = tokmaj;
+        const bool lo2 = k < 2;
+        const uint32_t r1 = quad_xor2(lo2 ? p1 : p0);
+        const uint32_t qa = lo2 ? p0 : r1, qb = lo2 ? r1 : p1;   // tokens k%2 and k%2+2, rows 2(k/2), +1
+        const bool even = (k & 1) == 0;
+        const uint32_t r2 = quad_xor1(even ? ((qa >> 16) | (qb & 0xFFFF0000u)) : ((qa & 0xFFFFu) | (qb << 16)));
+        u32x2 vocmaj;
+        vocmaj.x = even ? ((qa & 0xFFFFu) | (r2 << 16)) : ((r2 & 0xFFFFu) | (qa & 0xFFFF0000u));
+        vocmaj.y = even ? ((qb & 0xFFFFu) | (r2 & 0xFFFF0000u)) : ((r2 >> 16) | (qb & 0xFFFF0000u));
+        *reinterpret_cast<u32x2*>(tbase + (toff + (uint32_t)(j >> 1) * kstepT +
+                                           (uint32_t)(i * 16 * kTileK * 2 + (j & 1) * 32))) = vocmaj;
+        __builtin_amdgcn_sched_barrier(0);   // one block's values live at a time
       }
     }
-    __syncthreads();
-    // token-major tile: rows tn*256.., K blocks (tm*256)/32..
-    copy_out_kb(tile, dN + ((int64_t)(tm * (kTileM / kTileK)) * rN + tn * kTileN) * kTileK, rN);
-    __syncthreads();
-    // vocabulary-major layout: LDS row = vocabulary entry
-#pragma unroll
-    for (int j = 0; j < kBlocks; ++j) {
-      const int tl = acc_col(wn, j, lane);
-#pragma unroll
-      for (int i = 0; i < kBlocks; ++i)
-#pragma unroll
-        for (int r = 0; r < kAccPerBlock; ++r) {
-          const int vl = acc_row(wm, i, r, lane);
-          *reinterpret_cast<uint16_t*>(tile + tile_off(vl, tl)) = (uint16_t)f32_to_bf16_bits(acc.c[i][j][r]);
-        }
-    }
-    __syncthreads();
-    // vocabulary-major tile: rows tm*256.., K blocks (tn*256)/32..
-    copy_out_kb(tile, dT + ((int64_t)(tn * (kTileN / kTileK)) * rT + tm * kTileM) * kTileK, rT);
   }
 };
 
 // dW rows v0 + vl (A = Delta^T), columns = hidden features (B = H^T).
+// Addresses are a per-tile base plus 32-bit byte offsets (a tile spans
+// 384 rows of dW).  In accumulate mode each column block's 48 old values are
+// loaded, added and stored before the next block's loads (a compiler memory
+// fence between the blocks): hoisting every load of the tile would need 384
+// more registers.
 struct EpiDW {
   int V, d, v0;
   float* dW;
   bool accumulate;
 
   __device__ __forceinline__ void apply(const AccTile& acc, int tm, int tn, int wm, int wn, int lane, float*) const {
+    const int row0 = v0 + tm * kTileM;                   // first dW row of the tile
+    const int lr = acc_row(wm, 0, 0, lane);              // this lane's tile rows: lr + i*16 + r
+    unsigned char* base = reinterpret_cast<unsigned char*>(dW + (int64_t)row0 * d + tn * kTileN);
+    const uint32_t ld = (uint32_t)d * 4;
+    const uint32_t loff = (uint32_t)lr * ld + (uint32_t)acc_col(wn, 0, lane) * 4;
+    const int cb = tn * kTileN + acc_col(wn, 0, lane);   // this lane's columns: cb + j*16
 #pragma unroll
-    for (int j = 0; j < kBlocks; ++j) {
-      const int col = tn * kTileN + acc_col(wn, j, lane);
-      if (col >= d) continue;
+    for (int j = 0; j < kBlocksN; ++j) {
+      const bool cv = cb + j * 16 < d;
+      float old[kBlocksM][kAccPerBlock];
 #pragma unroll
-      for (int i = 0; i < kBlocks; ++i)
+      for (int i = 0; i < kBlocksM; ++i)
 #pragma unroll
         for (int r = 0; r < kAccPerBlock; ++r) {
-          const int v = v0 + tm * kTileM + acc_row(wm, i, r, lane);
-          if (v < V) {
-            float* p = dW + (int64_t)v * d + col;
-            *p = accumulate ? *p + acc.c[i][j][r] : acc.c[i][j][r];
-          }
+          const bool ok = accumulate && cv && row0 + lr + i * 16 + r < V;
+          const uint32_t off = loff + (uint32_t)(i * 16 + r) * ld + (uint32_t)j * 64;
+          old[i][r] = ok ? *reinterpret_cast<const float*>(base + off) : 0.f;
         }
+#pragma unroll
+      for (int i = 0; i < kBlocksM; ++i)
+#pragma unroll
+        for (int r = 0; r < kAccPerBlock; ++r) {
+          const uint32_t off = loff + (uint32_t)(i * 16 + r) * ld + (uint32_t)j * 64;
+          if (cv && row0 + lr + i * 16 + r < V)
+            *reinterpret_cast<float*>(base + off) = old[i][r] + acc_get(acc, i, j, r);
+        }
+      asm volatile("" ::: "memory");
     }
   }
 };
 
 // dH rows = compacted tokens (A = Delta), columns = hidden features
 // (B = W^T[:, v0:]); row t is written to d_hidden row tok[t], t < *n_dev.
+// After the first vocabulary chunk each row block's old values are loaded,
+// added and stored before the next block's loads (see EpiDW).
 struct EpiDH {
   int N, d;
   float* dH;
@@ -257,59 +285,34 @@ struct EpiDH {
 
   __device__ __forceinline__ void apply(const AccTile& acc, int tm, int tn, int wm, int wn, int lane, float*) const {
     const int n = min(N, __builtin_amdgcn_readfirstlane(*n_dev));
+    const int cb = tn * kTileN + acc_col(wn, 0, lane);   // this lane's columns: cb + j*16
 #pragma unroll
-    for (int i = 0; i < kBlocks; ++i)
+    for (int i = 0; i < kBlocksM; ++i) {
+      float* rows[kAccPerBlock];
 #pragma unroll
       for (int r = 0; r < kAccPerBlock; ++r) {
         const int t = tm * kTileM + acc_row(wm, i, r, lane);
-        if (t >= n) continue;
-        float* row = dH + (int64_t)tok[t] * d;
-#pragma unroll
-        for (int j = 0; j < kBlocks; ++j) {
-          const int col = tn * kTileN + acc_col(wn, j, lane);
-          if (col < d) {
-            float* p = row + col;
-            *p = first ? acc.c[i][j][r] : *p + acc.c[i][j][r];
-          }
-        }
+        rows[r] = t < n ? dH + (int64_t)tok[t] * d : nullptr;
       }
+      float old[kAccPerBlock][kBlocksN];
+#pragma unroll
+      for (int r = 0; r < kAccPerBlock; ++r)
+#pragma unroll
+        for (int j = 0; j < kBlocksN; ++j)
+          old[r][j] = (!first && rows[r] != nullptr && cb + j * 16 < d) ? rows[r][cb + j * 16] : 0.f;
+#pragma unroll
+      for (int r = 0; r < kAccPerBlock; ++r)
+#pragma unroll
+        for (int j = 0; j < kBlocksN; ++j)
+          if (rows[r] != nullptr && cb + j * 16 < d) rows[r][cb + j * 16] = old[r][j] + acc_get(acc, i, j, r);
+      asm volatile("" ::: "memory");
+    }
   }
 };
 
 // ---------------------------------------------------------------------------
 // Small kernels
 // ---------------------------------------------------------------------------
-
-// Transposed, zero-padded copy of a bf16 [rows x cols] matrix, in blocks of
-// `chunk` source rows, each block K-blocked: source row r, column c goes to
-//   dst[(r / chunk) * cols * chunk + (((r % chunk) / 32) * cols + c) * 32 + r % 32]
-// (0 for r >= rows), i.e. block b is the [cols x chunk] transpose of rows
-// [b*chunk, (b+1)*chunk) with each 32-deep K step of its cols rows contiguous.
-// 64 x 64 tiles through LDS; cols, chunk and the padded row count are
-// multiples of 64.
-// Optionally, row r of the source is row rmap[r] of `src` and only the first
-// min(rows, *n_dev) rows are present; 64-row blocks wholly past that count are
-// not written (no product reads them).
-__global__ __launch_bounds__(256) void transpose_pad_kernel(const uint16_t* __restrict__ src, int rows, int cols,
-                                                            int64_t ld_src, uint16_t* __restrict__ dst,
-                                                            int64_t chunk, const int32_t* __restrict__ rmap,
-                                                            const int32_t* __restrict__ n_dev) {
-  __shared__ uint16_t tile[64][66];
-  const int c0 = blockIdx.x * 64, r0 = blockIdx.y * 64;
-  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
-  if (n_dev != nullptr) {
-    rows = min(rows, *n_dev);
-    if (r0 >= (rows + 63) / 64 * 64) return;
-  }
-  for (int rr = ty; rr < 64; rr += 4) {
-    const int r = r0 + rr;
-    tile[rr][tx] = (r < rows) ? src[(int64_t)(rmap ? rmap[r] : r) * ld_src + c0 + tx] : (uint16_t)0;
-  }
-  __syncthreads();
-  const int64_t block = r0 / chunk, rin = r0 % chunk + tx;
-  uint16_t* out = dst + block * cols * chunk + ((rin / kTileK) * cols) * kTileK + rin % kTileK;
-  for (int cc = ty; cc < 64; cc += 4) out[(int64_t)(c0 + cc) * kTileK] = tile[tx][cc];
-}
 
 __global__ void fill_f32_kernel(float* __restrict__ p, int64_t n, float v) {
   for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
@@ -519,21 +522,22 @@ __global__ __launch_bounds__(kFinThreads) void reduce_loss_kernel(int nblk, cons
 
 
 struct Plan {
-  int64_t Npad, Vpad, Vc, ntv, nfin;
-  int64_t off_pm, off_pl, off_zt, off_lse, off_delta, off_fidx, off_fpos, off_nfwd, off_idx, off_nact, off_blk, off_ht,
-      off_wt, off_dn, off_dt, total;
+  int64_t Npad, Vpad, dpad, Vc, ntv, nfin;
+  int64_t off_pm, off_pl, off_zt, off_lse, off_delta, off_fidx, off_fpos, off_nfwd, off_idx, off_nact, off_blk, off_wk,
+      off_hk, off_ht, off_wt, off_dn, off_dt, total;
 };
 
 Plan make_plan(int64_t N, int64_t d, int64_t V) {
   Plan p{};
-  p.Npad = round_up(N > 0 ? N : 1, kTileN);
+  p.Npad = round_up(N > 0 ? N : 1, kTileLcm);   // token rows: tiles of 256 (B side) and 384 (A side)
   p.Vpad = round_up(V, kTileM);
-  // Vocabulary rows per backward chunk: a multiple of 256 tiles such that the
-  // dW product of a chunk ((Vc / 256) x ceil(d / 256) tiles of very long K) fills
-  // whole rounds of the 256 CUs (d = 3584: 14 column tiles, 128 row tiles,
-  // exactly 7 rounds); whole vocabulary if smaller.
+  p.dpad = round_up(d, kTileN);
+  // Vocabulary rows per backward chunk: a multiple of 384-row tiles such that
+  // the dW product of a chunk ((Vc / 384) x ceil(d / 256) tiles of very long
+  // K) fills whole rounds of the 256 CUs (d = 3584: 14 column tiles, 128 row
+  // tiles, exactly 7 rounds); the whole vocabulary if smaller.
   {
-    int64_t td = (d + kTileN - 1) / kTileN, a = td, b = 256;
+    int64_t a = p.dpad / kTileN, b = 256;
     while (b) {
       const int64_t r = a % b;
       a = b;
@@ -561,10 +565,12 @@ Plan make_plan(int64_t N, int64_t d, int64_t V) {
   p.off_idx = take(p.Npad * 4);
   p.off_nact = take(4);
   p.off_blk = take((p.nfin > 0 ? p.nfin : 1) * 5 * 8);
-  p.off_ht = take(d * p.Npad * 2);                                  // K-blocked [Npad/32][d][32]
-  p.off_wt = take(d * ((p.Vpad + p.Vc - 1) / p.Vc) * p.Vc * 2);     // per chunk: K-blocked [Vc/32][d][32]
-  p.off_dn = take(p.Npad * p.Vc * 2);                               // K-blocked [Vc/32][Npad][32]
-  p.off_dt = take(p.Vc * p.Npad * 2);                               // K-blocked [Npad/32][Vc][32]
+  p.off_wk = take(d * p.Vpad * 2);                                    // W, K-blocked [d/32][Vpad][32]
+  p.off_hk = take(d * p.Npad * 2);                                    // gathered hidden rows [d/32][Npad][32]
+  p.off_ht = take(p.dpad * p.Npad * 2);                               // H[bwd]^T [Npad/32][dpad][32]
+  p.off_wt = take(p.dpad * ((p.Vpad + p.Vc - 1) / p.Vc) * p.Vc * 2);  // per chunk: W^T [Vc/32][dpad][32]
+  p.off_dn = take(p.Npad * p.Vc * 2);                                 // K-blocked [Vc/32][Npad][32]
+  p.off_dt = take(p.Vc * p.Npad * 2);                                 // K-blocked [Npad/32][Vc][32]
   p.total = o;
   return p;
 }
@@ -649,22 +655,33 @@ int pspo_loss_fwd_bwd(const uint16_t* hidden, const uint16_t* w_head, const int3
   int32_t* act_idx = reinterpret_cast<int32_t*>(ws + pl.off_idx);
   int32_t* n_act = reinterpret_cast<int32_t*>(ws + pl.off_nact);
   double* blk = reinterpret_cast<double*>(ws + pl.off_blk);
+  uint16_t* wk = reinterpret_cast<uint16_t*>(ws + pl.off_wk);
+  uint16_t* hk = reinterpret_cast<uint16_t*>(ws + pl.off_hk);
   uint16_t* hT = reinterpret_cast<uint16_t*>(ws + pl.off_ht);
   uint16_t* wT = reinterpret_cast<uint16_t*>(ws + pl.off_wt);
   uint16_t* dN = reinterpret_cast<uint16_t*>(ws + pl.off_dn);
   uint16_t* dT = reinterpret_cast<uint16_t*>(ws + pl.off_dt);
 
-  const int tiles_tok = (int)(pl.Npad / kTileN);
-  const int tiles_voc = (int)(pl.ntv);
-  const int tiles_d = (d + kTileN - 1) / kTileN;
+  const int tiles_tok_n = (int)(pl.Npad / kTileN);    // tokens on the B side
+  const int tiles_tok_m = (int)(pl.Npad / kTileM);    // tokens on the A side
+  const int tiles_voc = (int)pl.ntv;
+  const int tiles_d = (int)(pl.dpad / kTileN);
+  const unsigned ksteps = (unsigned)(d / kTileK);
 
-  // 1. the tokens whose logits are needed (all of them if logp_new is wanted)
+  // 1. the tokens whose logits are needed (all of them if logp_new is wanted);
+  //    W and their hidden rows as K-blocked operands
   hipLaunchKernelGGL(compact_forward_kernel, dim3(1), dim3(kCompactThreads), 0, stream, N, R,
                      logp_new != nullptr ? 1 : 0, seq_id, advantage, fwd_idx, fwd_pos, n_fwd);
   PSPO_HIP_CHECK(hipGetLastError());
+  hipLaunchKernelGGL(kblock_rows_kernel, dim3(ksteps, (unsigned)(pl.Vpad / 64)), dim3(256), 0, stream, w_head,
+                     (int64_t)d, V, nullptr, nullptr, wk, pl.Vpad);
+  PSPO_HIP_CHECK(hipGetLastError());
+  hipLaunchKernelGGL(kblock_rows_kernel, dim3(ksteps, (unsigned)(pl.Npad / 64)), dim3(256), 0, stream, hidden,
+                     (int64_t)d, N, fwd_idx, n_fwd, hk, pl.Npad);
+  PSPO_HIP_CHECK(hipGetLastError());
   // 2. forward logits -> per-tile softmax partials and target logits
   {
-    GemmShape g{w_head, d, V, hidden, d, N, d, tiles_voc, tiles_tok, fwd_idx, n_fwd, kDynN};
+    GemmShape g{wk, pl.Vpad, V, hk, pl.Npad, N, d, tiles_voc, tiles_tok_n, n_fwd, kDynN};
     EpiForward e{V, N, pl.Npad, target, part_m, part_l, zt, fwd_idx, n_fwd};
     if (int rc = launch_gemm(g, e, stream)) return rc;
   }
@@ -683,12 +700,16 @@ int pspo_loss_fwd_bwd(const uint16_t* hidden, const uint16_t* w_head, const int3
   PSPO_HIP_CHECK(hipGetLastError());
   hipLaunchKernelGGL(zero_inactive_rows_kernel, dim3((unsigned)N), dim3(256), 0, stream, d, delta, d_hidden);
   PSPO_HIP_CHECK(hipGetLastError());
-  // 5. K-contiguous copies for the gradient products
+  // 5. operands of the gradient products: the backward tokens' hidden rows
+  //    (K-blocked, in the forward's buffer), H[bwd]^T and per chunk W[chunk]^T
+  hipLaunchKernelGGL(kblock_rows_kernel, dim3(ksteps, (unsigned)(pl.Npad / 64)), dim3(256), 0, stream, hidden,
+                     (int64_t)d, N, act_idx, n_act, hk, pl.Npad);
+  PSPO_HIP_CHECK(hipGetLastError());
   hipLaunchKernelGGL(transpose_pad_kernel, dim3(d / 64, (unsigned)(pl.Npad / 64)), dim3(256), 0, stream, hidden, N,
-                     d, (int64_t)d, hT, pl.Npad, act_idx, n_act);   // H[active]^T [d x Npad]
+                     d, (int64_t)d, hT, pl.dpad, pl.Npad, act_idx, n_act);   // H[active]^T [dpad x Npad]
   PSPO_HIP_CHECK(hipGetLastError());
   hipLaunchKernelGGL(transpose_pad_kernel, dim3(d / 64, (unsigned)(pl.Vpad / 64)), dim3(256), 0, stream, w_head, V,
-                     d, (int64_t)d, wT, pl.Vc, nullptr, nullptr);  // per chunk: W[chunk]^T [d x Vc]
+                     d, (int64_t)d, wT, pl.dpad, pl.Vc, nullptr, nullptr);  // per chunk: W[chunk]^T [dpad x Vc]
   PSPO_HIP_CHECK(hipGetLastError());
   // 6. backward, one vocabulary chunk at a time; every product is bounded by
   //    the active-token count in device memory
@@ -696,19 +717,18 @@ int pspo_loss_fwd_bwd(const uint16_t* hidden, const uint16_t* w_head, const int3
     const int64_t vc = (pl.Vpad - v0) < pl.Vc ? (pl.Vpad - v0) : pl.Vc;
     const int ctiles = (int)(vc / kTileM);
     {
-      GemmShape g{w_head + v0 * d, d, (int)(V - v0), hidden, d, N, d, ctiles, tiles_tok, act_idx, n_act, kDynN};
+      GemmShape g{wk + v0 * kTileK, pl.Vpad, (int)(V - v0), hk, pl.Npad, N, d, ctiles, tiles_tok_n, n_act, kDynN};
       EpiDelta e{V, N, (int)v0, target, lse, delta, dT, pl.Vc, dN, pl.Npad, act_idx, n_act};
       if (int rc = launch_gemm(g, e, stream)) return rc;
     }
     {
-      GemmShape g{dT,      pl.Vc * kTileK, (int)vc, hT, (int64_t)d * kTileK, d, (int)pl.Npad, ctiles, tiles_d,
-                  nullptr, n_act, kDynK,     true,     true};
+      GemmShape g{dT, pl.Vc, (int)vc, hT, pl.dpad, d, (int)pl.Npad, ctiles, tiles_d, n_act, kDynK};
       EpiDW e{V, d, (int)v0, d_w_head, accumulate};
       if (int rc = launch_gemm(g, e, stream)) return rc;
     }
     {
-      GemmShape g{dN,      pl.Npad * kTileK, (int)pl.Npad, wT + (v0 / pl.Vc) * d * pl.Vc, (int64_t)d * kTileK, d,
-                  (int)vc, tiles_tok, tiles_d, nullptr, n_act, kDynM, true, true};
+      GemmShape g{dN, pl.Npad, (int)pl.Npad, wT + (v0 / pl.Vc) * pl.dpad * pl.Vc, pl.dpad, d, (int)vc, tiles_tok_m,
+                  tiles_d, n_act, kDynM};
       EpiDH e{N, d, d_hidden, v0 == 0, act_idx, n_act};
       if (int rc = launch_gemm(g, e, stream)) return rc;
     }

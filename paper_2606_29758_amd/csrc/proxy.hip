@@ -23,6 +23,7 @@
 
 #include "common.h"
 #include "gemm.h"
+#include "layout.h"
 
 namespace pspo {
 namespace {
@@ -30,7 +31,7 @@ namespace {
 constexpr float kNegInf = -INFINITY;
 
 // rows = vocabulary (A = W), columns = tokens (B = H).  Writes, per column and
-// 256-row vocabulary tile, (m, S1, S2) over the tile's rows other than the
+// 384-row vocabulary tile, (m, S1, S2) over the tile's rows other than the
 // column's target, and the target logit.
 struct EpiProxy {
   int V, N;
@@ -46,38 +47,40 @@ struct EpiProxy {
     const int vbase = tm * kTileM + acc_row(wm, 0, 0, lane);   // this lane's rows: vbase + i*16 + r
     const bool full = (tm + 1) * kTileM <= V;                   // every row of the tile is a token id
     // the targets of the lane's 8 columns, fetched together
-    int tgts[kBlocks];
+    int tgts[kBlocksN];
 #pragma unroll
-    for (int j = 0; j < kBlocks; ++j) {
+    for (int j = 0; j < kBlocksN; ++j) {
       const int t = tn * kTileN + acc_col(wn, j, lane);
       tgts[j] = t < N ? target[t] : -1;
     }
 #pragma unroll
-    for (int j = 0; j < kBlocks; ++j) asm volatile("" ::"v"(tgts[j]));   // keep the batch: no sinking
+    for (int j = 0; j < kBlocksN; ++j) asm volatile("" ::"v"(tgts[j]));   // keep the batch: no sinking
+    // the target logits are stored after the column loop (a conditional store
+    // inside it makes the compiler keep far more accumulator copies live)
+    float zvs[kBlocksN];
+    bool has[kBlocksN];
 #pragma unroll
-    for (int j = 0; j < kBlocks; ++j) {
+    for (int j = 0; j < kBlocksN; ++j) {
       const int cl = acc_col(wn, j, lane);
-      const int t = tn * kTileN + cl;
       const int tgt = tgts[j];
-      float zv;
-      if (acc_pick(acc, j, tgt - vbase, zv)) zt[t] = zv;
+      has[j] = acc_pick(acc, j, tgt - vbase, zvs[j]);
       float m = kNegInf;
 #pragma unroll
-      for (int i = 0; i < kBlocks; ++i)
+      for (int i = 0; i < kBlocksM; ++i)
 #pragma unroll
         for (int r = 0; r < kAccPerBlock; ++r)
-          if (full || vbase + i * 16 + r < V) m = fmaxf(m, acc.c[i][j][r]);
+          if (full || vbase + i * 16 + r < V) m = fmaxf(m, acc_get(acc, i, j, r));
       m = fmaxf(m, __shfl_xor(m, 16));
       m = fmaxf(m, __shfl_xor(m, 32));
       float s1 = 0.f, s2 = 0.f;
       if (m != kNegInf) {
 #pragma unroll
-        for (int i = 0; i < kBlocks; ++i)
+        for (int i = 0; i < kBlocksM; ++i)
 #pragma unroll
           for (int r = 0; r < kAccPerBlock; ++r) {
             const int v = vbase + i * 16 + r;
             // the target's own entry is left out (selected away, not subtracted)
-            const float e = ((full || v < V) && v != tgt) ? __expf(acc.c[i][j][r] - m) : 0.f;
+            const float e = ((full || v < V) && v != tgt) ? __expf(acc_get(acc, i, j, r) - m) : 0.f;
             s1 += e;
             s2 += e * e;
           }
@@ -87,16 +90,19 @@ struct EpiProxy {
       s2 += __shfl_xor(s2, 16);
       s2 += __shfl_xor(s2, 32);
       if (lane < 16) {
-        float* o = red + (wm * 256 + cl) * 3;
+        float* o = red + (wm * kTileN + cl) * 3;
         o[0] = m;
         o[1] = s1;
         o[2] = s2;
       }
     }
+#pragma unroll
+    for (int j = 0; j < kBlocksN; ++j)
+      if (has[j]) zt[tn * kTileN + acc_col(wn, j, lane)] = zvs[j];
     __syncthreads();
     const int c = threadIdx.x;
     const float* a = red + c * 3;
-    const float* b = red + (256 + c) * 3;
+    const float* b = red + (kTileN + c) * 3;
     const float M = fmaxf(a[0], b[0]);
     float S1 = 0.f, S2 = 0.f;
     if (a[0] != kNegInf) {
@@ -178,10 +184,10 @@ __global__ __launch_bounds__(256) void proxy_finalize_kernel(int N, int V, int n
 
 struct ProxyPlan {
   int64_t Npad, Vpad, ntv;
-  int64_t off_m, off_s1, off_s2, off_zt, off_hn, total;
+  int64_t off_m, off_s1, off_s2, off_zt, off_hn, off_wk, off_hk, total;
 };
 
-ProxyPlan make_proxy_plan(int64_t N, int64_t V) {
+ProxyPlan make_proxy_plan(int64_t N, int64_t d, int64_t V) {
   ProxyPlan p{};
   p.Npad = round_up(N > 0 ? N : 1, kTileN);
   p.Vpad = round_up(V, kTileM);
@@ -197,6 +203,8 @@ ProxyPlan make_proxy_plan(int64_t N, int64_t V) {
   p.off_s2 = take(p.ntv * p.Npad * 4);
   p.off_zt = take(p.Npad * 4);
   p.off_hn = take(p.Npad * 4);
+  p.off_wk = take(d * p.Vpad * 2);   // W, K-blocked [d/32][Vpad][32]
+  p.off_hk = take(d * p.Npad * 2);   // hidden rows, K-blocked [d/32][Npad][32]
   p.total = o;
   return p;
 }
@@ -208,7 +216,7 @@ extern "C" {
 
 size_t pspo_score_proxy_workspace_bytes(int32_t N, int32_t d, int32_t V) {
   if (N < 0 || d <= 0 || V <= 0) return 0;
-  return (size_t)pspo::make_proxy_plan(N, V).total;
+  return (size_t)pspo::make_proxy_plan(N, d, V).total;
 }
 
 int pspo_score_proxy(const uint16_t* hidden, const uint16_t* w_head, const int32_t* target, int32_t N, int32_t d,
@@ -227,7 +235,7 @@ int pspo_score_proxy(const uint16_t* hidden, const uint16_t* w_head, const int32
                PSPO_ERR_INVALID_ARG, "misaligned per-token pointer");
   PSPO_REQUIRE(workspace != nullptr && aligned(workspace, 256), PSPO_ERR_INVALID_ARG,
                "workspace must be non-NULL and 256-byte aligned");
-  const ProxyPlan pl = make_proxy_plan(N, V);
+  const ProxyPlan pl = make_proxy_plan(N, d, V);
   PSPO_REQUIRE(workspace_bytes >= (size_t)pl.total, PSPO_ERR_WORKSPACE,
                "workspace too small: need " + std::to_string(pl.total) + " bytes");
   PSPO_REQUIRE(pl.Npad <= INT32_MAX && pl.Vpad <= INT32_MAX, PSPO_ERR_UNSUPPORTED, "problem too large");
@@ -239,11 +247,20 @@ int pspo_score_proxy(const uint16_t* hidden, const uint16_t* w_head, const int32
   float* part_s2 = reinterpret_cast<float*>(ws + pl.off_s2);
   float* zt = reinterpret_cast<float*>(ws + pl.off_zt);
   float* hn = reinterpret_cast<float*>(ws + pl.off_hn);
+  uint16_t* wk = reinterpret_cast<uint16_t*>(ws + pl.off_wk);
+  uint16_t* hk = reinterpret_cast<uint16_t*>(ws + pl.off_hk);
 
   const int tiles_tok = (int)(pl.Npad / kTileN);
   const int tiles_voc = (int)pl.ntv;
+  const unsigned ksteps = (unsigned)(d / kTileK);
+  hipLaunchKernelGGL(kblock_rows_kernel, dim3(ksteps, (unsigned)(pl.Vpad / 64)), dim3(256), 0, stream, w_head,
+                     (int64_t)d, V, nullptr, nullptr, wk, pl.Vpad);
+  PSPO_HIP_CHECK(hipGetLastError());
+  hipLaunchKernelGGL(kblock_rows_kernel, dim3(ksteps, (unsigned)(pl.Npad / 64)), dim3(256), 0, stream, hidden,
+                     (int64_t)d, N, nullptr, nullptr, hk, pl.Npad);
+  PSPO_HIP_CHECK(hipGetLastError());
   {
-    GemmShape g{w_head, d, V, hidden, d, N, d, tiles_voc, tiles_tok};
+    GemmShape g{wk, pl.Vpad, V, hk, pl.Npad, N, d, tiles_voc, tiles_tok};
     EpiProxy e{V, N, pl.Npad, target, part_m, part_s1, part_s2, zt};
     hipLaunchKernelGGL(gemm_nt_kernel<EpiProxy>, dim3(gemm_grid(tiles_voc, tiles_tok)), dim3(kGemmThreads), 0,
                        stream, g, e);
