@@ -20,7 +20,12 @@ nonzero advantage (the only ones whose loss term can be nonzero) and n_bwd the
 tokens whose logit gradient is not identically zero (the others add nothing to
 dH or dW); the kernels skip the rest.
 `dense_equivalent_tflops` is 6 N V d / duration, the rate a path that ran the
-gradient products over every token would need for the same throughput.  `cpu_baseline` times the float64 CPU oracle on a bounded sample of
+gradient products over every token would need for the same throughput.
+`full_trajectory_control` times the untruncated update on the same batch, and
+`reseed_check` (after the timed steps) averages the truncated update over 64
+cutoff draws: that mean must equal one weighted full-trajectory call (the
+estimator is linear in the keep indicators), and its distance from the plain
+full update is reported next to the paper's diagonal variance prediction.  `cpu_baseline` times the float64 CPU oracle on a bounded sample of
 the same step (all cutoffs and packing, then the loss of the first
 --cpu-tokens packed tokens).
 """
@@ -61,7 +66,11 @@ def parse():
     ap.add_argument("--cpu-tokens", type=int, default=4096)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-full-control", action="store_true",
-                    help="skip timing the full-trajectory control (every xi = 1) on the same batch")
+                    help="skip the full-trajectory control on the same batch: its timing (every xi = 1) "
+                         "and the reseed check")
+    ap.add_argument("--reseeds", type=int, default=64,
+                    help="cutoff draws averaged by the reseed check (after the timed steps; 0 skips it): "
+                         "their mean update against the full-trajectory one")
     ap.add_argument("--pass", dest="which", choices=["update", "xi"], default="update",
                     help="update: the policy-update hot path (default); xi: computing the cutoff "
                          "tables (score proxy over every completion token + cutoff design)")
@@ -274,6 +283,16 @@ def main():
         torch.cuda.synchronize()
         full = {"tokens": Nf, "loss_call_ms": fs.elapsed_time(fe) / nrep}
         del step_full, dw_full
+    # the reseed check (after the timed region): the mean of the truncated update over
+    # --reseeds cutoff draws against the weighted and the plain full-trajectory calls
+    reseed = None
+    if not args.no_full_control and args.reseeds > 0:
+        t0 = time.perf_counter()
+        res = pipeline.reseed_mean(step, range(args.reseeds), want_logp=True)
+        reseed = pipeline.reseed_summary(dw, res)
+        del res
+        torch.cuda.synchronize()
+        reseed["seconds"] = time.perf_counter() - t0
     st = out["stats"].cpu().numpy()
     n_fwd = N - int(st[2])   # tokens of completions with A != 0: the forward's columns
     n_bwd = int(st[4])       # tokens with a nonzero logit-gradient row
@@ -340,6 +359,8 @@ def main():
     }
     if full is not None:
         result["full_trajectory_control"] = dict(full, prefix_vs_full_ratio=loss_avg / full["loss_call_ms"])
+    if reseed is not None:
+        result["reseed_check"] = reseed
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(wl, logp_old, args.cpu_tokens, args.seed)
     print(json.dumps(result), flush=True)

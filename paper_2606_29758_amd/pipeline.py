@@ -87,3 +87,98 @@ class Step:
         out["N"] = N
         out["cutoffs"] = self.cutoffs
         return out
+
+
+def reseed_mean(step: "Step", seeds, want_logp: bool = False) -> dict:
+    """Mean of the truncated update over cutoff draws, and the full-trajectory calls it is checked against.
+
+    PS-PPO's truncated estimate (Sec. 3.2; App. B) is linear in the keep
+    indicators: the clip mask depends on the ratio only, never on the cutoff.
+    So the mean over S seeds of the loss, dW and dH (dH rows accumulated at
+    their full-trajectory positions) equals one call over every completion
+    token with weight n_t c_t / S, where c_t is the token's cutoff weight and
+    n_t the number of seeds that kept it.  That identity holds up to rounding.
+    A call with every weight 1 gives the full update G that the estimator is
+    unbiased for; the distance of the S-draw mean from it is a sample of the
+    estimator's noise (App. C).
+
+    Returns float64 host scalars and device tensors: mean_loss, weighted_loss, full_loss,
+    mean_dw, weighted_dw, full_dw, mean_dh, weighted_dh, full_dh (dH rows in full order),
+    kept (n_t, int32), weight_full (c_t), logp_full (log-probs of the full call, if asked),
+    tokens.
+    """
+    dw = step.dw
+    seeds = list(seeds)
+    S = len(seeds)
+    if S == 0:
+        raise ValueError("need at least one seed")
+    dev = dw.lengths.device
+    total = dw.capacity
+    acc_dw = torch.zeros((dw.V, dw.d), dtype=torch.float32, device=dev)
+    acc_dh = torch.zeros((max(total, 1), dw.d), dtype=torch.float32, device=dev)
+    kept = torch.zeros(max(total, 1), dtype=torch.int32, device=dev)
+    loss_sum = 0.0
+    for i, s in enumerate(seeds):
+        pk = step.sample_and_pack(s)
+        N = int(pk["n_tokens"].item())
+        out = step.loss(pk, N, flags=pspo.PSPO_ACCUMULATE_DW if i > 0 else 0, want_logp=False)
+        loss_sum += float(out["loss"].item())
+        if N > 0:
+            src = pk["src_row"][:N].long()
+            acc_dh.index_add_(0, src, out["d_hidden"])
+            kept.index_add_(0, src, torch.ones(N, dtype=torch.int32, device=dev))
+    acc_dw.copy_(step.d_w)   # the accumulated sum over the S draws
+    # every token of every completion: cutoffs at the lengths; c_t is the weight the packer gives it
+    full_cut = dw.lengths.clone()
+    pk = pspo.pack_prefixes(full_cut, dw.lengths, dw.xi, dw.xi_off, dw.P, dw.K, total,
+                            target_full=dw.target_full, logp_old_full=dw.logp_old_full,
+                            hidden_full=dw.hidden_full, err_flag=step.err)
+    c_full = pk["weight"][:total].clone()
+
+    def call(weight):
+        pk["weight"][:total] = weight
+        out = step.loss(pk, total, want_logp=want_logp)
+        return (float(out["loss"].item()), step.d_w.clone(), out["d_hidden"][:total].clone(),
+                None if out["logp_new"] is None else out["logp_new"][:total].clone())
+
+    wl, wdw, wdh, _ = call(c_full * kept[:total].to(torch.float32) / S)
+    fl, fdw, fdh, flp = call(torch.ones_like(c_full))
+    return dict(mean_loss=loss_sum / S, weighted_loss=wl, full_loss=fl,
+                mean_dw=acc_dw / S, weighted_dw=wdw, full_dw=fdw,
+                mean_dh=acc_dh[:total] / S, weighted_dh=wdh, full_dh=fdh,
+                kept=kept[:total], weight_full=c_full, logp_full=flp, tokens=total, seeds=S)
+
+
+def reseed_summary(dw: DeviceWorkload, res: dict) -> dict:
+    """Scalars of a reseed_mean result.
+
+    identity: how far the S-draw mean is from the weighted full call (rounding only):
+    loss relative error, dW and dH relative L2 errors.  mean_vs_full: the relative
+    distance of the mean dW from the full update G, and App. C's diagonal prediction of
+    it, sqrt(sum_t (1/xi_t - 1) ||g_t||^2 / S) / ||G||, with ||g_t||^2 = delta_t^2 ||h_t||^2
+    ||e_o - p_t||^2 = delta_t^2 gamma_t (gamma from the score proxy, delta_t the token's
+    logit-gradient scale at weight 1, from the full call's log-probs).  Needs
+    res['logp_full'] (reseed_mean(..., want_logp=True)).
+    """
+    f32 = lambda x: float(np.float32(x))
+    rel = lambda a, b: float(torch.linalg.vector_norm((a - b).double()) / torch.linalg.vector_norm(b.double()))
+    S = res["seeds"]
+    total = res["tokens"]
+    G = res["full_dw"]
+    gamma = pspo.score_proxy(dw.hidden_full, dw.w_head, dw.target_full, total, want_logp=False)["gamma"].double()
+    rho = torch.exp(res["logp_full"].double() - dw.logp_old_full[:total].double())
+    seq = torch.repeat_interleave(torch.arange(dw.P * dw.K, device=G.device), dw.lengths.long())
+    A = dw.advantage.double()[seq]
+    mu = ((A > 0) & (rho <= 1 + f32(dw.eps_high))) | ((A < 0) & (rho >= 1 - f32(dw.eps_low)))
+    delta = -f32(dw.loss_scale) * mu.double() * rho * A
+    var = torch.sum((res["weight_full"].double() - 1.0) * delta ** 2 * gamma) / S
+    return {
+        "seeds": S,
+        "tokens": total,
+        "identity": {"loss_rel": abs(res["mean_loss"] - res["weighted_loss"]) / abs(res["weighted_loss"]),
+                     "dw_rel_l2": rel(res["mean_dw"], res["weighted_dw"]),
+                     "dh_rel_l2": rel(res["mean_dh"], res["weighted_dh"])},
+        "mean_vs_full": {"dw_rel_dev": rel(res["mean_dw"], G),
+                         "app_c_diagonal_prediction": float(torch.sqrt(var) / torch.linalg.vector_norm(G.double())),
+                         "loss_mean": res["mean_loss"], "loss_full": res["full_loss"]},
+    }
