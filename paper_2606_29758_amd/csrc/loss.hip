@@ -121,23 +121,48 @@ struct EpiForward {
   }
 };
 
-// Lane exchange inside a quad of lanes (DPP quad_perm): value of lane l ^ 1 / l ^ 2.
+// Lane exchanges (all lanes active): DPP inside a quad (lane l ^ 1, l ^ 2) and
+// inside a 16-lane row (the value of lane l + 4 / l - 4).
 __device__ __forceinline__ uint32_t quad_xor1(uint32_t x) {
   return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0xB1, 0xF, 0xF, false);
 }
 __device__ __forceinline__ uint32_t quad_xor2(uint32_t x) {
   return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x4E, 0xF, 0xF, false);
 }
+__device__ __forceinline__ uint32_t row_from_plus4(uint32_t x) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x104, 0xF, 0xF, false);   // row_shl:4
+}
+__device__ __forceinline__ uint32_t row_from_minus4(uint32_t x) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x114, 0xF, 0xF, false);   // row_shr:4
+}
+
+// 4 x 4 transpose of bf16 pairs inside a quad of lanes: lane k holds rows 0..3 of
+// token k as (r0 | r1 << 16, r2 | r3 << 16) and receives row k of tokens 0..3.
+__device__ __forceinline__ u32x2 quad_transpose(u32x2 p, int k) {
+  const bool lo2 = k < 2;
+  const uint32_t r1 = quad_xor2(lo2 ? p.y : p.x);
+  const uint32_t qa = lo2 ? p.x : r1, qb = lo2 ? r1 : p.y;   // tokens k%2 and k%2+2, rows 2(k/2), +1
+  const bool even = (k & 1) == 0;
+  const uint32_t r2 = quad_xor1(even ? ((qa >> 16) | (qb & 0xFFFF0000u)) : ((qa & 0xFFFFu) | (qb << 16)));
+  u32x2 o;
+  o.x = even ? ((qa & 0xFFFFu) | (r2 << 16)) : ((r2 & 0xFFFFu) | (qa & 0xFFFF0000u));
+  o.y = even ? ((qb & 0xFFFFu) | (r2 & 0xFFFF0000u)) : ((r2 >> 16) | (qb & 0xFFFF0000u));
+  return o;
+}
 
 // Backward logit gradient for one vocabulary chunk: rows = vocabulary rows
 // v0 + vl (A = W[v0:]), columns = the compacted tokens that carry gradient
 // (column t is token tok[t], t < *n_dev).  Writes bf16 Delta in both K-blocked
 // layouts (vocabulary rows for dW, token rows for dH); zero outside t < *n_dev,
-// v < V.  Straight from registers: a lane's 4 consecutive rows of a block are
-// 4 consecutive K entries of the token-major layout (one 8-byte store); for the
-// vocabulary-major layout the 4 x 4 (rows x tokens) blocks of a quad of lanes
-// are transposed with two quad exchanges, so each lane stores 4 consecutive
-// tokens of one row.
+// v < V.  Straight from registers, as 16-byte stores of which each instruction
+// fills 16 whole 64-byte K rows (1 KB contiguous).  Blocks are taken two row
+// blocks x two column blocks at a time:
+//   * token-major: a lane's 4 rows of a block are 4 consecutive K entries of
+//     its token; swapping 16-lane rows (v_permlane16_swap) between the two row
+//     blocks gives each lane 8 consecutive K entries;
+//   * vocabulary-major: a 4 x 4 transpose inside each quad of lanes gives a
+//     lane 4 consecutive tokens of one row; exchanging with the quad 4 lanes
+//     away (DPP row shift) between the two column blocks gives it 8.
 struct EpiDelta {
   int V, N, v0;
   const int32_t* target;
@@ -171,59 +196,88 @@ struct EpiDelta {
       lss[j] = tv ? lse[tos[j]] : 0.f;
       tgs[j] = tv ? target[tos[j]] : -1;
     }
-    // Delta without a branch per value: columns past n have delta 0, and
-    // exp(min(z - lse, 0)) equals exp(z - lse) for the others (lse >= every
-    // logit) while staying finite for them.
     // Store addresses: a per-tile base (uniform) plus a 32-bit byte offset per
-    // lane and block (a tile spans 12 K blocks of the token-major layout and 8
-    // of the vocabulary-major one, far below 4 GB); 64-bit addresses for all
-    // 96 blocks would not fit in the registers left beside the accumulators.
-    const int k = lane & 3;
+    // lane and block group (a tile spans 12 K blocks of the token-major layout
+    // and 8 of the vocabulary-major one, far below 4 GB).
+    const int k = lane & 3, q = (lane >> 2) & 3, g = lane >> 4;
+    const bool qeven = (q & 1) == 0;
     unsigned char* nbase = reinterpret_cast<unsigned char*>(
         dN + ((int64_t)(tm * (kTileM / kTileK)) * rN + tn * kTileN) * kTileK);
     unsigned char* tbase = reinterpret_cast<unsigned char*>(
         dT + ((int64_t)(tn * (kTileN / kTileK)) * rT + tm * kTileM) * kTileK);
     const uint32_t kstepN = (uint32_t)rN * (kTileK * 2), kstepT = (uint32_t)rT * (kTileK * 2);
-    // token-major: lane holds chunk rows wm*192 + (lane/16)*4 + i*16 + r of token
-    // wn*128 + j*16 + lane%16 (tile-local); K block (row / 32), entry row % 32
+    // token-major: after the row swap the lane holds K entries
+    // 16 (g % 2) + 8 (g / 2) .. +7 of its token wn*128 + j*16 + lane%16
     const uint32_t noff = (uint32_t)(wm * (kWaveM / kTileK)) * kstepN +
-                          (uint32_t)(wn * kWaveN + (lane & 15)) * (kTileK * 2) + (uint32_t)(lane >> 4) * 8;
-    // vocabulary-major: after the exchanges lane k holds row wm*192 + (lane/16)*4
-    // + i*16 + k for tokens wn*128 + j*16 + (lane & 12) .. +3
+                          (uint32_t)(wn * kWaveN + (lane & 15)) * (kTileK * 2) +
+                          (uint32_t)((g & 1) * 16 + (g >> 1) * 8) * 2;
+    // vocabulary-major: after the exchanges the lane holds row wm*192 + i*16 +
+    // 4g + k, tokens 16 (q % 2) + 8 (q / 2) .. +7 of the column-block pair
     const uint32_t toff = (uint32_t)(wn * (kWaveN / kTileK)) * kstepT +
-                          (uint32_t)(wm * kWaveM + (lane >> 4) * 4 + k) * (kTileK * 2) + (uint32_t)(lane & 12) * 2;
+                          (uint32_t)(wm * kWaveM + g * 4 + k) * (kTileK * 2) +
+                          (uint32_t)((q & 1) * 16 + (q >> 1) * 8) * 2;
 #pragma unroll
-    for (int j = 0; j < kBlocksN; ++j) {
-      const float dl = dls[j];
-      const float ls = lss[j];
-      const int tgt = tgs[j];
+    for (int jp = 0; jp < kBlocksN / 2; ++jp) {
 #pragma unroll
-      for (int i = 0; i < kBlocksM; ++i) {
-        uint32_t x[kAccPerBlock];
+      for (int ip = 0; ip < kBlocksM / 2; ++ip) {
+        // Delta of the four blocks, packed as bf16 pairs: blk[ii][jj] = rows
+        // 0,1 | rows 2,3 of row block 2 ip + ii, column block 2 jp + jj.
+        // Without a branch per value: columns past n have delta 0, and
+        // exp(min(z - lse, 0)) equals exp(z - lse) for the others (lse >=
+        // every logit) while staying finite for them.
+        u32x2 blk[2][2];
 #pragma unroll
-        for (int r = 0; r < kAccPerBlock; ++r) {
-          const int v = vbase + i * 16 + r;
-          float dv = dl * ((v == tgt ? 1.f : 0.f) - __expf(fminf(acc_get(acc, i, j, r) - ls, 0.f)));
-          if (!full) dv = (v < V) ? dv : 0.f;
-          x[r] = f32_to_bf16_bits(dv);
+        for (int ii = 0; ii < 2; ++ii)
+#pragma unroll
+          for (int jj = 0; jj < 2; ++jj) {
+            const int i = 2 * ip + ii, j = 2 * jp + jj;
+            uint32_t x[kAccPerBlock];
+#pragma unroll
+            for (int r = 0; r < kAccPerBlock; ++r) {
+              const int v = vbase + i * 16 + r;
+              float dv = dls[j] * ((v == tgs[j] ? 1.f : 0.f) - __expf(fminf(acc_get(acc, i, j, r) - lss[j], 0.f)));
+              if (!full) dv = (v < V) ? dv : 0.f;
+              x[r] = f32_to_bf16_bits(dv);
+            }
+            blk[ii][jj].x = x[0] | (x[1] << 16);
+            blk[ii][jj].y = x[2] | (x[3] << 16);
+          }
+        // token-major stores, one per column block
+#pragma unroll
+        for (int jj = 0; jj < 2; ++jj) {
+          const auto sx = __builtin_amdgcn_permlane16_swap(blk[0][jj].x, blk[1][jj].x, false, false);
+          const auto sy = __builtin_amdgcn_permlane16_swap(blk[0][jj].y, blk[1][jj].y, false, false);
+          u32x4 o;
+          o.x = sx[0];
+          o.y = sy[0];
+          o.z = sx[1];
+          o.w = sy[1];
+          *reinterpret_cast<u32x4*>(nbase + (noff + (uint32_t)ip * kstepN +
+                                             (uint32_t)((2 * jp + jj) * 16 * kTileK * 2))) = o;
         }
-        const uint32_t p0 = x[0] | (x[1] << 16), p1 = x[2] | (x[3] << 16);
-        u32x2 tokmaj;
-        tokmaj.x = p0;
-        tokmaj.y = p1;
-        *reinterpret_cast<u32x2*>(nbase + (noff + (uint32_t)(i >> 1) * kstepN + (uint32_t)(j * 16 * kTileK * 2 +
-                                                                                         (i & 1) * 32))) = tokmaj;
-        const bool lo2 = k < 2;
-        const uint32_t r1 = quad_xor2(lo2 ? p1 : p0);
-        const uint32_t qa = lo2 ? p0 : r1, qb = lo2 ? r1 : p1;   // tokens k%2 and k%2+2, rows 2(k/2), +1
-        const bool even = (k & 1) == 0;
-        const uint32_t r2 = quad_xor1(even ? ((qa >> 16) | (qb & 0xFFFF0000u)) : ((qa & 0xFFFFu) | (qb << 16)));
-        u32x2 vocmaj;
-        vocmaj.x = even ? ((qa & 0xFFFFu) | (r2 << 16)) : ((r2 & 0xFFFFu) | (qa & 0xFFFF0000u));
-        vocmaj.y = even ? ((qb & 0xFFFFu) | (r2 & 0xFFFF0000u)) : ((r2 >> 16) | (qb & 0xFFFF0000u));
-        *reinterpret_cast<u32x2*>(tbase + (toff + (uint32_t)(j >> 1) * kstepT +
-                                           (uint32_t)(i * 16 * kTileK * 2 + (j & 1) * 32))) = vocmaj;
-        __builtin_amdgcn_sched_barrier(0);   // one block's values live at a time
+        // vocabulary-major stores, one per row block
+#pragma unroll
+        for (int ii = 0; ii < 2; ++ii) {
+          const u32x2 t0 = quad_transpose(blk[ii][0], k), t1 = quad_transpose(blk[ii][1], k);
+          const u32x2 send = qeven ? t1 : t0;
+          // both shifts in every lane, then a select: written as a select of
+          // two lane exchanges, the compiler may branch on the condition, and
+          // a DPP move reads nothing from lanes its EXEC mask has switched off
+          uint32_t px = row_from_plus4(send.x), mx = row_from_minus4(send.x);
+          uint32_t py = row_from_plus4(send.y), my = row_from_minus4(send.y);
+          asm volatile("" : "+v"(px), "+v"(mx), "+v"(py), "+v"(my));
+          u32x2 recv;
+          recv.x = qeven ? px : mx;
+          recv.y = qeven ? py : my;
+          u32x4 o;
+          o.x = qeven ? t0.x : recv.x;
+          o.y = qeven ? t0.y : recv.y;
+          o.z = qeven ? recv.x : t1.x;
+          o.w = qeven ? recv.y : t1.y;
+          *reinterpret_cast<u32x4*>(tbase + (toff + (uint32_t)jp * kstepT +
+                                             (uint32_t)((2 * ip + ii) * 16 * kTileK * 2))) = o;
+        }
+        __builtin_amdgcn_sched_barrier(0);   // one group's values live at a time
       }
     }
   }
