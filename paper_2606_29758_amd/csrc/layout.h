@@ -9,61 +9,58 @@
 namespace pspo {
 namespace {
 
-// K-blocked copy of (selected) bf16 rows: row t of dst is row idx[t] (or t) of
-// the row-major `src` (cols columns, a multiple of 32) for t < n, where
-// n = min(rows, *n_dev) (or rows), and zeros for n <= t.  With n_dev, rows at
-// or past the next multiple of kTileLcm above n are not written (no product
-// reads them).  Grid (cols / 32, rows_pad / 64), 256 threads: thread -> row
-// blockIdx.y * 64 + tid / 4, 16-byte chunk tid % 4 of that row's K step.
+// K-blocked copies of (selected) bf16 rows, in one pass over the source.
+// Row t of the copy is row idx[t] (or t) of the row-major `src` (cols columns,
+// a multiple of 64) for t < n, where n = min(rows, *n_dev) (or rows), and zero
+// for n <= t.  With n_dev, 32-row blocks at or past the next multiple of
+// kTileLcm above n are not written (no product reads them).
+//   dst_kb (if not NULL): the rows K-blocked with R_kb rows per K block:
+//     element (t, c) at ((c / 32) * R_kb + t) * 32 + c % 32;
+//   dst_t (if not NULL): their transpose, in blocks of `chunk` rows (a
+//     multiple of 32), each K-blocked with R_t >= cols rows per K block:
+//     element (t, c) at (t / chunk) * R_t * chunk + (((t % chunk) / 32) * R_t + c) * 32 + t % 32
+//     (rows cols .. R_t-1 of each K block are left unwritten).
+// Grid (cols / 64, rows_pad / 32), 256 threads: a 32 x 64 tile, one 16-byte
+// piece per thread in and out; the transposed pieces go through LDS and are
+// written as whole 64-byte K rows (each output row of the tile is 32 source rows).
 __global__ __launch_bounds__(256) void kblock_rows_kernel(const uint16_t* __restrict__ src, int64_t ld_src, int rows,
                                                           const int32_t* __restrict__ idx,
                                                           const int32_t* __restrict__ n_dev,
-                                                          uint16_t* __restrict__ dst, int64_t R) {
+                                                          uint16_t* __restrict__ dst_kb, int64_t R_kb,
+                                                          uint16_t* __restrict__ dst_t, int64_t R_t, int64_t chunk) {
+  __shared__ uint16_t tile[32][64 + 8];   // padded rows: the column reads below hit distinct banks
   int n = rows;
-  const int t = blockIdx.y * 64 + (threadIdx.x >> 2);
+  const int r0 = blockIdx.y * 32, c0 = blockIdx.x * 64;
   if (n_dev != nullptr) {
     n = min(n, *n_dev);
-    if (t >= (n + kTileLcm - 1) / kTileLcm * kTileLcm) return;
+    if (r0 >= (n + kTileLcm - 1) / kTileLcm * kTileLcm) return;
   }
-  const int ks = blockIdx.x, q = threadIdx.x & 3;
-  u32x4 v = {0u, 0u, 0u, 0u};
-  if (t < n) {
-    const int64_t s = idx != nullptr ? idx[t] : t;
-    v = *reinterpret_cast<const u32x4*>(src + s * ld_src + ks * kTileK + q * 8);
+  const int tid = threadIdx.x;
+  // in: row r0 + tid / 8, columns c0 + (tid % 8) * 8 .. +7
+  {
+    const int r = r0 + (tid >> 3), cp = (tid & 7) * 8;
+    u32x4 v = {0u, 0u, 0u, 0u};
+    if (r < n) {
+      const int64_t s = idx != nullptr ? idx[r] : r;
+      v = *reinterpret_cast<const u32x4*>(src + s * ld_src + c0 + cp);
+    }
+    const int c = c0 + cp;
+    if (dst_kb != nullptr)
+      *reinterpret_cast<u32x4*>(dst_kb + ((int64_t)(c >> 5) * R_kb + r) * kTileK + (c & 31)) = v;
+    if (dst_t != nullptr) *reinterpret_cast<u32x4*>(&tile[tid >> 3][cp]) = v;
   }
-  *reinterpret_cast<u32x4*>(dst + ((int64_t)ks * R + t) * kTileK + q * 8) = v;
-}
-
-// Transposed, zero-padded copy of a bf16 [rows x cols] matrix, in blocks of
-// `chunk` source rows, each block K-blocked with R >= cols rows per K block:
-// source row r, column c goes to
-//   dst[(r / chunk) * R * chunk + (((r % chunk) / 32) * R + c) * 32 + r % 32]
-// (0 for r >= rows), i.e. block b is the [cols x chunk] transpose of rows
-// [b*chunk, (b+1)*chunk) with each 32-deep K step contiguous (rows cols..R-1
-// of each K step are left unwritten).  64 x 64 tiles through LDS; cols, chunk
-// and the padded row count are multiples of 64.
-// Optionally, row r of the source is row rmap[r] of `src` and only the first
-// min(rows, *n_dev) rows are present; 64-row blocks wholly past that count are
-// not written (no product reads them).
-__global__ __launch_bounds__(256) void transpose_pad_kernel(const uint16_t* __restrict__ src, int rows, int cols,
-                                                            int64_t ld_src, uint16_t* __restrict__ dst, int64_t R,
-                                                            int64_t chunk, const int32_t* __restrict__ rmap,
-                                                            const int32_t* __restrict__ n_dev) {
-  __shared__ uint16_t tile[64][66];
-  const int c0 = blockIdx.x * 64, r0 = blockIdx.y * 64;
-  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
-  if (n_dev != nullptr) {
-    rows = min(rows, *n_dev);
-    if (r0 >= (rows + 63) / 64 * 64) return;
-  }
-  for (int rr = ty; rr < 64; rr += 4) {
-    const int r = r0 + rr;
-    tile[rr][tx] = (r < rows) ? src[(int64_t)(rmap ? rmap[r] : r) * ld_src + c0 + tx] : (uint16_t)0;
-  }
+  if (dst_t == nullptr) return;
   __syncthreads();
-  const int64_t block = r0 / chunk, rin = r0 % chunk + tx;
-  uint16_t* out = dst + block * R * chunk + ((rin / kTileK) * R) * kTileK + rin % kTileK;
-  for (int cc = ty; cc < 64; cc += 4) out[(int64_t)(c0 + cc) * kTileK] = tile[tx][cc];
+  // out: column c0 + tid / 4 of source rows r0 + (tid % 4) * 8 .. +7
+  {
+    const int cl = tid >> 2, rp = (tid & 3) * 8;
+    uint32_t w[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) w[e] = (uint32_t)tile[rp + 2 * e][cl] | ((uint32_t)tile[rp + 2 * e + 1][cl] << 16);
+    u32x4 v = {w[0], w[1], w[2], w[3]};
+    const int64_t blk = r0 / chunk, rin = r0 % chunk;   // 32-row blocks never straddle a chunk
+    *reinterpret_cast<u32x4*>(dst_t + blk * R_t * chunk + ((rin >> 5) * R_t + c0 + cl) * kTileK + rp) = v;
+  }
 }
 
 }  // namespace

@@ -9,16 +9,17 @@
 //   dH_i = G_i W,  dW = sum_i G_i^T h_i.
 //
 // Schedule (the [N, V] logits never reach memory):
-//   1. K-blocked bf16 copies of W and of the hidden rows of the tokens whose
-//      logits are needed (the operand layout of the matrix-core products);
+//   1. K-blocked bf16 copies of W (with, per vocabulary chunk, W[chunk]^T) and
+//      of the hidden rows of the tokens whose logits are needed (the operand
+//      layout of the matrix-core products);
 //   2. forward product z^T = W H^T in 384 x 256 tiles; the epilogue reduces
 //      each tile column (one token) to a partial (max, sum exp) over the tile's
 //      384 vocabulary rows and picks up the target logit;
 //   3. finalize: merge the partials into lse, then l, rho, the clip mask, delta
 //      and a deterministic float64 loss reduction;
-//   4. K-blocked copies of the backward tokens' hidden rows, of their
-//      transpose H^T [d x Npad] and, per vocabulary chunk, of W[chunk]^T
-//      [d x Vc] (K-contiguous operands of the gradient products);
+//   4. K-blocked copies of the backward tokens' hidden rows and of their
+//      transpose H^T [d x Npad] (K-contiguous operands of the gradient
+//      products);
 //   5. per vocabulary chunk of Vc rows: recompute the chunk's logit tiles and
 //      write the bf16 logit gradient Delta = delta (e_o - exp(z - lse)) in both
 //      layouts ([Npad x Vc] and [Vc x Npad]); then dW[chunk] = Delta^T H and
@@ -720,18 +721,20 @@ int pspo_loss_fwd_bwd(const uint16_t* hidden, const uint16_t* w_head, const int3
   const int tiles_tok_m = (int)(pl.Npad / kTileM);    // tokens on the A side
   const int tiles_voc = (int)pl.ntv;
   const int tiles_d = (int)(pl.dpad / kTileN);
-  const unsigned ksteps = (unsigned)(d / kTileK);
+  const unsigned ctiles64 = (unsigned)(d / 64);
 
   // 1. the tokens whose logits are needed (all of them if logp_new is wanted);
   //    W and their hidden rows as K-blocked operands
   hipLaunchKernelGGL(compact_forward_kernel, dim3(1), dim3(kCompactThreads), 0, stream, N, R,
                      logp_new != nullptr ? 1 : 0, seq_id, advantage, fwd_idx, fwd_pos, n_fwd);
   PSPO_HIP_CHECK(hipGetLastError());
-  hipLaunchKernelGGL(kblock_rows_kernel, dim3(ksteps, (unsigned)(pl.Vpad / 64)), dim3(256), 0, stream, w_head,
-                     (int64_t)d, V, nullptr, nullptr, wk, pl.Vpad);
+  // W K-blocked (forward and logit-gradient products) and, per vocabulary
+  // chunk, W[chunk]^T (dH product), in one pass over W
+  hipLaunchKernelGGL(kblock_rows_kernel, dim3(ctiles64, (unsigned)(pl.Vpad / 32)), dim3(256), 0, stream, w_head,
+                     (int64_t)d, V, nullptr, nullptr, wk, pl.Vpad, wT, pl.dpad, pl.Vc);
   PSPO_HIP_CHECK(hipGetLastError());
-  hipLaunchKernelGGL(kblock_rows_kernel, dim3(ksteps, (unsigned)(pl.Npad / 64)), dim3(256), 0, stream, hidden,
-                     (int64_t)d, N, fwd_idx, n_fwd, hk, pl.Npad);
+  hipLaunchKernelGGL(kblock_rows_kernel, dim3(ctiles64, (unsigned)(pl.Npad / 32)), dim3(256), 0, stream, hidden,
+                     (int64_t)d, N, fwd_idx, n_fwd, hk, pl.Npad, nullptr, (int64_t)0, (int64_t)kTileK);
   PSPO_HIP_CHECK(hipGetLastError());
   // 2. forward logits -> per-tile softmax partials and target logits
   {
@@ -755,15 +758,10 @@ int pspo_loss_fwd_bwd(const uint16_t* hidden, const uint16_t* w_head, const int3
   hipLaunchKernelGGL(zero_inactive_rows_kernel, dim3((unsigned)N), dim3(256), 0, stream, d, delta, d_hidden);
   PSPO_HIP_CHECK(hipGetLastError());
   // 5. operands of the gradient products: the backward tokens' hidden rows
-  //    (K-blocked, in the forward's buffer), H[bwd]^T and per chunk W[chunk]^T
-  hipLaunchKernelGGL(kblock_rows_kernel, dim3(ksteps, (unsigned)(pl.Npad / 64)), dim3(256), 0, stream, hidden,
-                     (int64_t)d, N, act_idx, n_act, hk, pl.Npad);
-  PSPO_HIP_CHECK(hipGetLastError());
-  hipLaunchKernelGGL(transpose_pad_kernel, dim3(d / 64, (unsigned)(pl.Npad / 64)), dim3(256), 0, stream, hidden, N,
-                     d, (int64_t)d, hT, pl.dpad, pl.Npad, act_idx, n_act);   // H[active]^T [dpad x Npad]
-  PSPO_HIP_CHECK(hipGetLastError());
-  hipLaunchKernelGGL(transpose_pad_kernel, dim3(d / 64, (unsigned)(pl.Vpad / 64)), dim3(256), 0, stream, w_head, V,
-                     d, (int64_t)d, wT, pl.dpad, pl.Vc, nullptr, nullptr);  // per chunk: W[chunk]^T [dpad x Vc]
+  //    (K-blocked, in the forward's buffer) and their transpose H[bwd]^T
+  //    [dpad x Npad], in one pass
+  hipLaunchKernelGGL(kblock_rows_kernel, dim3(ctiles64, (unsigned)(pl.Npad / 32)), dim3(256), 0, stream, hidden,
+                     (int64_t)d, N, act_idx, n_act, hk, pl.Npad, hT, pl.dpad, pl.Npad);
   PSPO_HIP_CHECK(hipGetLastError());
   // 6. backward, one vocabulary chunk at a time; every product is bounded by
   //    the active-token count in device memory

@@ -252,12 +252,12 @@ int pspo_score_proxy(const uint16_t* hidden, const uint16_t* w_head, const int32
 
   const int tiles_tok = (int)(pl.Npad / kTileN);
   const int tiles_voc = (int)pl.ntv;
-  const unsigned ksteps = (unsigned)(d / kTileK);
-  hipLaunchKernelGGL(kblock_rows_kernel, dim3(ksteps, (unsigned)(pl.Vpad / 64)), dim3(256), 0, stream, w_head,
-                     (int64_t)d, V, nullptr, nullptr, wk, pl.Vpad);
+  const unsigned ctiles64 = (unsigned)(d / 64);
+  hipLaunchKernelGGL(kblock_rows_kernel, dim3(ctiles64, (unsigned)(pl.Vpad / 32)), dim3(256), 0, stream, w_head,
+                     (int64_t)d, V, nullptr, nullptr, wk, pl.Vpad, nullptr, (int64_t)0, (int64_t)kTileK);
   PSPO_HIP_CHECK(hipGetLastError());
-  hipLaunchKernelGGL(kblock_rows_kernel, dim3(ksteps, (unsigned)(pl.Npad / 64)), dim3(256), 0, stream, hidden,
-                     (int64_t)d, N, nullptr, nullptr, hk, pl.Npad);
+  hipLaunchKernelGGL(kblock_rows_kernel, dim3(ctiles64, (unsigned)(pl.Npad / 32)), dim3(256), 0, stream, hidden,
+                     (int64_t)d, N, nullptr, nullptr, hk, pl.Npad, nullptr, (int64_t)0, (int64_t)kTileK);
   PSPO_HIP_CHECK(hipGetLastError());
   {
     GemmShape g{wk, pl.Vpad, V, hk, pl.Npad, N, d, tiles_voc, tiles_tok};
