@@ -375,20 +375,63 @@ __global__ void fill_f32_kernel(float* __restrict__ p, int64_t n, float v) {
 }
 
 constexpr int kFinThreads = 256;
-constexpr int kCompactThreads = 1024;
+constexpr int kCompactThreads = 256, kCompactPer = 8, kCompactSpan = kCompactThreads * kCompactPer;
 
-// Order-preserving compaction of the tokens t < N with keep(t), by one block
-// (each thread owns a contiguous slice): idx[0 .. count) are their indices in
-// increasing order; pos[t] (if pos is not NULL) is t's place in idx, or -1.
-// Returns the count in every thread.
+// Order-preserving compaction of the tokens t < N with keep(t) in two
+// launches over blocks of kCompactSpan consecutive tokens: the first counts
+// each block's kept tokens; the second adds the counts of the blocks before
+// it and scatters: idx[0 .. count) are the kept indices in increasing order,
+// pos[t] (if pos is not NULL) is t's place in idx or -1; the last block writes
+// the count (and stats[4], if asked).
 template <class Keep>
-__device__ int compact_tokens(int N, Keep keep, int32_t* __restrict__ idx, int32_t* __restrict__ pos) {
+__global__ __launch_bounds__(kCompactThreads) void compact_count_kernel(int N, Keep keep, int32_t* __restrict__ cnt) {
   __shared__ int sh[kCompactThreads];
-  const int per = (N + kCompactThreads - 1) / kCompactThreads;
-  const int t0 = min(N, (int)threadIdx.x * per), t1 = min(N, t0 + per);
-  int cnt = 0;
-  for (int t = t0; t < t1; ++t) cnt += keep(t) ? 1 : 0;
-  sh[threadIdx.x] = cnt;
+  const int base = blockIdx.x * kCompactSpan;
+  int c = 0;
+#pragma unroll
+  for (int e = 0; e < kCompactPer; ++e) {
+    const int t = base + e * kCompactThreads + threadIdx.x;
+    c += (t < N && keep(t)) ? 1 : 0;
+  }
+  sh[threadIdx.x] = c;
+  __syncthreads();
+  for (int s = kCompactThreads / 2; s > 0; s >>= 1) {
+    if (threadIdx.x < s) sh[threadIdx.x] += sh[threadIdx.x + s];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) cnt[blockIdx.x] = sh[0];
+}
+
+template <class Keep>
+__global__ __launch_bounds__(kCompactThreads) void compact_scatter_kernel(int N, Keep keep,
+                                                                          const int32_t* __restrict__ cnt,
+                                                                          int32_t* __restrict__ idx,
+                                                                          int32_t* __restrict__ pos,
+                                                                          int32_t* __restrict__ count,
+                                                                          double* __restrict__ stats) {
+  __shared__ int sh[kCompactThreads];
+  // this block's offset: the kept tokens of the blocks before it
+  int o = 0;
+  for (int k = threadIdx.x; k < (int)blockIdx.x; k += kCompactThreads) o += cnt[k];
+  sh[threadIdx.x] = o;
+  __syncthreads();
+  for (int s = kCompactThreads / 2; s > 0; s >>= 1) {
+    if (threadIdx.x < s) sh[threadIdx.x] += sh[threadIdx.x + s];
+    __syncthreads();
+  }
+  o = sh[0];
+  __syncthreads();
+  // each thread owns kCompactPer consecutive tokens (the order of the output)
+  const int t0 = blockIdx.x * kCompactSpan + threadIdx.x * kCompactPer;
+  bool kept[kCompactPer];
+  int c = 0;
+#pragma unroll
+  for (int e = 0; e < kCompactPer; ++e) {
+    const int t = t0 + e;
+    kept[e] = t < N && keep(t);
+    c += kept[e] ? 1 : 0;
+  }
+  sh[threadIdx.x] = c;
   __syncthreads();
   for (int off = 1; off < kCompactThreads; off <<= 1) {
     const int v = threadIdx.x >= off ? sh[threadIdx.x - off] : 0;
@@ -396,14 +439,20 @@ __device__ int compact_tokens(int N, Keep keep, int32_t* __restrict__ idx, int32
     sh[threadIdx.x] += v;
     __syncthreads();
   }
-  int p = sh[threadIdx.x] - cnt;
-  for (int t = t0; t < t1; ++t) {
-    const bool k = keep(t);
-    if (k) idx[p] = t;
-    if (pos) pos[t] = k ? p : -1;
-    p += k ? 1 : 0;
+  int p = o + sh[threadIdx.x] - c;
+#pragma unroll
+  for (int e = 0; e < kCompactPer; ++e) {
+    const int t = t0 + e;
+    if (t < N) {
+      if (kept[e]) idx[p] = t;
+      if (pos) pos[t] = kept[e] ? p : -1;
+    }
+    p += kept[e] ? 1 : 0;
   }
-  return sh[kCompactThreads - 1];
+  if (blockIdx.x == gridDim.x - 1 && threadIdx.x == kCompactThreads - 1) {
+    *count = p;
+    if (stats) stats[4] = (double)p;
+  }
 }
 
 // Tokens whose logits the forward computes: all of them when every token's
@@ -411,33 +460,34 @@ __device__ int compact_tokens(int N, Keep keep, int32_t* __restrict__ idx, int32
 // makes the token's loss term and gradient exactly zero, so its logits are
 // not needed; a token with an invalid completion id is left to finalize,
 // which flags it).
-__global__ __launch_bounds__(kCompactThreads) void compact_forward_kernel(int N, int R, int all,
-                                                                          const int32_t* __restrict__ seq_id,
-                                                                          const float* __restrict__ adv,
-                                                                          int32_t* __restrict__ idx,
-                                                                          int32_t* __restrict__ pos,
-                                                                          int32_t* __restrict__ count) {
-  auto keep = [&](int t) {
+struct KeepForward {
+  int R, all;
+  const int32_t* seq_id;
+  const float* adv;
+  __device__ bool operator()(int t) const {
     if (all) return true;
     const int s = seq_id[t];
     return s >= 0 && s < R && adv[s] != 0.f;
-  };
-  const int n = compact_tokens(N, keep, idx, pos);
-  if (threadIdx.x == 0) *count = n;
-}
+  }
+};
 
 // Tokens whose logit gradient is not identically zero (delta != 0): the
-// backward products run over these only.  The count also goes to stats[4].
-__global__ __launch_bounds__(kCompactThreads) void compact_active_kernel(int N, const float* __restrict__ delta,
-                                                                         int32_t* __restrict__ idx,
-                                                                         int32_t* __restrict__ n_act,
-                                                                         double* __restrict__ stats) {
-  auto keep = [&](int t) { return delta[t] != 0.f; };
-  const int n = compact_tokens(N, keep, idx, nullptr);
-  if (threadIdx.x == 0) {
-    *n_act = n;
-    if (stats) stats[4] = (double)n;
-  }
+// backward products run over these only.
+struct KeepActive {
+  const float* delta;
+  __device__ bool operator()(int t) const { return delta[t] != 0.f; }
+};
+
+template <class Keep>
+int launch_compact(int N, const Keep& keep, int32_t* cnt, int32_t* idx, int32_t* pos, int32_t* count, double* stats,
+                   hipStream_t stream) {
+  const unsigned nblk = (unsigned)((N + kCompactSpan - 1) / kCompactSpan);
+  hipLaunchKernelGGL(compact_count_kernel<Keep>, dim3(nblk), dim3(kCompactThreads), 0, stream, N, keep, cnt);
+  PSPO_HIP_CHECK(hipGetLastError());
+  hipLaunchKernelGGL(compact_scatter_kernel<Keep>, dim3(nblk), dim3(kCompactThreads), 0, stream, N, keep, cnt, idx,
+                     pos, count, stats);
+  PSPO_HIP_CHECK(hipGetLastError());
+  return PSPO_OK;
 }
 
 // d_hidden rows of tokens with delta == 0 are exactly zero.
@@ -566,7 +616,7 @@ __global__ __launch_bounds__(kFinThreads) void reduce_loss_kernel(int nblk, cons
       stats[1] = v[2];
       stats[2] = v[3];
       stats[3] = shd[0];
-      if (nblk == 0) stats[4] = 0.0;   // otherwise written by compact_active_kernel
+      if (nblk == 0) stats[4] = 0.0;   // otherwise written by the backward-token compaction
     }
   }
 }
@@ -578,7 +628,7 @@ __global__ __launch_bounds__(kFinThreads) void reduce_loss_kernel(int nblk, cons
 
 struct Plan {
   int64_t Npad, Vpad, dpad, Vc, ntv, nfin;
-  int64_t off_pm, off_pl, off_zt, off_lse, off_delta, off_fidx, off_fpos, off_nfwd, off_idx, off_nact, off_blk, off_wk,
+  int64_t off_pm, off_pl, off_zt, off_lse, off_delta, off_fidx, off_fpos, off_nfwd, off_idx, off_nact, off_cnt, off_blk, off_wk,
       off_hk, off_ht, off_wt, off_dn, off_dt, total;
 };
 
@@ -619,6 +669,7 @@ Plan make_plan(int64_t N, int64_t d, int64_t V) {
   p.off_nfwd = take(4);
   p.off_idx = take(p.Npad * 4);
   p.off_nact = take(4);
+  p.off_cnt = take((p.Npad + kCompactSpan - 1) / kCompactSpan * 4);   // per-block counts of a compaction
   p.off_blk = take((p.nfin > 0 ? p.nfin : 1) * 5 * 8);
   p.off_wk = take(d * p.Vpad * 2);                                    // W, K-blocked [d/32][Vpad][32]
   p.off_hk = take(d * p.Npad * 2);                                    // gathered hidden rows [d/32][Npad][32]
@@ -709,6 +760,7 @@ int pspo_loss_fwd_bwd(const uint16_t* hidden, const uint16_t* w_head, const int3
   int32_t* n_fwd = reinterpret_cast<int32_t*>(ws + pl.off_nfwd);
   int32_t* act_idx = reinterpret_cast<int32_t*>(ws + pl.off_idx);
   int32_t* n_act = reinterpret_cast<int32_t*>(ws + pl.off_nact);
+  int32_t* cnt = reinterpret_cast<int32_t*>(ws + pl.off_cnt);
   double* blk = reinterpret_cast<double*>(ws + pl.off_blk);
   uint16_t* wk = reinterpret_cast<uint16_t*>(ws + pl.off_wk);
   uint16_t* hk = reinterpret_cast<uint16_t*>(ws + pl.off_hk);
@@ -725,9 +777,9 @@ int pspo_loss_fwd_bwd(const uint16_t* hidden, const uint16_t* w_head, const int3
 
   // 1. the tokens whose logits are needed (all of them if logp_new is wanted);
   //    W and their hidden rows as K-blocked operands
-  hipLaunchKernelGGL(compact_forward_kernel, dim3(1), dim3(kCompactThreads), 0, stream, N, R,
-                     logp_new != nullptr ? 1 : 0, seq_id, advantage, fwd_idx, fwd_pos, n_fwd);
-  PSPO_HIP_CHECK(hipGetLastError());
+  if (int rc = launch_compact(N, KeepForward{R, logp_new != nullptr ? 1 : 0, seq_id, advantage}, cnt, fwd_idx,
+                              fwd_pos, n_fwd, nullptr, stream))
+    return rc;
   // W K-blocked (forward and logit-gradient products) and, per vocabulary
   // chunk, W[chunk]^T (dH product), in one pass over W
   hipLaunchKernelGGL(kblock_rows_kernel, dim3(ctiles64, (unsigned)(pl.Vpad / 32)), dim3(256), 0, stream, w_head,
@@ -752,9 +804,7 @@ int pspo_loss_fwd_bwd(const uint16_t* hidden, const uint16_t* w_head, const int3
   PSPO_HIP_CHECK(hipGetLastError());
   // 4. the backward runs over the tokens with delta != 0 only (every other
   //    token has a zero logit-gradient row: zero d_hidden row, no dW term)
-  hipLaunchKernelGGL(compact_active_kernel, dim3(1), dim3(kCompactThreads), 0, stream, N, delta, act_idx, n_act,
-                     stats);
-  PSPO_HIP_CHECK(hipGetLastError());
+  if (int rc = launch_compact(N, KeepActive{delta}, cnt, act_idx, nullptr, n_act, stats, stream)) return rc;
   hipLaunchKernelGGL(zero_inactive_rows_kernel, dim3((unsigned)N), dim3(256), 0, stream, d, delta, d_hidden);
   PSPO_HIP_CHECK(hipGetLastError());
   // 5. operands of the gradient products: the backward tokens' hidden rows
