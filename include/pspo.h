@@ -57,6 +57,10 @@ typedef enum {
 
 /* Flags of pspo_loss_fwd_bwd. */
 #define PSPO_ACCUMULATE_DW   1u /* d_w_head += gradient instead of d_w_head = gradient */
+#define PSPO_RECOMPUTE_LOGITS 2u /* recompute every logit tile in the backward instead of keeping the
+                                    first vocabulary chunk's fp32 logits from the forward: the same
+                                    results (bitwise), a smaller workspace (by Vc x Npad x 4 bytes),
+                                    more matrix-core work */
 
 /* Human-readable name of a status code (static storage). */
 const char* pspo_status_string(int status);
@@ -160,9 +164,12 @@ size_t pspo_loss_workspace_bytes(int32_t N, int32_t d, int32_t V, uint32_t flags
  *             (A > 0 and rho <= 1+eps_high, or A < 0 and rho >= 1-eps_low);
  *   G_i     = delta_i (e_{o_i} - softmax(z_i))     (App. D: grad log p(o) = (e_o - p) h^T)
  *   d_hidden[i] = G_i W,   d_w_head = sum_i G_i^T h_i.
- * The [N, V] logits are never written to memory: the kernels recompute logit
- * tiles on the matrix cores, keeping only per-token softmax statistics and a
- * bounded vocabulary chunk of bf16 logit gradients in the workspace.
+ * The [N, V] logits are never written to memory whole: the workspace holds
+ * per-token softmax statistics, one vocabulary chunk of bf16 logit gradients
+ * (in two layouts) and the fp32 logits of the first chunk, kept by the forward
+ * so that the backward recomputes the logit tiles of the other chunks only.
+ * The chunk is Vc = 384 * 256 / gcd(ceil(d / 256), 256) vocabulary rows (the
+ * whole padded vocabulary if that is smaller); 49152 at d = 3584.
  *
  *  hidden     device, bf16 bits [N, d] row-major (packed prefix tokens).
  *  w_head     device, bf16 bits [V, d] row-major.
@@ -171,7 +178,7 @@ size_t pspo_loss_workspace_bytes(int32_t N, int32_t d, int32_t V, uint32_t flags
  *  N >= 0, R >= 1 if N > 0, V >= 1, d > 0 with d % 64 == 0.  All device
  *  pointers 16-byte aligned.
  *  eps_low, eps_high in [0, 1); loss_scale finite (e.g. 1/(P*K)).
- *  flags      PSPO_ACCUMULATE_DW or 0.
+ *  flags      PSPO_ACCUMULATE_DW | PSPO_RECOMPUTE_LOGITS or 0.
  *  loss       device, float64 [1] out.
  *  d_hidden   device, float32 [N, d] out.
  *  d_w_head   device, float32 [V, d] out (or accumulated, see flags).

@@ -88,6 +88,11 @@ struct GemmShape {
   // Tiles outside the bound exit at once; a shorter K shortens the loop.
   const int32_t* dyn = nullptr;
   int dyn_dim = kDynNone;
+  // Row tiles 0 .. spread_m-1 are placed evenly among the others in launch
+  // order (and so spread over the XCDs, each of which takes a contiguous run
+  // of the order) instead of first: for an epilogue that does extra work on
+  // those tiles only.
+  int spread_m = 0;
 };
 
 // Accumulator (i, j, r) of lane `lane` in wave (wm, wn) holds
@@ -137,7 +142,17 @@ __device__ __forceinline__ int chunk_swizzle(int row) { return ((row >> 1) ^ (ro
 // product needs when M or N is bounded on the device).  The tile count is
 // taken from the actual M and N so that the work spreads over all XCDs even
 // when a device-side bound leaves only part of the launch with work.
-__device__ __forceinline__ bool map_tile(int tiles_m, int tiles_n, int M, int N, int& tm, int& tn) {
+// Row tile of launch-order position l when the first s of T row tiles are
+// spread: position l holds one of them iff the count ceil((l + 1) s / T) of
+// such slots up to l grows at l (slots evenly spaced, in increasing order);
+// the other tiles keep their order.  A bijection on [0, T).
+__device__ __forceinline__ int spread_row_tile(int l, int s, int T) {
+  const int c = ((l + 1) * s + T - 1) / T, cp = (l * s + T - 1) / T;
+  return c > cp ? c - 1 : s + l - c;
+}
+
+__device__ __forceinline__ bool map_tile(int tiles_m, int tiles_n, int M, int N, int& tm, int& tn,
+                                         int spread_m = 0) {
   tiles_m = min(tiles_m, (M + kTileM - 1) / kTileM);
   tiles_n = min(tiles_n, (N + kTileN - 1) / kTileN);
   const int total = tiles_m * tiles_n;
@@ -152,6 +167,7 @@ __device__ __forceinline__ bool map_tile(int tiles_m, int tiles_n, int M, int N,
   const int rem = t % width;
   tm = first + rem % gsize;
   tn = rem / gsize;
+  if (spread_m > 0) tm = spread_row_tile(tm, min(spread_m, tiles_m), tiles_m);
   return true;
 }
 
@@ -224,7 +240,7 @@ void gemm_nt_kernel(GemmShape g, Epi epi) {
     else if (g.dyn_dim == kDynK) K = min(K, (v + kTileK - 1) / kTileK * kTileK);
   }
   int tm, tn;
-  if (!map_tile(g.tiles_m, g.tiles_n, M, N, tm, tn)) return;
+  if (!map_tile(g.tiles_m, g.tiles_n, M, N, tm, tn, g.spread_m)) return;
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;

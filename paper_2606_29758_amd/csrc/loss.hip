@@ -20,10 +20,14 @@
 //   4. K-blocked copies of the backward tokens' hidden rows and of their
 //      transpose H^T [d x Npad] (K-contiguous operands of the gradient
 //      products);
-//   5. per vocabulary chunk of Vc rows: recompute the chunk's logit tiles and
-//      write the bf16 logit gradient Delta = delta (e_o - exp(z - lse)) in both
-//      layouts ([Npad x Vc] and [Vc x Npad]); then dW[chunk] = Delta^T H and
-//      dH += Delta W[chunk] as two more matrix-core products.
+//   5. per vocabulary chunk of Vc rows: the bf16 logit gradient
+//      Delta = delta (e_o - exp(z - lse)) of the chunk in both layouts
+//      ([Npad x Vc] and [Vc x Npad]), then dW[chunk] = Delta^T H and
+//      dH += Delta W[chunk] as two more matrix-core products.  The first
+//      chunk's fp32 logits are kept by the forward (one chunk, the size of the
+//      Delta buffers), so its Delta is a memory-bound conversion; the other
+//      chunks recompute their logit tiles on the matrix cores (every chunk
+//      does with PSPO_RECOMPUTE_LOGITS).
 #include <cmath>
 
 #include "common.h"
@@ -39,6 +43,16 @@ constexpr float kNegInf = -INFINITY;
 // Epilogues
 // ---------------------------------------------------------------------------
 
+// One entry of the logit gradient, delta (1[v = o] - exp(z - lse)) (the
+// objective of Sec. 3.1 differentiated through the log-softmax of App. D).
+// exp(min(z - lse, 0)) equals exp(z - lse) for every real entry (lse bounds
+// each logit) and stays finite for padding columns, whose delta is 0.  The
+// recomputing product and the kept-logit conversion both use it, so they
+// produce the same bits.
+__device__ __forceinline__ float logit_grad(float z, float lse, float delta, bool is_target) {
+  return delta * ((is_target ? 1.f : 0.f) - __expf(fminf(z - lse, 0.f)));
+}
+
 // Forward: rows = vocabulary (A = W), columns = the tokens whose logits are
 // needed (B = their hidden rows, gathered; column t is token tok[t]); writes
 // per-column softmax partials of each 384-row vocabulary tile and the target
@@ -52,9 +66,46 @@ struct EpiForward {
   float* zt;
   const int32_t* tok;    // column t is token tok[t] (columns t < *n_dev)
   const int32_t* n_dev;
+  float* zk;             // kept fp32 logits of vocabulary tiles tm < kept_tiles, or NULL:
+  int kept_tiles;        //   per tile (tm, tn) a block at (tm * kept_cols + tn) * 384 * 256,
+  int kept_cols;         //   [12 blocks of 32 rows][256 columns][32]
 
   __device__ __forceinline__ void apply(const AccTile& acc, int tm, int tn, int wm, int wn, int lane, float* smem) const {
     float* red = smem;  // [2 wave rows][256 columns][m, l]
+    if (zk != nullptr && tm < kept_tiles) {
+      // the tile's fp32 logits, kept for the first backward chunk, as one
+      // contiguous 384 x 256 block (few address translations per tile):
+      // [12 blocks of 32 vocabulary rows][256 columns][32]; the lane's 4 rows
+      // of an accumulator block are one 16-byte piece of a column's 128-byte
+      // row, and a store instruction fills 16 consecutive rows' halves
+      unsigned char* zb = reinterpret_cast<unsigned char*>(zk + ((int64_t)tm * kept_cols + tn) * (kTileM * kTileN));
+      uint32_t lo = (uint32_t)(wm * (kWaveM / 32)) * (kTileN * 128u) + (uint32_t)(wn * kWaveN + (lane & 15)) * 128u +
+                    (uint32_t)(lane >> 4) * 16u;
+#pragma unroll
+      for (int i = 0; i < kBlocksM; ++i) {
+#pragma unroll
+        for (int j = 0; j < kBlocksN; ++j) {
+          // AGPR blocks are read by explicit v_accvgpr_read: taken as one
+          // 4-register value, the compiler keeps a VGPR copy of the block
+          // live from the loop's end and spills accumulators to make room
+          f32x4 b;
+          if (i < kBlocksAgpr) {
+#pragma unroll
+            for (int r = 0; r < kAccPerBlock; ++r) {
+              float x;
+              asm volatile("v_accvgpr_read_b32 %0, %1" : "=v"(x) : "a"(acc.a[i][j][r]));
+              b[r] = x;
+            }
+          } else {
+            b = acc.v[i - kBlocksAgpr][j];
+          }
+          __builtin_nontemporal_store(b, reinterpret_cast<f32x4*>(zb + (lo + (uint32_t)(j * 2048))));
+        }
+        lo += (i & 1) ? kTileN * 128u - 64u : 64u;
+        __builtin_amdgcn_sched_barrier(0);   // one row block's stores at a time
+      }
+    }
+    __builtin_amdgcn_sched_barrier(0);
     const int n = min(N, __builtin_amdgcn_readfirstlane(*n_dev));
     const int vbase = tm * kTileM + acc_row(wm, 0, 0, lane);   // this lane's rows: vbase + i*16 + r
     const bool full = (tm + 1) * kTileM <= V;                   // every row of the tile is a token id
@@ -222,10 +273,8 @@ struct EpiDelta {
 #pragma unroll
       for (int ip = 0; ip < kBlocksM / 2; ++ip) {
         // Delta of the four blocks, packed as bf16 pairs: blk[ii][jj] = rows
-        // 0,1 | rows 2,3 of row block 2 ip + ii, column block 2 jp + jj.
-        // Without a branch per value: columns past n have delta 0, and
-        // exp(min(z - lse, 0)) equals exp(z - lse) for the others (lse >=
-        // every logit) while staying finite for them.
+        // 0,1 | rows 2,3 of row block 2 ip + ii, column block 2 jp + jj
+        // (columns past n have delta 0: no branch per value).
         u32x2 blk[2][2];
 #pragma unroll
         for (int ii = 0; ii < 2; ++ii)
@@ -236,7 +285,7 @@ struct EpiDelta {
 #pragma unroll
             for (int r = 0; r < kAccPerBlock; ++r) {
               const int v = vbase + i * 16 + r;
-              float dv = dls[j] * ((v == tgs[j] ? 1.f : 0.f) - __expf(fminf(acc_get(acc, i, j, r) - lss[j], 0.f)));
+              float dv = logit_grad(acc_get(acc, i, j, r), lss[j], dls[j], v == tgs[j]);
               if (!full) dv = (v < V) ? dv : 0.f;
               x[r] = f32_to_bf16_bits(dv);
             }
@@ -283,6 +332,73 @@ struct EpiDelta {
     }
   }
 };
+
+// The logit gradient of the first vocabulary chunk from the forward's kept
+// fp32 logits (zk: per 384 x 256 forward tile (tm, tn) a block at
+// (tm * kept_cols + tn) * 384 * 256, [12 blocks of 32 rows][256 columns][32])
+// instead of a recomputing product: the values and layouts the
+// logit-gradient epilogue writes for that chunk.  Backward column a < n =
+// min(N, *n_dev) is token act[a], whose logits sit in forward column
+// fpos[act[a]]; columns n <= a <
+// round_up(n, 32) are written as the zero gradient of a padding column (the
+// dW product reads whole 32-token K steps); rows v >= V are zero.
+// Grid (Vc / 64, Npad / 32), 256 threads: 32 backward tokens x 64 vocabulary
+// entries per block; the token-major pieces go straight out, the
+// vocabulary-major ones through LDS as whole 64-byte K rows.
+__global__ __launch_bounds__(256) void logit_grad_kept_kernel(const float* __restrict__ zk, int kept_cols, int V, int N,
+                                                              const int32_t* __restrict__ n_dev,
+                                                              const int32_t* __restrict__ act,
+                                                              const int32_t* __restrict__ fpos,
+                                                              const int32_t* __restrict__ target,
+                                                              const float* __restrict__ lse,
+                                                              const float* __restrict__ delta,
+                                                              uint16_t* __restrict__ dN, int64_t rN,
+                                                              uint16_t* __restrict__ dT, int64_t rT) {
+  __shared__ uint16_t tile[32][64 + 8];   // padded rows: the column reads below hit distinct banks
+  const int n = min(N, *n_dev);
+  const int a0 = blockIdx.y * 32, v0 = blockIdx.x * 64;
+  if (a0 >= n) return;
+  const int tid = threadIdx.x;
+  // in: column a0 + tid / 8, entries v0 + (tid % 8) * 8 .. +7
+  {
+    const int a = a0 + (tid >> 3), v = v0 + (tid & 7) * 8;
+    float dl = 0.f, ls = 0.f;
+    int tg = -1;
+    f32x4 z0 = {0.f, 0.f, 0.f, 0.f}, z1 = {0.f, 0.f, 0.f, 0.f};
+    if (a < n) {
+      const int t = act[a];
+      dl = delta[t];
+      ls = lse[t];
+      tg = target[t];
+      const int f = fpos[t], vt = v / kTileM;
+      const float* s = zk + ((int64_t)vt * kept_cols + (f >> 8)) * (kTileM * kTileN) +
+                       ((((v - vt * kTileM) >> 5) * kTileN + (f & (kTileN - 1))) * 32 + (v & 31));
+      z0 = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(s));
+      z1 = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(s + 4));
+    }
+    uint32_t x[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float z = e < 4 ? z0[e] : z1[e - 4];
+      float g = logit_grad(z, ls, dl, v + e == tg);
+      if (v + e >= V) g = 0.f;
+      x[e] = f32_to_bf16_bits(g);
+    }
+    const u32x4 o = {x[0] | (x[1] << 16), x[2] | (x[3] << 16), x[4] | (x[5] << 16), x[6] | (x[7] << 16)};
+    *reinterpret_cast<u32x4*>(dN + ((int64_t)(v >> 5) * rN + a) * kTileK + (v & 31)) = o;
+    *reinterpret_cast<u32x4*>(&tile[tid >> 3][(tid & 7) * 8]) = o;
+  }
+  __syncthreads();
+  // out: entry v0 + tid / 4 of columns a0 + (tid % 4) * 8 .. +7
+  {
+    const int vl = tid >> 2, ap = (tid & 3) * 8;
+    uint32_t w[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) w[e] = (uint32_t)tile[ap + 2 * e][vl] | ((uint32_t)tile[ap + 2 * e + 1][vl] << 16);
+    const u32x4 o = {w[0], w[1], w[2], w[3]};
+    *reinterpret_cast<u32x4*>(dT + ((int64_t)(a0 >> 5) * rT + v0 + vl) * kTileK + ap) = o;
+  }
+}
 
 // dW rows v0 + vl (A = Delta^T), columns = hidden features (B = H^T).
 // Addresses are a per-tile base plus 32-bit byte offsets (a tile spans
@@ -629,10 +745,11 @@ __global__ __launch_bounds__(kFinThreads) void reduce_loss_kernel(int nblk, cons
 struct Plan {
   int64_t Npad, Vpad, dpad, Vc, ntv, nfin;
   int64_t off_pm, off_pl, off_zt, off_lse, off_delta, off_fidx, off_fpos, off_nfwd, off_idx, off_nact, off_cnt, off_blk, off_wk,
-      off_hk, off_ht, off_wt, off_dn, off_dt, total;
+      off_hk, off_ht, off_wt, off_dn, off_dt, off_zk, total;
+  bool keep;   // the forward keeps the first chunk's fp32 logits
 };
 
-Plan make_plan(int64_t N, int64_t d, int64_t V) {
+Plan make_plan(int64_t N, int64_t d, int64_t V, bool keep) {
   Plan p{};
   p.Npad = round_up(N > 0 ? N : 1, kTileLcm);   // token rows: tiles of 256 (B side) and 384 (A side)
   p.Vpad = round_up(V, kTileM);
@@ -677,6 +794,8 @@ Plan make_plan(int64_t N, int64_t d, int64_t V) {
   p.off_wt = take(p.dpad * ((p.Vpad + p.Vc - 1) / p.Vc) * p.Vc * 2);  // per chunk: W^T [Vc/32][dpad][32]
   p.off_dn = take(p.Npad * p.Vc * 2);                                 // K-blocked [Vc/32][Npad][32]
   p.off_dt = take(p.Vc * p.Npad * 2);                                 // K-blocked [Npad/32][Vc][32]
+  p.keep = keep;
+  p.off_zk = take(keep ? p.Vc * p.Npad * 4 : 0);                      // kept fp32 logits, one block per forward tile
   p.total = o;
   return p;
 }
@@ -695,9 +814,8 @@ int launch_gemm(const GemmShape& g, const Epi& epi, hipStream_t stream) {
 extern "C" {
 
 size_t pspo_loss_workspace_bytes(int32_t N, int32_t d, int32_t V, uint32_t flags) {
-  (void)flags;
   if (N < 0 || d <= 0 || V <= 0) return 0;
-  return (size_t)pspo::make_plan(N, d, V).total;
+  return (size_t)pspo::make_plan(N, d, V, (flags & PSPO_RECOMPUTE_LOGITS) == 0).total;
 }
 
 int pspo_loss_fwd_bwd(const uint16_t* hidden, const uint16_t* w_head, const int32_t* target, const float* logp_old,
@@ -711,7 +829,8 @@ int pspo_loss_fwd_bwd(const uint16_t* hidden, const uint16_t* w_head, const int3
   PSPO_REQUIRE(d > 0 && V > 0, PSPO_ERR_INVALID_ARG, "d and V must be > 0");
   PSPO_REQUIRE(d % 64 == 0, PSPO_ERR_UNSUPPORTED, "d must be a multiple of 64");
   PSPO_REQUIRE(N == 0 || R > 0, PSPO_ERR_INVALID_ARG, "R must be > 0 when N > 0");
-  PSPO_REQUIRE((flags & ~PSPO_ACCUMULATE_DW) == 0, PSPO_ERR_INVALID_ARG, "unknown flag bits");
+  PSPO_REQUIRE((flags & ~(PSPO_ACCUMULATE_DW | PSPO_RECOMPUTE_LOGITS)) == 0, PSPO_ERR_INVALID_ARG,
+               "unknown flag bits");
   PSPO_REQUIRE(std::isfinite(eps_low) && eps_low >= 0.f && eps_low < 1.f, PSPO_ERR_INVALID_ARG,
                "eps_low must lie in [0, 1)");
   PSPO_REQUIRE(std::isfinite(eps_high) && eps_high >= 0.f && eps_high < 1.f, PSPO_ERR_INVALID_ARG,
@@ -731,7 +850,7 @@ int pspo_loss_fwd_bwd(const uint16_t* hidden, const uint16_t* w_head, const int3
                  "workspace must be non-NULL and 256-byte aligned");
   }
   if (stats) PSPO_REQUIRE(aligned(stats, 8), PSPO_ERR_INVALID_ARG, "misaligned stats");
-  const Plan pl = make_plan(N, d, V);
+  const Plan pl = make_plan(N, d, V, (flags & PSPO_RECOMPUTE_LOGITS) == 0);
   PSPO_REQUIRE(N == 0 || workspace_bytes >= (size_t)pl.total, PSPO_ERR_WORKSPACE,
                "workspace too small: need " + std::to_string(pl.total) + " bytes");
   PSPO_REQUIRE(pl.Npad <= INT32_MAX && pl.Vpad <= INT32_MAX, PSPO_ERR_UNSUPPORTED, "problem too large");
@@ -768,6 +887,7 @@ int pspo_loss_fwd_bwd(const uint16_t* hidden, const uint16_t* w_head, const int3
   uint16_t* wT = reinterpret_cast<uint16_t*>(ws + pl.off_wt);
   uint16_t* dN = reinterpret_cast<uint16_t*>(ws + pl.off_dn);
   uint16_t* dT = reinterpret_cast<uint16_t*>(ws + pl.off_dt);
+  float* zk = pl.keep ? reinterpret_cast<float*>(ws + pl.off_zk) : nullptr;
 
   const int tiles_tok_n = (int)(pl.Npad / kTileN);    // tokens on the B side
   const int tiles_tok_m = (int)(pl.Npad / kTileM);    // tokens on the A side
@@ -790,8 +910,10 @@ int pspo_loss_fwd_bwd(const uint16_t* hidden, const uint16_t* w_head, const int3
   PSPO_HIP_CHECK(hipGetLastError());
   // 2. forward logits -> per-tile softmax partials and target logits
   {
-    GemmShape g{wk, pl.Vpad, V, hk, pl.Npad, N, d, tiles_voc, tiles_tok_n, n_fwd, kDynN};
-    EpiForward e{V, N, pl.Npad, target, part_m, part_l, zt, fwd_idx, n_fwd};
+    // the kept tiles' stores spread over the XCDs
+    GemmShape g{wk, pl.Vpad, V, hk, pl.Npad, N, d, tiles_voc, tiles_tok_n, n_fwd, kDynN,
+                zk != nullptr ? (int)(pl.Vc / kTileM) : 0};
+    EpiForward e{V, N, pl.Npad, target, part_m, part_l, zt, fwd_idx, n_fwd, zk, (int)(pl.Vc / kTileM), tiles_tok_n};
     if (int rc = launch_gemm(g, e, stream)) return rc;
   }
   // 3. lse, PPO terms, delta, loss
@@ -818,7 +940,12 @@ int pspo_loss_fwd_bwd(const uint16_t* hidden, const uint16_t* w_head, const int3
   for (int64_t v0 = 0; v0 < pl.Vpad; v0 += pl.Vc) {
     const int64_t vc = (pl.Vpad - v0) < pl.Vc ? (pl.Vpad - v0) : pl.Vc;
     const int ctiles = (int)(vc / kTileM);
-    {
+    if (v0 == 0 && zk != nullptr) {
+      hipLaunchKernelGGL(logit_grad_kept_kernel, dim3((unsigned)(pl.Vc / 64), (unsigned)(pl.Npad / 32)), dim3(256), 0,
+                         stream, zk, tiles_tok_n, V, N, n_act, act_idx, fwd_pos, target, lse, delta, dN, pl.Npad, dT,
+                         pl.Vc);
+      PSPO_HIP_CHECK(hipGetLastError());
+    } else {
       GemmShape g{wk + v0 * kTileK, pl.Vpad, (int)(V - v0), hk, pl.Npad, N, d, ctiles, tiles_tok_n, n_act, kDynN};
       EpiDelta e{V, N, (int)v0, target, lse, delta, dT, pl.Vc, dN, pl.Npad, act_idx, n_act};
       if (int rc = launch_gemm(g, e, stream)) return rc;

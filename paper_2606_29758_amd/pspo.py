@@ -16,6 +16,7 @@ _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libpspo.so")
 
 PSPO_ACCUMULATE_DW = 1
+PSPO_RECOMPUTE_LOGITS = 2
 DEVERR_TARGET, DEVERR_BAD_XI, DEVERR_CAPACITY, DEVERR_SEQ_ID = 1, 2, 4, 8
 
 _P = ctypes.c_void_p

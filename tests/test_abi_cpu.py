@@ -122,7 +122,7 @@ def test_loss_argument_errors(lib):
     assert _loss(lib, V=0) == INVALID
     assert _loss(lib, d=96) == UNSUPPORTED
     assert _loss(lib, R=0) == INVALID
-    assert _loss(lib, flags=2) == INVALID
+    assert _loss(lib, flags=4) == INVALID            # unknown flag bit
     assert _loss(lib, el=1.0) == INVALID
     assert _loss(lib, eh=-0.1) == INVALID
     assert _loss(lib, el=float("nan")) == INVALID
@@ -136,6 +136,17 @@ def test_loss_argument_errors(lib):
     assert _loss(lib, ws=None) == INVALID
     assert _loss(lib, wsb=1024) == WORKSPACE
     assert b"workspace too small" in lib.pspo_last_error()
+
+
+def test_workspace_bytes_recompute_flag(lib):
+    # without PSPO_RECOMPUTE_LOGITS the forward keeps the first vocabulary
+    # chunk's fp32 logits: Vc x round_up(N, 768) x 4 bytes more (Vc = 49152 at
+    # d = 3584, the whole padded vocabulary when that is smaller)
+    for N, d, V, vc in ((1000, 3584, 152064, 49152), (300, 128, 2048, 2304), (5000, 4096, 151936, 6144)):
+        keep = lib.pspo_loss_workspace_bytes(N, d, V, 0)
+        lean = lib.pspo_loss_workspace_bytes(N, d, V, 2)
+        npad = -(-N // 768) * 768
+        assert keep - lean == vc * npad * 4, (N, d, V)
 
 
 def test_workspace_bytes(lib):

@@ -185,6 +185,30 @@ def test_without_logp_is_identical(name):
     assert rel_l2(_to_np(b["d_w_head"]), ref["d_w"]) <= GRAD_REL_L2
 
 
+@pytest.mark.parametrize("name", ["tiny", "mini7b", "mini1p5b"])
+@pytest.mark.parametrize("want_logp", [True, False])
+def test_kept_logits_match_recompute(name, want_logp):
+    """The forward keeps the first vocabulary chunk's fp32 logits and the backward turns
+    them into that chunk's logit gradient without a recomputing product: every output is
+    bitwise the one of the path that recomputes every chunk (PSPO_RECOMPUTE_LOGITS).
+    tiny has one chunk (the whole padded vocabulary); the 7B and 1.5B widths have several."""
+    wl, lp = _workload(name)
+    step = pipeline.Step(pipeline.upload(wl, lp))
+    pk = step.sample_and_pack(seed=11)
+    N = int(pk["n_tokens"].item())
+    a = step.loss(pk, N, want_logp=want_logp)
+    ka = {k: a[k].clone() for k in ("loss", "d_hidden", "d_w_head", "stats")}
+    ka_lp = a["logp_new"].clone() if want_logp else None
+    b = step.loss(pk, N, flags=pspo.PSPO_RECOMPUTE_LOGITS, want_logp=want_logp)
+    torch.cuda.synchronize()
+    for k in ka:
+        assert torch.equal(ka[k], b[k]), k
+    if want_logp:
+        assert torch.equal(ka_lp, b["logp_new"])
+    assert int(step.err.item()) == 0
+    assert float(ka["stats"][4].item()) > 32   # several 32-token K steps of backward tokens
+
+
 def test_deterministic():
     wl, lp = _workload("tiny")
     step = pipeline.Step(pipeline.upload(wl, lp))
