@@ -347,7 +347,8 @@ def main():
         "dense_equivalent_tflops": dense_equiv,
         "roofline": {
             "bound": "mfma",
-            "kernel": "pspo_loss_fwd_bwd (forward, logit-gradient, dW and dH bf16 MFMA kernels)",
+            "kernel": "pspo_loss_fwd_bwd (forward, logit-gradient, dW and dH bf16 MFMA kernels; the first "
+                      "vocabulary chunk's logit gradient converted from the forward's kept logits)",
             "flops": "(2 n_fwd + 4 n_bwd) V d per call: forward over the tokens of completions with "
                      "A != 0, dH and dW over the tokens with a nonzero logit gradient",
             "achieved": achieved,

@@ -68,19 +68,20 @@ struct EpiForward {
   const int32_t* n_dev;
   float* zk;             // kept fp32 logits of vocabulary tiles tm < kept_tiles, or NULL:
   int kept_tiles;        //   per tile (tm, tn) a block at (tm * kept_cols + tn) * 384 * 256,
-  int kept_cols;         //   [12 blocks of 32 rows][256 columns][32]
+  int kept_cols;         //   [24 blocks of 16 rows][256 columns][16]
 
   __device__ __forceinline__ void apply(const AccTile& acc, int tm, int tn, int wm, int wn, int lane, float* smem) const {
     float* red = smem;  // [2 wave rows][256 columns][m, l]
     if (zk != nullptr && tm < kept_tiles) {
       // the tile's fp32 logits, kept for the first backward chunk, as one
       // contiguous 384 x 256 block (few address translations per tile):
-      // [12 blocks of 32 vocabulary rows][256 columns][32]; the lane's 4 rows
-      // of an accumulator block are one 16-byte piece of a column's 128-byte
-      // row, and a store instruction fills 16 consecutive rows' halves
+      // [24 blocks of 16 vocabulary rows][256 columns][16].  An accumulator
+      // block is 16 rows x 16 columns, the lane's 4 rows one 16-byte piece:
+      // each store instruction writes 1 KB of whole 128-byte lines (a store
+      // of half lines makes the L2 fetch the other half from memory)
       unsigned char* zb = reinterpret_cast<unsigned char*>(zk + ((int64_t)tm * kept_cols + tn) * (kTileM * kTileN));
-      uint32_t lo = (uint32_t)(wm * (kWaveM / 32)) * (kTileN * 128u) + (uint32_t)(wn * kWaveN + (lane & 15)) * 128u +
-                    (uint32_t)(lane >> 4) * 16u;
+      const uint32_t lo = (uint32_t)(wm * (kWaveM / 16)) * (kTileN * 64u) +
+                          (uint32_t)(wn * kWaveN + (lane & 15)) * 64u + (uint32_t)(lane >> 4) * 16u;
 #pragma unroll
       for (int i = 0; i < kBlocksM; ++i) {
 #pragma unroll
@@ -99,9 +100,8 @@ struct EpiForward {
           } else {
             b = acc.v[i - kBlocksAgpr][j];
           }
-          __builtin_nontemporal_store(b, reinterpret_cast<f32x4*>(zb + (lo + (uint32_t)(j * 2048))));
+          __builtin_nontemporal_store(b, reinterpret_cast<f32x4*>(zb + (lo + (uint32_t)(i * kTileN * 64 + j * 1024))));
         }
-        lo += (i & 1) ? kTileN * 128u - 64u : 64u;
         __builtin_amdgcn_sched_barrier(0);   // one row block's stores at a time
       }
     }
@@ -335,7 +335,7 @@ struct EpiDelta {
 
 // The logit gradient of the first vocabulary chunk from the forward's kept
 // fp32 logits (zk: per 384 x 256 forward tile (tm, tn) a block at
-// (tm * kept_cols + tn) * 384 * 256, [12 blocks of 32 rows][256 columns][32])
+// (tm * kept_cols + tn) * 384 * 256, [24 blocks of 16 rows][256 columns][16])
 // instead of a recomputing product: the values and layouts the
 // logit-gradient epilogue writes for that chunk.  Backward column a < n =
 // min(N, *n_dev) is token act[a], whose logits sit in forward column
@@ -372,7 +372,7 @@ __global__ __launch_bounds__(256) void logit_grad_kept_kernel(const float* __res
       tg = target[t];
       const int f = fpos[t], vt = v / kTileM;
       const float* s = zk + ((int64_t)vt * kept_cols + (f >> 8)) * (kTileM * kTileN) +
-                       ((((v - vt * kTileM) >> 5) * kTileN + (f & (kTileN - 1))) * 32 + (v & 31));
+                       ((((v - vt * kTileM) >> 4) * kTileN + (f & (kTileN - 1))) * 16 + (v & 15));
       z0 = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(s));
       z1 = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(s + 4));
     }
