@@ -25,9 +25,16 @@ gradient products over every token would need for the same throughput.
 `reseed_check` (after the timed steps) averages the truncated update over 64
 cutoff draws: that mean must equal one weighted full-trajectory call (the
 estimator is linear in the keep indicators), and its distance from the plain
-full update is reported next to the paper's diagonal variance prediction.  `cpu_baseline` times the float64 CPU oracle on a bounded sample of
-the same step (all cutoffs and packing, then the loss of the first
---cpu-tokens packed tokens).
+full update is reported next to the paper's diagonal variance prediction.
+`recompute_logits_control` times the same loss calls with PSPO_RECOMPUTE_LOGITS
+(the backward recomputes every logit tile instead of converting the first
+vocabulary chunk's logits that the forward kept), and `mfma_loop_peak` is the
+matrix cores' sustained bf16 rate on the products' MFMA form with no memory
+traffic (the ceiling at the clock the chip holds, next to the published peak).
+`cpu_baseline` times the float64 CPU oracle on a bounded sample of the same step
+(all cutoffs and packing, then the loss of the first --cpu-tokens packed
+tokens), with the BLAS library it ran on and a single-thread rate on a
+sixteenth of that sample.
 """
 import argparse
 import json
@@ -108,10 +115,48 @@ def cpu_baseline(wl, logp_old, ntok, seed):
                        float(np.float32(cfg.eps_high)), float(np.float32(cfg.loss_scale)))
     dt = time.perf_counter() - t0
     n = sel.stop
-    threads = max([p.get("num_threads", 1) for p in threadpool_info() if p.get("user_api") == "blas"] or [1])
+    blas = [p for p in threadpool_info() if p.get("user_api") == "blas"]
+    threads = max([p.get("num_threads", 1) for p in blas] or [1])
+    # the same loss on one BLAS thread, on a smaller sample of the same tokens
+    from threadpoolctl import threadpool_limits
+    n1 = min(ntok // 16, n)
+    with threadpool_limits(limits=1, user_api="blas"):
+        t1 = time.perf_counter()
+        s1 = slice(0, n1)
+        ohead.loss_fwd_bwd(wl.hidden_bits[src[s1]], wl.w_bits, pk["target"][s1], pk["logp_old"][s1],
+                           pk["weight"][s1], pk["seq_id"][s1], wl.advantage, float(np.float32(cfg.eps_low)),
+                           float(np.float32(cfg.eps_high)), float(np.float32(cfg.loss_scale)))
+        dt1 = time.perf_counter() - t1
     return {"value": n / dt, "unit": "prefix tokens/s", "cores": int(threads), "kind": "oracle",
             "sample": f"cutoffs and packing of all {cfg.R} rollouts, then loss + gradients of the first "
-                      f"{n} packed tokens (float64 numpy, {dt:.1f} s)"}
+                      f"{n} packed tokens (float64 numpy, {dt:.1f} s)",
+            "blas": ", ".join(f"{p.get('internal_api')} {p.get('version')}" for p in blas) or "unknown",
+            "single_core": {"value": n1 / dt1, "unit": "prefix tokens/s",
+                            "sample": f"loss + gradients of the first {n1} packed tokens on one BLAS thread "
+                                      f"({dt1:.1f} s)"}}
+
+
+def mfma_loop_peak(iters=32768, blocks=1024):
+    """The matrix cores' sustained bf16 rate on the products' MFMA form with no memory
+    traffic (pspo_mfma_loop), timed with events on the current stream."""
+    import torch
+    from paper_2606_29758_amd import pspo
+    out = pspo.mfma_loop(iters, blocks)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    reps = 3
+    s.record(stream)
+    for _ in range(reps):
+        pspo.mfma_loop(iters, blocks, out)
+    e.record(stream)
+    torch.cuda.synchronize()
+    ms = s.elapsed_time(e) / reps
+    flops = blocks * 4.0 * iters * 16 * 16384
+    tf = flops / (ms * 1e-3) / 1e12
+    return {"achieved": tf, "unit": "TFLOP/s", "frac_of_peak": tf / PEAK_BF16_TFLOPS,
+            "what": f"{blocks} work-groups x 4 waves x {iters} rounds of 16 independent "
+                    f"v_mfma_f32_16x16x32_bf16, no memory traffic ({ms:.1f} ms)"}
 
 
 def bench_proxy(args):
@@ -217,7 +262,7 @@ def main():
         return
 
     import torch
-    from paper_2606_29758_amd import pipeline, synth
+    from paper_2606_29758_amd import pipeline, pspo, synth
 
     wl = synth.make_workload(args.workload)
     cfg = wl.cfg
@@ -261,6 +306,20 @@ def main():
     pack_avg = float(np.mean([a.elapsed_time(b) for a, b in pack_marks]))
     assert int(step.err.item()) == 0, "device error flag raised"
     peak_bytes = torch.cuda.max_memory_allocated()
+
+    # the same loss calls with every logit tile recomputed in the backward
+    # (PSPO_RECOMPUTE_LOGITS: no logits stored at all, a smaller workspace)
+    step.loss(pk, N, flags=pspo.PSPO_RECOMPUTE_LOGITS, want_logp=False)
+    torch.cuda.synchronize()
+    rs, re_ = ev(), ev()
+    nrep = max(3, args.steps // 2)
+    rs.record(stream)
+    for _ in range(nrep):
+        step.loss(pk, N, flags=pspo.PSPO_RECOMPUTE_LOGITS, want_logp=False)
+    re_.record(stream)
+    torch.cuda.synchronize()
+    recompute_ms = rs.elapsed_time(re_) / nrep
+    mfma_peak = mfma_loop_peak()
 
     # the full-trajectory control on the same batch (every xi = 1: the standard, untruncated
     # update): its loss-call time against the truncated one
@@ -357,6 +416,13 @@ def main():
             "frac": achieved / PEAK_BF16_TFLOPS,
             "traffic": traffic,
         },
+        "recompute_logits_control": {
+            "loss_call_ms": recompute_ms,
+            "pct_bf16_peak": 100.0 * flops / (recompute_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
+            "what": "the same calls with PSPO_RECOMPUTE_LOGITS: every logit tile recomputed in the "
+                    "backward, no logits stored",
+        },
+        "mfma_loop_peak": mfma_peak,
     }
     if full is not None:
         result["full_trajectory_control"] = dict(full, prefix_vs_full_ratio=loss_avg / full["loss_call_ms"])

@@ -315,6 +315,17 @@ int pspo_design_cutoffs(const double* w, const int64_t* xi_off, int32_t P, int64
                         void* workspace, size_t workspace_bytes, int32_t* err_flag,
                         hipStream_t stream);
 
+/*
+ * Measurement helper, not a step of the method: `blocks` work-groups of 256
+ * threads each run `iters` rounds of 16 independent v_mfma_f32_16x16x32_bf16
+ * per wave (the block form and tied accumulators of the loss products), with
+ * no memory traffic, so that a caller timing it with stream events gets the
+ * sustained bf16 matrix-core rate: blocks * 4 * iters * 16 * 16384 flops.
+ *  iters, blocks  >= 1.
+ *  out            device, float32 [blocks * 256], written (values meaningless).
+ */
+int pspo_mfma_loop(int32_t iters, int32_t blocks, float* out, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -15,7 +15,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB_NAME = "libpspo.so"
 LIB_PATH = os.path.join(PKG, LIB_NAME)
-SOURCES = ["abi.cpp", "sampler.hip", "loss.hip", "proxy.hip", "design.hip"]
+SOURCES = ["abi.cpp", "sampler.hip", "loss.hip", "proxy.hip", "design.hip", "probe.hip"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950",

@@ -40,6 +40,7 @@ _SIGNATURES = {
     "pspo_design_cutoffs": (ctypes.c_int, [_P, _P, _I32, _I64, ctypes.c_double, _I32, ctypes.c_double,
                                            _P, _P, _SZ, _P, _P]),
     "pspo_score_proxy": (ctypes.c_int, [_P, _P, _P, _I32, _I32, _I32, _P, _P, _P, _P, _P, _SZ, _P]),
+    "pspo_mfma_loop": (ctypes.c_int, [_I32, _I32, _P, _P]),
 }
 
 _lib = None
@@ -291,3 +292,15 @@ def design_cutoffs(w, xi_off, P: int, total_T: int, budget: float, variant: int 
     _check(load().pspo_design_cutoffs(_ptr(w), _ptr(xi_off), P, total_T, float(budget), int(variant), float(lam),
                                       _ptr(xi), _ptr(ws), ws.numel(), _ptr(err_flag), _stream()))
     return xi[:total_T]
+
+
+def mfma_loop(iters: int, blocks: int, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Enqueues the matrix-core rate probe (blocks * 4 * iters * 16 * 16384 bf16 flops) on the
+    current stream; the caller times it."""
+    if out is None:
+        out = torch.empty(blocks * 256, dtype=torch.float32, device="cuda")
+    _dev(out, torch.float32, "out")
+    if out.numel() < blocks * 256:
+        raise ValueError("out needs blocks * 256 floats")
+    _check(load().pspo_mfma_loop(int(iters), int(blocks), _ptr(out), _stream()))
+    return out

@@ -29,7 +29,7 @@ def _declared():
 
 def test_exports_every_declared_symbol(lib):
     names = _declared()
-    assert len(names) == 13
+    assert len(names) == 14
     for name in names:
         assert hasattr(lib, name), name
     assert sorted(pspo.exported_symbols()) == names
@@ -234,3 +234,11 @@ def test_binding_refuses_host_tensors():
     with pytest.raises(ValueError, match="device tensor"):
         pspo.sample_cutoffs(torch.ones(3, dtype=torch.float64), torch.zeros(2, dtype=torch.int64),
                             torch.ones(1, dtype=torch.int32), 1, 1, 0)
+
+
+def test_mfma_loop_argument_errors(lib):
+    out = ctypes.c_void_p(1 << 20)
+    assert lib.pspo_mfma_loop(0, 4, out, None) == INVALID
+    assert lib.pspo_mfma_loop(4, 0, out, None) == INVALID
+    assert lib.pspo_mfma_loop(4, 4, None, None) == INVALID
+    assert lib.pspo_mfma_loop(4, 4, ctypes.c_void_p((1 << 20) + 2), None) == INVALID
