@@ -156,7 +156,7 @@ def mfma_loop_peak(iters=32768, blocks=1024):
     tf = flops / (ms * 1e-3) / 1e12
     return {"achieved": tf, "unit": "TFLOP/s", "frac_of_peak": tf / PEAK_BF16_TFLOPS,
             "what": f"{blocks} work-groups x 4 waves x {iters} rounds of 16 independent "
-                    f"v_mfma_f32_16x16x32_bf16, no memory traffic ({ms:.1f} ms)"}
+                    f"v_mfma_f32_16x16x32_bf16 on random bf16 operands, no memory traffic ({ms:.1f} ms)"}
 
 
 def bench_proxy(args):

@@ -318,7 +318,8 @@ int pspo_design_cutoffs(const double* w, const int64_t* xi_off, int32_t P, int64
 /*
  * Measurement helper, not a step of the method: `blocks` work-groups of 256
  * threads each run `iters` rounds of 16 independent v_mfma_f32_16x16x32_bf16
- * per wave (the block form and tied accumulators of the loss products), with
+ * per wave (the block form and tied accumulators of the loss products, random
+ * bf16 operands alternating between consecutive MFMAs), with
  * no memory traffic, so that a caller timing it with stream events gets the
  * sustained bf16 matrix-core rate: blocks * 4 * iters * 16 * 16384 flops.
  *  iters, blocks  >= 1.

@@ -338,65 +338,99 @@ struct EpiDelta {
 // (tm * kept_cols + tn) * 384 * 256, [24 blocks of 16 rows][256 columns][16])
 // instead of a recomputing product: the values and layouts the
 // logit-gradient epilogue writes for that chunk.  Backward column a < n =
-// min(N, *n_dev) is token act[a], whose logits sit in forward column
-// fpos[act[a]]; columns n <= a <
-// round_up(n, 32) are written as the zero gradient of a padding column (the
-// dW product reads whole 32-token K steps); rows v >= V are zero.
-// Grid (Vc / 64, Npad / 32), 256 threads: 32 backward tokens x 64 vocabulary
-// entries per block; the token-major pieces go straight out, the
-// vocabulary-major ones through LDS as whole 64-byte K rows.
-__global__ __launch_bounds__(256) void logit_grad_kept_kernel(const float* __restrict__ zk, int kept_cols, int V, int N,
-                                                              const int32_t* __restrict__ n_dev,
+// min(N, *n_dev) is token act[a], whose logits sit in forward column afwd[a];
+// columns n <= a < round_up(n, 32) are written as the zero gradient of a
+// padding column (the dW product reads whole 32-token K steps); rows v >= V
+// are zero.
+// Grid (ceil(Vc / (128 kConvSeg)), Npad / 32), 256 threads: 32 backward
+// tokens x up to kConvSeg segments of 128 vocabulary entries per block, every
+// segment's logits loaded before the first is converted.  (One segment per
+// block: with four, twice the bytes in flight per thread, the kernel ran no
+// faster; it moves its bytes at ~5 TB/s, reads and writes mixed.)  Load q of
+// segment sg of thread `tid` takes the 16-byte quarter tid % 4 of token
+// (tid % 128) / 4's 64-byte piece of 16-row block 2q + tid / 128, so one load
+// instruction reads whole runs of consecutive tokens' pieces; each segment's
+// gradient goes through LDS and out in both layouts as 16-byte stores of whole
+// 64-byte K rows.
+constexpr int kConvSeg = 1;
+
+__global__ __launch_bounds__(256) void logit_grad_kept_kernel(const float* __restrict__ zk, int kept_cols, int Vc,
+                                                              int V, int N, const int32_t* __restrict__ n_dev,
                                                               const int32_t* __restrict__ act,
-                                                              const int32_t* __restrict__ fpos,
+                                                              const int32_t* __restrict__ afwd,
                                                               const int32_t* __restrict__ target,
                                                               const float* __restrict__ lse,
                                                               const float* __restrict__ delta,
                                                               uint16_t* __restrict__ dN, int64_t rN,
                                                               uint16_t* __restrict__ dT, int64_t rT) {
-  __shared__ uint16_t tile[32][64 + 8];   // padded rows: the column reads below hit distinct banks
+  __shared__ uint16_t tile[32][128 + 8];   // [token][entry]; padded rows: the column reads hit distinct banks
   const int n = min(N, *n_dev);
-  const int a0 = blockIdx.y * 32, v0 = blockIdx.x * 64;
+  const int a0 = blockIdx.y * 32, vb = blockIdx.x * (128 * kConvSeg);
   if (a0 >= n) return;
+  const int nseg = min(kConvSeg, (Vc - vb) / 128);   // Vc is a multiple of 128
   const int tid = threadIdx.x;
-  // in: column a0 + tid / 8, entries v0 + (tid % 8) * 8 .. +7
-  {
-    const int a = a0 + (tid >> 3), v = v0 + (tid & 7) * 8;
-    float dl = 0.f, ls = 0.f;
-    int tg = -1;
-    f32x4 z0 = {0.f, 0.f, 0.f, 0.f}, z1 = {0.f, 0.f, 0.f, 0.f};
-    if (a < n) {
-      const int t = act[a];
-      dl = delta[t];
-      ls = lse[t];
-      tg = target[t];
-      const int f = fpos[t], vt = v / kTileM;
-      const float* s = zk + ((int64_t)vt * kept_cols + (f >> 8)) * (kTileM * kTileN) +
-                       ((((v - vt * kTileM) >> 4) * kTileN + (f & (kTileN - 1))) * 16 + (v & 15));
-      z0 = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(s));
-      z1 = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(s + 4));
-    }
-    uint32_t x[8];
+  const int al = (tid & 127) >> 2, qt = tid & 3, a = a0 + al;
+  float dl = 0.f, ls = 0.f;
+  int tg = -1;
+  f32x4 z[kConvSeg][4];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const float z = e < 4 ? z0[e] : z1[e - 4];
-      float g = logit_grad(z, ls, dl, v + e == tg);
-      if (v + e >= V) g = 0.f;
-      x[e] = f32_to_bf16_bits(g);
+  for (int sg = 0; sg < kConvSeg; ++sg)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) z[sg][q] = f32x4{0.f, 0.f, 0.f, 0.f};
+  if (a < n) {
+    const int t = act[a], f = afwd[a];
+#pragma unroll
+    for (int sg = 0; sg < kConvSeg; ++sg) {
+      if (sg < nseg) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int v = vb + sg * 128 + (2 * q + (tid >> 7)) * 16, vt = v / kTileM;
+          const float* src = zk + ((int64_t)vt * kept_cols + (f >> 8)) * (kTileM * kTileN) +
+                             ((((v - vt * kTileM) >> 4) * kTileN + (f & (kTileN - 1))) * 16 + qt * 4);
+          z[sg][q] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(src));
+        }
+      }
     }
-    const u32x4 o = {x[0] | (x[1] << 16), x[2] | (x[3] << 16), x[4] | (x[5] << 16), x[6] | (x[7] << 16)};
-    *reinterpret_cast<u32x4*>(dN + ((int64_t)(v >> 5) * rN + a) * kTileK + (v & 31)) = o;
-    *reinterpret_cast<u32x4*>(&tile[tid >> 3][(tid & 7) * 8]) = o;
+    dl = delta[t];
+    ls = lse[t];
+    tg = target[t];
   }
-  __syncthreads();
-  // out: entry v0 + tid / 4 of columns a0 + (tid % 4) * 8 .. +7
-  {
-    const int vl = tid >> 2, ap = (tid & 3) * 8;
-    uint32_t w[4];
 #pragma unroll
-    for (int e = 0; e < 4; ++e) w[e] = (uint32_t)tile[ap + 2 * e][vl] | ((uint32_t)tile[ap + 2 * e + 1][vl] << 16);
-    const u32x4 o = {w[0], w[1], w[2], w[3]};
-    *reinterpret_cast<u32x4*>(dT + ((int64_t)(a0 >> 5) * rT + v0 + vl) * kTileK + ap) = o;
+  for (int sg = 0; sg < kConvSeg; ++sg) {
+    if (sg >= nseg) break;
+    const int v0 = vb + sg * 128;
+    if (sg > 0) __syncthreads();   // the previous segment's LDS reads are done
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int vl = (2 * q + (tid >> 7)) * 16 + qt * 4, v = v0 + vl;
+      uint32_t x[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        float g = logit_grad(z[sg][q][e], ls, dl, v + e == tg);
+        if (v + e >= V) g = 0.f;
+        x[e] = f32_to_bf16_bits(g);
+      }
+      *reinterpret_cast<uint2*>(&tile[al][vl]) = make_uint2(x[0] | (x[1] << 16), x[2] | (x[3] << 16));
+    }
+    __syncthreads();
+    // token-major: token a0 + tid / 8, entries v0 + (tid % 8) * 16 .. +15
+    {
+      const int tl = tid >> 3, vl = (tid & 7) * 16, v = v0 + vl;
+      uint16_t* pn = dN + ((int64_t)(v >> 5) * rN + a0 + tl) * kTileK + (v & 31);
+      *reinterpret_cast<u32x4*>(pn) = *reinterpret_cast<const u32x4*>(&tile[tl][vl]);
+      *reinterpret_cast<u32x4*>(pn + 8) = *reinterpret_cast<const u32x4*>(&tile[tl][vl + 8]);
+    }
+    // vocabulary-major: entry v0 + tid / 2 of tokens a0 + (tid % 2) * 16 .. +15
+    {
+      const int vl = tid >> 1, ap = (tid & 1) * 16;
+      uint32_t w[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        w[e] = (uint32_t)tile[ap + 2 * e][vl] | ((uint32_t)tile[ap + 2 * e + 1][vl] << 16);
+      uint16_t* pt = dT + ((int64_t)(a0 >> 5) * rT + v0 + vl) * kTileK + ap;
+      *reinterpret_cast<u32x4*>(pt) = u32x4{w[0], w[1], w[2], w[3]};
+      *reinterpret_cast<u32x4*>(pt + 8) = u32x4{w[4], w[5], w[6], w[7]};
+    }
   }
 }
 
@@ -497,8 +531,9 @@ constexpr int kCompactThreads = 256, kCompactPer = 8, kCompactSpan = kCompactThr
 // launches over blocks of kCompactSpan consecutive tokens: the first counts
 // each block's kept tokens; the second adds the counts of the blocks before
 // it and scatters: idx[0 .. count) are the kept indices in increasing order,
-// pos[t] (if pos is not NULL) is t's place in idx or -1; the last block writes
-// the count (and stats[4], if asked).
+// pos[t] (if pos is not NULL) is t's place in idx or -1, mapped[p] (if mapped
+// is not NULL) is map[idx[p]]; the last block writes the count (and stats[4],
+// if asked).
 template <class Keep>
 __global__ __launch_bounds__(kCompactThreads) void compact_count_kernel(int N, Keep keep, int32_t* __restrict__ cnt) {
   __shared__ int sh[kCompactThreads];
@@ -523,6 +558,8 @@ __global__ __launch_bounds__(kCompactThreads) void compact_scatter_kernel(int N,
                                                                           const int32_t* __restrict__ cnt,
                                                                           int32_t* __restrict__ idx,
                                                                           int32_t* __restrict__ pos,
+                                                                          const int32_t* __restrict__ map,
+                                                                          int32_t* __restrict__ mapped,
                                                                           int32_t* __restrict__ count,
                                                                           double* __restrict__ stats) {
   __shared__ int sh[kCompactThreads];
@@ -560,7 +597,10 @@ __global__ __launch_bounds__(kCompactThreads) void compact_scatter_kernel(int N,
   for (int e = 0; e < kCompactPer; ++e) {
     const int t = t0 + e;
     if (t < N) {
-      if (kept[e]) idx[p] = t;
+      if (kept[e]) {
+        idx[p] = t;
+        if (mapped) mapped[p] = map[t];
+      }
       if (pos) pos[t] = kept[e] ? p : -1;
     }
     p += kept[e] ? 1 : 0;
@@ -595,13 +635,13 @@ struct KeepActive {
 };
 
 template <class Keep>
-int launch_compact(int N, const Keep& keep, int32_t* cnt, int32_t* idx, int32_t* pos, int32_t* count, double* stats,
-                   hipStream_t stream) {
+int launch_compact(int N, const Keep& keep, int32_t* cnt, int32_t* idx, int32_t* pos, const int32_t* map,
+                   int32_t* mapped, int32_t* count, double* stats, hipStream_t stream) {
   const unsigned nblk = (unsigned)((N + kCompactSpan - 1) / kCompactSpan);
   hipLaunchKernelGGL(compact_count_kernel<Keep>, dim3(nblk), dim3(kCompactThreads), 0, stream, N, keep, cnt);
   PSPO_HIP_CHECK(hipGetLastError());
   hipLaunchKernelGGL(compact_scatter_kernel<Keep>, dim3(nblk), dim3(kCompactThreads), 0, stream, N, keep, cnt, idx,
-                     pos, count, stats);
+                     pos, map, mapped, count, stats);
   PSPO_HIP_CHECK(hipGetLastError());
   return PSPO_OK;
 }
@@ -744,7 +784,7 @@ __global__ __launch_bounds__(kFinThreads) void reduce_loss_kernel(int nblk, cons
 
 struct Plan {
   int64_t Npad, Vpad, dpad, Vc, ntv, nfin;
-  int64_t off_pm, off_pl, off_zt, off_lse, off_delta, off_fidx, off_fpos, off_nfwd, off_idx, off_nact, off_cnt, off_blk, off_wk,
+  int64_t off_pm, off_pl, off_zt, off_lse, off_delta, off_fidx, off_fpos, off_nfwd, off_idx, off_nact, off_afwd, off_cnt, off_blk, off_wk,
       off_hk, off_ht, off_wt, off_dn, off_dt, off_zk, total;
   bool keep;   // the forward keeps the first chunk's fp32 logits
 };
@@ -786,6 +826,7 @@ Plan make_plan(int64_t N, int64_t d, int64_t V, bool keep) {
   p.off_nfwd = take(4);
   p.off_idx = take(p.Npad * 4);
   p.off_nact = take(4);
+  p.off_afwd = take(p.Npad * 4);                                      // forward column of each backward token
   p.off_cnt = take((p.Npad + kCompactSpan - 1) / kCompactSpan * 4);   // per-block counts of a compaction
   p.off_blk = take((p.nfin > 0 ? p.nfin : 1) * 5 * 8);
   p.off_wk = take(d * p.Vpad * 2);                                    // W, K-blocked [d/32][Vpad][32]
@@ -880,6 +921,7 @@ int pspo_loss_fwd_bwd(const uint16_t* hidden, const uint16_t* w_head, const int3
   int32_t* act_idx = reinterpret_cast<int32_t*>(ws + pl.off_idx);
   int32_t* n_act = reinterpret_cast<int32_t*>(ws + pl.off_nact);
   int32_t* cnt = reinterpret_cast<int32_t*>(ws + pl.off_cnt);
+  int32_t* act_fwd = reinterpret_cast<int32_t*>(ws + pl.off_afwd);
   double* blk = reinterpret_cast<double*>(ws + pl.off_blk);
   uint16_t* wk = reinterpret_cast<uint16_t*>(ws + pl.off_wk);
   uint16_t* hk = reinterpret_cast<uint16_t*>(ws + pl.off_hk);
@@ -898,7 +940,7 @@ int pspo_loss_fwd_bwd(const uint16_t* hidden, const uint16_t* w_head, const int3
   // 1. the tokens whose logits are needed (all of them if logp_new is wanted);
   //    W and their hidden rows as K-blocked operands
   if (int rc = launch_compact(N, KeepForward{R, logp_new != nullptr ? 1 : 0, seq_id, advantage}, cnt, fwd_idx,
-                              fwd_pos, n_fwd, nullptr, stream))
+                              fwd_pos, nullptr, nullptr, n_fwd, nullptr, stream))
     return rc;
   // W K-blocked (forward and logit-gradient products) and, per vocabulary
   // chunk, W[chunk]^T (dH product), in one pass over W
@@ -926,7 +968,9 @@ int pspo_loss_fwd_bwd(const uint16_t* hidden, const uint16_t* w_head, const int3
   PSPO_HIP_CHECK(hipGetLastError());
   // 4. the backward runs over the tokens with delta != 0 only (every other
   //    token has a zero logit-gradient row: zero d_hidden row, no dW term)
-  if (int rc = launch_compact(N, KeepActive{delta}, cnt, act_idx, nullptr, n_act, stats, stream)) return rc;
+  // (with each backward token's forward column, where the kept logits sit)
+  if (int rc = launch_compact(N, KeepActive{delta}, cnt, act_idx, nullptr, fwd_pos, act_fwd, n_act, stats, stream))
+    return rc;
   hipLaunchKernelGGL(zero_inactive_rows_kernel, dim3((unsigned)N), dim3(256), 0, stream, d, delta, d_hidden);
   PSPO_HIP_CHECK(hipGetLastError());
   // 5. operands of the gradient products: the backward tokens' hidden rows
@@ -941,8 +985,10 @@ int pspo_loss_fwd_bwd(const uint16_t* hidden, const uint16_t* w_head, const int3
     const int64_t vc = (pl.Vpad - v0) < pl.Vc ? (pl.Vpad - v0) : pl.Vc;
     const int ctiles = (int)(vc / kTileM);
     if (v0 == 0 && zk != nullptr) {
-      hipLaunchKernelGGL(logit_grad_kept_kernel, dim3((unsigned)(pl.Vc / 64), (unsigned)(pl.Npad / 32)), dim3(256), 0,
-                         stream, zk, tiles_tok_n, V, N, n_act, act_idx, fwd_pos, target, lse, delta, dN, pl.Npad, dT,
+      hipLaunchKernelGGL(logit_grad_kept_kernel,
+                         dim3((unsigned)((pl.Vc + 128 * kConvSeg - 1) / (128 * kConvSeg)), (unsigned)(pl.Npad / 32)),
+                         dim3(256), 0, stream, zk, tiles_tok_n, (int)pl.Vc, V, N, n_act, act_idx, act_fwd, target, lse,
+                         delta, dN, pl.Npad, dT,
                          pl.Vc);
       PSPO_HIP_CHECK(hipGetLastError());
     } else {

@@ -10,26 +10,40 @@ namespace {
 
 constexpr int kProbeChains = 16;   // independent accumulators per wave: covers the MFMA latency
 
+// A bf16 in [-1, 1) from a 32-bit hash (random mantissa bits, like real operands).
+__device__ __forceinline__ __bf16 probe_value(uint32_t x) {
+  x ^= x >> 16;
+  x *= 0x7feb352du;
+  x ^= x >> 15;
+  x *= 0x846ca68bu;
+  x ^= x >> 16;
+  return (__bf16)((float)(int32_t)x * (1.0f / 2147483648.0f));
+}
+
 __global__ __launch_bounds__(256) void mfma_loop_kernel(int iters, float* __restrict__ out) {
-  const int tid = threadIdx.x;
-  bf16x8 a, b;
+  const uint32_t tid = blockIdx.x * 256u + threadIdx.x;
+  // two operand sets, alternated between consecutive MFMAs, so that the
+  // operand bits toggle as they do in the products (power follows the data)
+  bf16x8 a[2], b[2];
 #pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    a[e] = (__bf16)(0.001f * (float)((tid + e) & 15));
-    b[e] = (__bf16)(0.002f * (float)((tid * 3 + e) & 7));
-  }
+  for (int s = 0; s < 2; ++s)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      a[s][e] = probe_value(tid * 32u + s * 16u + e);
+      b[s][e] = probe_value(tid * 32u + s * 16u + 8u + e);
+    }
   f32x4 acc[kProbeChains];
 #pragma unroll
   for (int c = 0; c < kProbeChains; ++c) acc[c] = f32x4{0.f, 0.f, 0.f, 0.f};
   for (int i = 0; i < iters; ++i) {
 #pragma unroll
-    for (int c = 0; c < kProbeChains; ++c) mfma_vgpr(acc[c], a, b);
+    for (int c = 0; c < kProbeChains; ++c) mfma_vgpr(acc[c], a[c & 1], b[c & 1]);
   }
   mfma_drain();
   float s = 0.f;
 #pragma unroll
   for (int c = 0; c < kProbeChains; ++c) s += acc[c][0] + acc[c][1] + acc[c][2] + acc[c][3];
-  out[(int64_t)blockIdx.x * 256 + tid] = s;
+  out[(int64_t)blockIdx.x * 256 + threadIdx.x] = s;
 }
 
 }  // namespace
