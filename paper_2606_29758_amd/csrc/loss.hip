@@ -64,7 +64,7 @@ struct EpiForward {
   float* part_m;
   float* part_l;
   float* zt;
-  const int32_t* tok;    // column t is token tok[t] (columns t < *n_dev)
+  const int32_t* ftgt;   // target id of column t (columns t < *n_dev), in column order
   const int32_t* n_dev;
   float* zk;             // kept fp32 logits of vocabulary tiles tm < kept_tiles, or NULL:
   int kept_tiles;        //   per tile (tm, tn) a block at (tm * kept_cols + tn) * 384 * 256,
@@ -109,28 +109,19 @@ struct EpiForward {
     const int n = min(N, __builtin_amdgcn_readfirstlane(*n_dev));
     const int vbase = tm * kTileM + acc_row(wm, 0, 0, lane);   // this lane's rows: vbase + i*16 + r
     const bool full = (tm + 1) * kTileM <= V;                   // every row of the tile is a token id
-    // the targets of the lane's 8 columns, fetched together (two round trips, not 16)
+    // the targets of the lane's 8 columns: one load each, issued before the
+    // column loop (fenced so they are not sunk to their use) and used after it,
+    // so their latency hides behind the maxima and exponentials
     int tgts[kBlocksN];
 #pragma unroll
     for (int j = 0; j < kBlocksN; ++j) {
       const int t = tn * kTileN + acc_col(wn, j, lane);
-      tgts[j] = t < n ? tok[t] : -1;
+      tgts[j] = t < n ? ftgt[t] : -1;
     }
-#pragma unroll
-    for (int j = 0; j < kBlocksN; ++j) asm volatile("" ::"v"(tgts[j]));   // keep the batch: no sinking
-#pragma unroll
-    for (int j = 0; j < kBlocksN; ++j) tgts[j] = tgts[j] >= 0 ? target[tgts[j]] : -1;
-#pragma unroll
-    for (int j = 0; j < kBlocksN; ++j) asm volatile("" ::"v"(tgts[j]));
-    // the target logits are stored after the column loop: a conditional store
-    // inside it makes the compiler keep far more accumulator copies live
-    float zvs[kBlocksN];
-    bool has[kBlocksN];
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int j = 0; j < kBlocksN; ++j) {
       const int cl = acc_col(wn, j, lane);
-      const int tgt = tgts[j];
-      has[j] = acc_pick(acc, j, tgt - vbase, zvs[j]);
       float m = kNegInf;
 #pragma unroll
       for (int i = 0; i < kBlocksM; ++i)
@@ -154,6 +145,13 @@ struct EpiForward {
         red[(wm * kTileN + cl) * 2 + 1] = l;
       }
     }
+    // the target logits (each picked by the one lane whose rows hold it),
+    // stored after the picks: a conditional store among them makes the
+    // compiler keep far more accumulator copies live
+    float zvs[kBlocksN];
+    bool has[kBlocksN];
+#pragma unroll
+    for (int j = 0; j < kBlocksN; ++j) has[j] = acc_pick(acc, j, tgts[j] - vbase, zvs[j]);
 #pragma unroll
     for (int j = 0; j < kBlocksN; ++j)
       if (has[j]) zt[tn * kTileN + acc_col(wn, j, lane)] = zvs[j];
@@ -217,14 +215,13 @@ __device__ __forceinline__ u32x2 quad_transpose(u32x2 p, int k) {
 //     away (DPP row shift) between the two column blocks gives it 8.
 struct EpiDelta {
   int V, N, v0;
-  const int32_t* target;
-  const float* lse;
-  const float* delta;
   uint16_t* dT;          // K-blocked [Npad/32][rT][32]: rows = vocabulary entries of the chunk, K = tokens
   int64_t rT;
   uint16_t* dN;          // K-blocked [Vc/32][rN][32]: rows = tokens, K = vocabulary entries of the chunk
   int64_t rN;
-  const int32_t* tok;    // column t of the tile is token tok[t] (columns t < *n_dev)
+  const int32_t* ctgt;   // target, lse and delta of column t (columns t < *n_dev), in column order
+  const float* clse;
+  const float* cdelta;
   const int32_t* n_dev;
 
   __device__ __forceinline__ void apply(AccTile& acc, int tm, int tn, int wm, int wn, int lane, float*) const {
@@ -232,21 +229,17 @@ struct EpiDelta {
     const int vl0 = tm * kTileM + acc_row(wm, 0, 0, lane);   // chunk rows of this lane: vl0 + i*16 + r
     const int vbase = v0 + vl0;
     const bool full = v0 + (tm + 1) * kTileM <= V;            // every row of the tile is a token id
-    // per-column token data of the lane's 8 columns, fetched together
-    int tos[kBlocksN];
+    // per-column token data of the lane's 8 columns, fetched together (one
+    // round trip: the arrays are in column order)
     float dls[kBlocksN], lss[kBlocksN];
     int tgs[kBlocksN];
 #pragma unroll
     for (int j = 0; j < kBlocksN; ++j) {
       const int t = tn * kTileN + acc_col(wn, j, lane);
-      tos[j] = t < n ? tok[t] : -1;
-    }
-#pragma unroll
-    for (int j = 0; j < kBlocksN; ++j) {
-      const bool tv = tos[j] >= 0;
-      dls[j] = tv ? delta[tos[j]] : 0.f;
-      lss[j] = tv ? lse[tos[j]] : 0.f;
-      tgs[j] = tv ? target[tos[j]] : -1;
+      const bool tv = t < n;
+      dls[j] = tv ? cdelta[t] : 0.f;
+      lss[j] = tv ? clse[t] : 0.f;
+      tgs[j] = tv ? ctgt[t] : -1;
     }
     // Store addresses: a per-tile base (uniform) plus a 32-bit byte offset per
     // lane and block group (a tile spans 12 K blocks of the token-major layout
@@ -338,7 +331,8 @@ struct EpiDelta {
 // (tm * kept_cols + tn) * 384 * 256, [24 blocks of 16 rows][256 columns][16])
 // instead of a recomputing product: the values and layouts the
 // logit-gradient epilogue writes for that chunk.  Backward column a < n =
-// min(N, *n_dev) is token act[a], whose logits sit in forward column afwd[a];
+// min(N, *n_dev) has the target, lse and delta ctgt[a], clse[a], cdelta[a] and
+// its logits sit in forward column afwd[a];
 // columns n <= a < round_up(n, 32) are written as the zero gradient of a
 // padding column (the dW product reads whole 32-token K steps); rows v >= V
 // are zero.
@@ -356,11 +350,10 @@ constexpr int kConvSeg = 1;
 
 __global__ __launch_bounds__(256) void logit_grad_kept_kernel(const float* __restrict__ zk, int kept_cols, int Vc,
                                                               int V, int N, const int32_t* __restrict__ n_dev,
-                                                              const int32_t* __restrict__ act,
                                                               const int32_t* __restrict__ afwd,
-                                                              const int32_t* __restrict__ target,
-                                                              const float* __restrict__ lse,
-                                                              const float* __restrict__ delta,
+                                                              const int32_t* __restrict__ ctgt,
+                                                              const float* __restrict__ clse,
+                                                              const float* __restrict__ cdelta,
                                                               uint16_t* __restrict__ dN, int64_t rN,
                                                               uint16_t* __restrict__ dT, int64_t rT) {
   __shared__ uint16_t tile[32][128 + 8];   // [token][entry]; padded rows: the column reads hit distinct banks
@@ -378,7 +371,7 @@ __global__ __launch_bounds__(256) void logit_grad_kept_kernel(const float* __res
 #pragma unroll
     for (int q = 0; q < 4; ++q) z[sg][q] = f32x4{0.f, 0.f, 0.f, 0.f};
   if (a < n) {
-    const int t = act[a], f = afwd[a];
+    const int f = afwd[a];
 #pragma unroll
     for (int sg = 0; sg < kConvSeg; ++sg) {
       if (sg < nseg) {
@@ -391,9 +384,9 @@ __global__ __launch_bounds__(256) void logit_grad_kept_kernel(const float* __res
         }
       }
     }
-    dl = delta[t];
-    ls = lse[t];
-    tg = target[t];
+    dl = cdelta[a];
+    ls = clse[a];
+    tg = ctgt[a];
   }
 #pragma unroll
   for (int sg = 0; sg < kConvSeg; ++sg) {
@@ -777,6 +770,27 @@ __global__ __launch_bounds__(kFinThreads) void reduce_loss_kernel(int nblk, cons
   }
 }
 
+// Per backward column a < min(N, *n_dev) (token act[a]): its forward column
+// (where the kept logits sit), target, lse and delta, in column order, so the
+// backward kernels fetch a column's data in one contiguous round trip.
+__global__ __launch_bounds__(256) void gather_backward_kernel(int N, const int32_t* __restrict__ n_dev,
+                                                              const int32_t* __restrict__ act,
+                                                              const int32_t* __restrict__ fpos,
+                                                              const int32_t* __restrict__ target,
+                                                              const float* __restrict__ lse,
+                                                              const float* __restrict__ delta,
+                                                              int32_t* __restrict__ afwd, int32_t* __restrict__ ctgt,
+                                                              float* __restrict__ clse, float* __restrict__ cdelta) {
+  const int n = min(N, *n_dev);
+  for (int a = blockIdx.x * 256 + threadIdx.x; a < n; a += gridDim.x * 256) {
+    const int t = act[a];
+    afwd[a] = fpos[t];
+    ctgt[a] = target[t];
+    clse[a] = lse[t];
+    cdelta[a] = delta[t];
+  }
+}
+
 // ---------------------------------------------------------------------------
 // Workspace plan
 // ---------------------------------------------------------------------------
@@ -784,7 +798,7 @@ __global__ __launch_bounds__(kFinThreads) void reduce_loss_kernel(int nblk, cons
 
 struct Plan {
   int64_t Npad, Vpad, dpad, Vc, ntv, nfin;
-  int64_t off_pm, off_pl, off_zt, off_lse, off_delta, off_fidx, off_fpos, off_nfwd, off_idx, off_nact, off_afwd, off_cnt, off_blk, off_wk,
+  int64_t off_pm, off_pl, off_zt, off_lse, off_delta, off_fidx, off_fpos, off_nfwd, off_idx, off_nact, off_afwd, off_ctgt, off_clse, off_cdelta, off_ftgt, off_cnt, off_blk, off_wk,
       off_hk, off_ht, off_wt, off_dn, off_dt, off_zk, total;
   bool keep;   // the forward keeps the first chunk's fp32 logits
 };
@@ -826,7 +840,11 @@ Plan make_plan(int64_t N, int64_t d, int64_t V, bool keep) {
   p.off_nfwd = take(4);
   p.off_idx = take(p.Npad * 4);
   p.off_nact = take(4);
-  p.off_afwd = take(p.Npad * 4);                                      // forward column of each backward token
+  p.off_afwd = take(p.Npad * 4);                                      // backward columns: forward column,
+  p.off_ctgt = take(p.Npad * 4);                                      //   target, lse, delta
+  p.off_clse = take(p.Npad * 4);
+  p.off_cdelta = take(p.Npad * 4);
+  p.off_ftgt = take(p.Npad * 4);                                      // forward columns: target
   p.off_cnt = take((p.Npad + kCompactSpan - 1) / kCompactSpan * 4);   // per-block counts of a compaction
   p.off_blk = take((p.nfin > 0 ? p.nfin : 1) * 5 * 8);
   p.off_wk = take(d * p.Vpad * 2);                                    // W, K-blocked [d/32][Vpad][32]
@@ -922,6 +940,10 @@ int pspo_loss_fwd_bwd(const uint16_t* hidden, const uint16_t* w_head, const int3
   int32_t* n_act = reinterpret_cast<int32_t*>(ws + pl.off_nact);
   int32_t* cnt = reinterpret_cast<int32_t*>(ws + pl.off_cnt);
   int32_t* act_fwd = reinterpret_cast<int32_t*>(ws + pl.off_afwd);
+  int32_t* act_tgt = reinterpret_cast<int32_t*>(ws + pl.off_ctgt);
+  float* act_lse = reinterpret_cast<float*>(ws + pl.off_clse);
+  float* act_delta = reinterpret_cast<float*>(ws + pl.off_cdelta);
+  int32_t* fwd_tgt = reinterpret_cast<int32_t*>(ws + pl.off_ftgt);
   double* blk = reinterpret_cast<double*>(ws + pl.off_blk);
   uint16_t* wk = reinterpret_cast<uint16_t*>(ws + pl.off_wk);
   uint16_t* hk = reinterpret_cast<uint16_t*>(ws + pl.off_hk);
@@ -940,7 +962,7 @@ int pspo_loss_fwd_bwd(const uint16_t* hidden, const uint16_t* w_head, const int3
   // 1. the tokens whose logits are needed (all of them if logp_new is wanted);
   //    W and their hidden rows as K-blocked operands
   if (int rc = launch_compact(N, KeepForward{R, logp_new != nullptr ? 1 : 0, seq_id, advantage}, cnt, fwd_idx,
-                              fwd_pos, nullptr, nullptr, n_fwd, nullptr, stream))
+                              fwd_pos, target, fwd_tgt, n_fwd, nullptr, stream))
     return rc;
   // W K-blocked (forward and logit-gradient products) and, per vocabulary
   // chunk, W[chunk]^T (dH product), in one pass over W
@@ -955,7 +977,7 @@ int pspo_loss_fwd_bwd(const uint16_t* hidden, const uint16_t* w_head, const int3
     // the kept tiles' stores spread over the XCDs
     GemmShape g{wk, pl.Vpad, V, hk, pl.Npad, N, d, tiles_voc, tiles_tok_n, n_fwd, kDynN,
                 zk != nullptr ? (int)(pl.Vc / kTileM) : 0};
-    EpiForward e{V, N, pl.Npad, target, part_m, part_l, zt, fwd_idx, n_fwd, zk, (int)(pl.Vc / kTileM), tiles_tok_n};
+    EpiForward e{V, N, pl.Npad, target, part_m, part_l, zt, fwd_tgt, n_fwd, zk, (int)(pl.Vc / kTileM), tiles_tok_n};
     if (int rc = launch_gemm(g, e, stream)) return rc;
   }
   // 3. lse, PPO terms, delta, loss
@@ -968,9 +990,11 @@ int pspo_loss_fwd_bwd(const uint16_t* hidden, const uint16_t* w_head, const int3
   PSPO_HIP_CHECK(hipGetLastError());
   // 4. the backward runs over the tokens with delta != 0 only (every other
   //    token has a zero logit-gradient row: zero d_hidden row, no dW term)
-  // (with each backward token's forward column, where the kept logits sit)
-  if (int rc = launch_compact(N, KeepActive{delta}, cnt, act_idx, nullptr, fwd_pos, act_fwd, n_act, stats, stream))
+  if (int rc = launch_compact(N, KeepActive{delta}, cnt, act_idx, nullptr, nullptr, nullptr, n_act, stats, stream))
     return rc;
+  hipLaunchKernelGGL(gather_backward_kernel, dim3((unsigned)((pl.Npad + 255) / 256)), dim3(256), 0, stream, N, n_act,
+                     act_idx, fwd_pos, target, lse, delta, act_fwd, act_tgt, act_lse, act_delta);
+  PSPO_HIP_CHECK(hipGetLastError());
   hipLaunchKernelGGL(zero_inactive_rows_kernel, dim3((unsigned)N), dim3(256), 0, stream, d, delta, d_hidden);
   PSPO_HIP_CHECK(hipGetLastError());
   // 5. operands of the gradient products: the backward tokens' hidden rows
@@ -987,13 +1011,13 @@ int pspo_loss_fwd_bwd(const uint16_t* hidden, const uint16_t* w_head, const int3
     if (v0 == 0 && zk != nullptr) {
       hipLaunchKernelGGL(logit_grad_kept_kernel,
                          dim3((unsigned)((pl.Vc + 128 * kConvSeg - 1) / (128 * kConvSeg)), (unsigned)(pl.Npad / 32)),
-                         dim3(256), 0, stream, zk, tiles_tok_n, (int)pl.Vc, V, N, n_act, act_idx, act_fwd, target, lse,
-                         delta, dN, pl.Npad, dT,
+                         dim3(256), 0, stream, zk, tiles_tok_n, (int)pl.Vc, V, N, n_act, act_fwd, act_tgt, act_lse,
+                         act_delta, dN, pl.Npad, dT,
                          pl.Vc);
       PSPO_HIP_CHECK(hipGetLastError());
     } else {
       GemmShape g{wk + v0 * kTileK, pl.Vpad, (int)(V - v0), hk, pl.Npad, N, d, ctiles, tiles_tok_n, n_act, kDynN};
-      EpiDelta e{V, N, (int)v0, target, lse, delta, dT, pl.Vc, dN, pl.Npad, act_idx, n_act};
+      EpiDelta e{V, N, (int)v0, dT, pl.Vc, dN, pl.Npad, act_tgt, act_lse, act_delta, n_act};
       if (int rc = launch_gemm(g, e, stream)) return rc;
     }
     {
