@@ -43,6 +43,17 @@ constexpr float kNegInf = -INFINITY;
 // Epilogues
 // ---------------------------------------------------------------------------
 
+constexpr float kLog2e = 1.4426950408889634f;
+
+// max(a, b, c) in one instruction (v_max3_f32, IEEE maxNum semantics: a NaN
+// operand is ignored, as with fmaxf); written as asm because the compiler's
+// fmaxf on values of unknown origin first canonicalises each operand.
+__device__ __forceinline__ float max3(float a, float b, float c) {
+  float r;
+  asm("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+  return r;
+}
+
 // One entry of the logit gradient, delta (1[v = o] - exp(z - lse)) (the
 // objective of Sec. 3.1 differentiated through the log-softmax of App. D).
 // exp(min(z - lse, 0)) equals exp(z - lse) for every real entry (lse bounds
@@ -57,10 +68,15 @@ __device__ __forceinline__ float logit_grad(float z, float lse, float delta, boo
 // needed (B = their hidden rows, gathered; column t is token tok[t]); writes
 // per-column softmax partials of each 384-row vocabulary tile and the target
 // logit.
+// kFull: every row of every tile is a token id (no per-row mask); otherwise
+// the launch is the partial last vocabulary tile, tm0 its index (the product's
+// row tile 0).  Two instantiations rather than a branch in one: with a branch
+// the compiler spills accumulators.
+template <bool kFull>
 struct EpiForward {
   int V, N;
   int64_t ldp;  // stride between vocabulary tiles in the partial arrays (= Npad)
-  const int32_t* target;
+  int tm0;
   float* part_m;
   float* part_l;
   float* zt;
@@ -70,8 +86,10 @@ struct EpiForward {
   int kept_tiles;        //   per tile (tm, tn) a block at (tm * kept_cols + tn) * 384 * 256,
   int kept_cols;         //   [24 blocks of 16 rows][256 columns][16]
 
-  __device__ __forceinline__ void apply(const AccTile& acc, int tm, int tn, int wm, int wn, int lane, float* smem) const {
+  __device__ __forceinline__ void apply(const AccTile& acc, int tm_launch, int tn, int wm, int wn, int lane,
+                                        float* smem) const {
     float* red = smem;  // [2 wave rows][256 columns][m, l]
+    const int tm = kFull ? tm_launch : tm0 + tm_launch;
     if (zk != nullptr && tm < kept_tiles) {
       // the tile's fp32 logits, kept for the first backward chunk, as one
       // contiguous 384 x 256 block (few address translations per tile):
@@ -108,7 +126,6 @@ struct EpiForward {
     __builtin_amdgcn_sched_barrier(0);
     const int n = min(N, __builtin_amdgcn_readfirstlane(*n_dev));
     const int vbase = tm * kTileM + acc_row(wm, 0, 0, lane);   // this lane's rows: vbase + i*16 + r
-    const bool full = (tm + 1) * kTileM <= V;                   // every row of the tile is a token id
     // the targets of the lane's 8 columns: one load each, issued before the
     // column loop (fenced so they are not sunk to their use) and used after it,
     // so their latency hides behind the maxima and exponentials
@@ -122,21 +139,45 @@ struct EpiForward {
 #pragma unroll
     for (int j = 0; j < kBlocksN; ++j) {
       const int cl = acc_col(wn, j, lane);
-      float m = kNegInf;
+      // value q = 4 i + r of the lane's column (row vbase + 16 i + r)
+      auto x = [&](int q) { return acc_get(acc, q >> 2, j, q & 3); };
+      float m, l;
+      if constexpr (kFull) {
+        // every row is a token id: three-input maxima (no per-value select),
+        // exp2(z log2e - m log2e) as one fma + exp, four partial sums
+        float mm[4];
 #pragma unroll
-      for (int i = 0; i < kBlocksM; ++i)
+        for (int k = 0; k < 4; ++k) mm[k] = max3(x(k), x(k + 4), x(k + 8));
 #pragma unroll
-        for (int r = 0; r < kAccPerBlock; ++r)
-          if (full || vbase + i * 16 + r < V) m = fmaxf(m, acc_get(acc, i, j, r));
-      m = fmaxf(m, __shfl_xor(m, 16));
-      m = fmaxf(m, __shfl_xor(m, 32));
-      float l = 0.f;
-      if (m != kNegInf) {
+        for (int q = 12; q < kBlocksM * kAccPerBlock; q += 8)
+#pragma unroll
+          for (int k = 0; k < 4; ++k) mm[k] = max3(mm[k], x(q + k), x(q + k + 4));
+        m = max3(mm[0], mm[1], max3(mm[2], mm[3], mm[3]));
+        m = fmaxf(m, __shfl_xor(m, 16));
+        m = fmaxf(m, __shfl_xor(m, 32));
+        const float mb = m * kLog2e;
+        float ls[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int q = 0; q < kBlocksM * kAccPerBlock; ++q) ls[q & 3] += __builtin_amdgcn_exp2f(fmaf(x(q), kLog2e, -mb));
+        l = (ls[0] + ls[1]) + (ls[2] + ls[3]);
+      } else {
+        m = kNegInf;
 #pragma unroll
         for (int i = 0; i < kBlocksM; ++i)
 #pragma unroll
           for (int r = 0; r < kAccPerBlock; ++r)
-            if (full || vbase + i * 16 + r < V) l += __expf(acc_get(acc, i, j, r) - m);
+            if (vbase + i * 16 + r < V) m = fmaxf(m, x(i * kAccPerBlock + r));
+        m = fmaxf(m, __shfl_xor(m, 16));
+        m = fmaxf(m, __shfl_xor(m, 32));
+        l = 0.f;
+        if (m != kNegInf) {
+          const float mb = m * kLog2e;
+#pragma unroll
+          for (int i = 0; i < kBlocksM; ++i)
+#pragma unroll
+            for (int r = 0; r < kAccPerBlock; ++r)
+              if (vbase + i * 16 + r < V) l += __builtin_amdgcn_exp2f(fmaf(x(i * kAccPerBlock + r), kLog2e, -mb));
+        }
       }
       l += __shfl_xor(l, 16);
       l += __shfl_xor(l, 32);
@@ -972,13 +1013,23 @@ int pspo_loss_fwd_bwd(const uint16_t* hidden, const uint16_t* w_head, const int3
   hipLaunchKernelGGL(kblock_rows_kernel, dim3(ctiles64, (unsigned)(pl.Npad / 32)), dim3(256), 0, stream, hidden,
                      (int64_t)d, N, fwd_idx, n_fwd, hk, pl.Npad, nullptr, (int64_t)0, (int64_t)kTileK);
   PSPO_HIP_CHECK(hipGetLastError());
-  // 2. forward logits -> per-tile softmax partials and target logits
+  // 2. forward logits -> per-tile softmax partials and target logits: the
+  //    vocabulary tiles whose rows are all token ids, then a partial last one
   {
-    // the kept tiles' stores spread over the XCDs
-    GemmShape g{wk, pl.Vpad, V, hk, pl.Npad, N, d, tiles_voc, tiles_tok_n, n_fwd, kDynN,
-                zk != nullptr ? (int)(pl.Vc / kTileM) : 0};
-    EpiForward e{V, N, pl.Npad, target, part_m, part_l, zt, fwd_tgt, n_fwd, zk, (int)(pl.Vc / kTileM), tiles_tok_n};
-    if (int rc = launch_gemm(g, e, stream)) return rc;
+    const int tiles_full = V / kTileM, kept_tiles = zk != nullptr ? (int)(pl.Vc / kTileM) : 0;
+    if (tiles_full > 0) {
+      // the kept tiles' stores spread over the XCDs
+      GemmShape g{wk, pl.Vpad, tiles_full * kTileM, hk, pl.Npad, N, d, tiles_full, tiles_tok_n, n_fwd, kDynN,
+                  kept_tiles < tiles_full ? kept_tiles : tiles_full};
+      EpiForward<true> e{V, N, pl.Npad, 0, part_m, part_l, zt, fwd_tgt, n_fwd, zk, kept_tiles, tiles_tok_n};
+      if (int rc = launch_gemm(g, e, stream)) return rc;
+    }
+    if (tiles_full < tiles_voc) {
+      GemmShape g{wk + (int64_t)tiles_full * kTileM * kTileK, pl.Vpad, V - tiles_full * kTileM, hk, pl.Npad, N, d, 1,
+                  tiles_tok_n, n_fwd, kDynN};
+      EpiForward<false> e{V, N, pl.Npad, tiles_full, part_m, part_l, zt, fwd_tgt, n_fwd, zk, kept_tiles, tiles_tok_n};
+      if (int rc = launch_gemm(g, e, stream)) return rc;
+    }
   }
   // 3. lse, PPO terms, delta, loss
   hipLaunchKernelGGL(finalize_kernel, dim3((unsigned)pl.nfin), dim3(kFinThreads), 0, stream, N, V, R, tiles_voc,
