@@ -55,13 +55,19 @@ __device__ __forceinline__ float max3(float a, float b, float c) {
 }
 
 // One entry of the logit gradient, delta (1[v = o] - exp(z - lse)) (the
-// objective of Sec. 3.1 differentiated through the log-softmax of App. D).
-// exp(min(z - lse, 0)) equals exp(z - lse) for every real entry (lse bounds
-// each logit) and stays finite for padding columns, whose delta is 0.  The
-// recomputing product and the kept-logit conversion both use it, so they
-// produce the same bits.
-__device__ __forceinline__ float logit_grad(float z, float lse, float delta, bool is_target) {
-  return delta * ((is_target ? 1.f : 0.f) - __expf(fminf(z - lse, 0.f)));
+// objective of Sec. 3.1 differentiated through the log-softmax of App. D),
+// with lsb = lse log2(e): p = exp2(min(z log2(e) - lsb, 0)) (one fma; the min
+// keeps p <= 1 and finite for padding columns, whose delta is 0), then
+// delta [v = o] - delta p as one fma.  The recomputing product and the
+// kept-logit conversion both use it, so they produce the same bits.
+__device__ __forceinline__ float logit_grad(float z, float lsb, float delta, bool is_target) {
+  const float p = __builtin_amdgcn_exp2f(fminf(fmaf(z, kLog2e, -lsb), 0.f));
+  return fmaf(-delta, p, is_target ? delta : 0.f);
+}
+
+// Two floats as packed bf16 (round to nearest even): one v_cvt_pk_bf16_f32.
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{lo, hi}, bf16x2));
 }
 
 // Forward: rows = vocabulary (A = W), columns = the tokens whose logits are
@@ -233,11 +239,15 @@ __device__ __forceinline__ u32x2 quad_transpose(u32x2 p, int k) {
   const bool lo2 = k < 2;
   const uint32_t r1 = quad_xor2(lo2 ? p.y : p.x);
   const uint32_t qa = lo2 ? p.x : r1, qb = lo2 ? r1 : p.y;   // tokens k%2 and k%2+2, rows 2(k/2), +1
+  // 16-bit halves picked by lane parity with v_perm_b32 (byte selectors 0-3
+  // take bytes of the second operand, 4-7 of the first): one instruction per
+  // word instead of a select between two shift/mask pairs, which the compiler
+  // turns into a divergent branch
   const bool even = (k & 1) == 0;
-  const uint32_t r2 = quad_xor1(even ? ((qa >> 16) | (qb & 0xFFFF0000u)) : ((qa & 0xFFFFu) | (qb << 16)));
+  const uint32_t r2 = quad_xor1(__builtin_amdgcn_perm(qb, qa, even ? 0x07060302u : 0x05040100u));
   u32x2 o;
-  o.x = even ? ((qa & 0xFFFFu) | (r2 << 16)) : ((r2 & 0xFFFFu) | (qa & 0xFFFF0000u));
-  o.y = even ? ((qb & 0xFFFFu) | (r2 & 0xFFFF0000u)) : ((r2 >> 16) | (qb & 0xFFFF0000u));
+  o.x = __builtin_amdgcn_perm(r2, qa, even ? 0x05040100u : 0x03020504u);
+  o.y = __builtin_amdgcn_perm(r2, qb, even ? 0x07060100u : 0x03020706u);
   return o;
 }
 
@@ -279,7 +289,7 @@ struct EpiDelta {
       const int t = tn * kTileN + acc_col(wn, j, lane);
       const bool tv = t < n;
       dls[j] = tv ? cdelta[t] : 0.f;
-      lss[j] = tv ? clse[t] : 0.f;
+      lss[j] = tv ? clse[t] * kLog2e : 0.f;   // lse log2(e)
       tgs[j] = tv ? ctgt[t] : -1;
     }
     // Store addresses: a per-tile base (uniform) plus a 32-bit byte offset per
@@ -315,16 +325,15 @@ struct EpiDelta {
 #pragma unroll
           for (int jj = 0; jj < 2; ++jj) {
             const int i = 2 * ip + ii, j = 2 * jp + jj;
-            uint32_t x[kAccPerBlock];
+            float x[kAccPerBlock];
 #pragma unroll
             for (int r = 0; r < kAccPerBlock; ++r) {
               const int v = vbase + i * 16 + r;
-              float dv = logit_grad(acc_get(acc, i, j, r), lss[j], dls[j], v == tgs[j]);
-              if (!full) dv = (v < V) ? dv : 0.f;
-              x[r] = f32_to_bf16_bits(dv);
+              x[r] = logit_grad(acc_get(acc, i, j, r), lss[j], dls[j], v == tgs[j]);
+              if (!full) x[r] = (v < V) ? x[r] : 0.f;
             }
-            blk[ii][jj].x = x[0] | (x[1] << 16);
-            blk[ii][jj].y = x[2] | (x[3] << 16);
+            blk[ii][jj].x = pack_bf16x2(x[0], x[1]);
+            blk[ii][jj].y = pack_bf16x2(x[2], x[3]);
           }
         // token-major stores, one per column block
 #pragma unroll
@@ -426,7 +435,7 @@ __global__ __launch_bounds__(256) void logit_grad_kept_kernel(const float* __res
       }
     }
     dl = cdelta[a];
-    ls = clse[a];
+    ls = clse[a] * kLog2e;   // lse log2(e), as the recomputing epilogue takes it
     tg = ctgt[a];
   }
 #pragma unroll
@@ -437,14 +446,13 @@ __global__ __launch_bounds__(256) void logit_grad_kept_kernel(const float* __res
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const int vl = (2 * q + (tid >> 7)) * 16 + qt * 4, v = v0 + vl;
-      uint32_t x[4];
+      float x[4];
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        float g = logit_grad(z[sg][q][e], ls, dl, v + e == tg);
-        if (v + e >= V) g = 0.f;
-        x[e] = f32_to_bf16_bits(g);
+        x[e] = logit_grad(z[sg][q][e], ls, dl, v + e == tg);
+        if (v + e >= V) x[e] = 0.f;
       }
-      *reinterpret_cast<uint2*>(&tile[al][vl]) = make_uint2(x[0] | (x[1] << 16), x[2] | (x[3] << 16));
+      *reinterpret_cast<uint2*>(&tile[al][vl]) = make_uint2(pack_bf16x2(x[0], x[1]), pack_bf16x2(x[2], x[3]));
     }
     __syncthreads();
     // token-major: token a0 + tid / 8, entries v0 + (tid % 8) * 16 .. +15
