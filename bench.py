@@ -75,6 +75,10 @@ def parse():
     ap.add_argument("--no-full-control", action="store_true",
                     help="skip the full-trajectory control on the same batch: its timing (every xi = 1) "
                          "and the reseed check")
+    ap.add_argument("--no-recompute-control", action="store_true",
+                    help="skip the timing of the same calls with PSPO_RECOMPUTE_LOGITS (profiling runs)")
+    ap.add_argument("--no-mfma-peak", action="store_true",
+                    help="skip the matrix-core rate probe (profiling runs)")
     ap.add_argument("--reseeds", type=int, default=64,
                     help="cutoff draws averaged by the reseed check (after the timed steps; 0 skips it): "
                          "their mean update against the full-trajectory one")
@@ -309,17 +313,19 @@ def main():
 
     # the same loss calls with every logit tile recomputed in the backward
     # (PSPO_RECOMPUTE_LOGITS: no logits stored at all, a smaller workspace)
-    step.loss(pk, N, flags=pspo.PSPO_RECOMPUTE_LOGITS, want_logp=False)
-    torch.cuda.synchronize()
-    rs, re_ = ev(), ev()
-    nrep = max(3, args.steps // 2)
-    rs.record(stream)
-    for _ in range(nrep):
+    recompute_ms = None
+    if not args.no_recompute_control:
         step.loss(pk, N, flags=pspo.PSPO_RECOMPUTE_LOGITS, want_logp=False)
-    re_.record(stream)
-    torch.cuda.synchronize()
-    recompute_ms = rs.elapsed_time(re_) / nrep
-    mfma_peak = mfma_loop_peak()
+        torch.cuda.synchronize()
+        rs, re_ = ev(), ev()
+        nrep = max(3, args.steps // 2)
+        rs.record(stream)
+        for _ in range(nrep):
+            step.loss(pk, N, flags=pspo.PSPO_RECOMPUTE_LOGITS, want_logp=False)
+        re_.record(stream)
+        torch.cuda.synchronize()
+        recompute_ms = rs.elapsed_time(re_) / nrep
+    mfma_peak = None if args.no_mfma_peak else mfma_loop_peak()
 
     # the full-trajectory control on the same batch (every xi = 1: the standard, untruncated
     # update): its loss-call time against the truncated one
@@ -416,14 +422,16 @@ def main():
             "frac": achieved / PEAK_BF16_TFLOPS,
             "traffic": traffic,
         },
-        "recompute_logits_control": {
+    }
+    if recompute_ms is not None:
+        result["recompute_logits_control"] = {
             "loss_call_ms": recompute_ms,
             "pct_bf16_peak": 100.0 * flops / (recompute_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
             "what": "the same calls with PSPO_RECOMPUTE_LOGITS: every logit tile recomputed in the "
                     "backward, no logits stored",
-        },
-        "mfma_loop_peak": mfma_peak,
-    }
+        }
+    if mfma_peak is not None:
+        result["mfma_loop_peak"] = mfma_peak
     if full is not None:
         result["full_trajectory_control"] = dict(full, prefix_vs_full_ratio=loss_avg / full["loss_call_ms"])
     if reseed is not None:

@@ -135,6 +135,17 @@ __device__ __forceinline__ bool acc_pick(const AccTile& acc, int j, int rel, flo
   return has;
 }
 
+constexpr float kLog2e = 1.4426950408889634f;
+
+// max(a, b, c) in one instruction (v_max3_f32, IEEE maxNum semantics: a NaN
+// operand is ignored, as with fmaxf); written as asm because the compiler's
+// fmaxf on values of unknown origin first canonicalises each operand.
+__device__ __forceinline__ float max3(float a, float b, float c) {
+  float r;
+  asm("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+  return r;
+}
+
 __device__ __forceinline__ int chunk_swizzle(int row) { return ((row >> 1) ^ (row >> 2)) & 3; }
 
 // Tile of work-group blockIdx.x among the tiles_m x tiles_n tiles that cover

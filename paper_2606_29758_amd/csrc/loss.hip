@@ -43,17 +43,6 @@ constexpr float kNegInf = -INFINITY;
 // Epilogues
 // ---------------------------------------------------------------------------
 
-constexpr float kLog2e = 1.4426950408889634f;
-
-// max(a, b, c) in one instruction (v_max3_f32, IEEE maxNum semantics: a NaN
-// operand is ignored, as with fmaxf); written as asm because the compiler's
-// fmaxf on values of unknown origin first canonicalises each operand.
-__device__ __forceinline__ float max3(float a, float b, float c) {
-  float r;
-  asm("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
-  return r;
-}
-
 // One entry of the logit gradient, delta (1[v = o] - exp(z - lse)) (the
 // objective of Sec. 3.1 differentiated through the log-softmax of App. D),
 // with lsb = lse log2(e): p = exp2(min(z log2(e) - lsb, 0)) (one fma; the min

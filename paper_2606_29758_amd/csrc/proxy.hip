@@ -33,19 +33,29 @@ constexpr float kNegInf = -INFINITY;
 // rows = vocabulary (A = W), columns = tokens (B = H).  Writes, per column and
 // 384-row vocabulary tile, (m, S1, S2) over the tile's rows other than the
 // column's target, and the target logit.
+// kFull: every row of every tile is a token id (no per-row mask); otherwise
+// the launch is the partial last vocabulary tile, tm0 its index.  Two
+// instantiations rather than a branch in one: with a branch the compiler
+// spills accumulators.
+template <bool kFull>
 struct EpiProxy {
   int V, N;
   int64_t ldp;  // stride between vocabulary tiles in the partial arrays (= Npad)
+  int tm0;
   const int32_t* target;
   float* part_m;
   float* part_s1;
   float* part_s2;
   float* zt;
 
-  __device__ __forceinline__ void apply(const AccTile& acc, int tm, int tn, int wm, int wn, int lane, float* smem) const {
+  __device__ __forceinline__ void apply(const AccTile& acc, int tm_launch, int tn, int wm, int wn, int,
+                                        float* smem) const {
     float* red = smem;  // [2 wave rows][256 columns][m, S1, S2]
+    // the lane index, recomputed here: otherwise the compiler keeps values
+    // derived from the kernel's copy live across the product loop and spills one
+    const int lane = (int)__builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u));
+    const int tm = kFull ? tm_launch : tm0 + tm_launch;
     const int vbase = tm * kTileM + acc_row(wm, 0, 0, lane);   // this lane's rows: vbase + i*16 + r
-    const bool full = (tm + 1) * kTileM <= V;                   // every row of the tile is a token id
     // the targets of the lane's 8 columns, fetched together
     int tgts[kBlocksN];
 #pragma unroll
@@ -64,26 +74,57 @@ struct EpiProxy {
       const int cl = acc_col(wn, j, lane);
       const int tgt = tgts[j];
       has[j] = acc_pick(acc, j, tgt - vbase, zvs[j]);
-      float m = kNegInf;
+      // value q = 4 i + r of the lane's column (row vbase + 16 i + r)
+      auto x = [&](int q) { return acc_get(acc, q >> 2, j, q & 3); };
+      float m, s1, s2;
+      if constexpr (kFull) {
+        // every row is a token id: three-input maxima, exp2(z log2e - m log2e)
+        // as one fma + exp, the target's own entry selected away, four
+        // partial sums of each kind
+        float mm[4];
 #pragma unroll
-      for (int i = 0; i < kBlocksM; ++i)
+        for (int k = 0; k < 4; ++k) mm[k] = max3(x(k), x(k + 4), x(k + 8));
 #pragma unroll
-        for (int r = 0; r < kAccPerBlock; ++r)
-          if (full || vbase + i * 16 + r < V) m = fmaxf(m, acc_get(acc, i, j, r));
-      m = fmaxf(m, __shfl_xor(m, 16));
-      m = fmaxf(m, __shfl_xor(m, 32));
-      float s1 = 0.f, s2 = 0.f;
-      if (m != kNegInf) {
+        for (int q = 12; q < kBlocksM * kAccPerBlock; q += 8)
+#pragma unroll
+          for (int k = 0; k < 4; ++k) mm[k] = max3(mm[k], x(q + k), x(q + k + 4));
+        m = max3(mm[0], mm[1], max3(mm[2], mm[3], mm[3]));
+        m = fmaxf(m, __shfl_xor(m, 16));
+        m = fmaxf(m, __shfl_xor(m, 32));
+        const float mb = m * kLog2e;
+        float a1[4] = {0.f, 0.f, 0.f, 0.f}, a2[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int q = 0; q < kBlocksM * kAccPerBlock; ++q) {
+          float e = __builtin_amdgcn_exp2f(fmaf(x(q), kLog2e, -mb));
+          e = vbase + (q >> 2) * 16 + (q & 3) != tgt ? e : 0.f;
+          a1[q & 3] += e;
+          a2[q & 3] = fmaf(e, e, a2[q & 3]);
+        }
+        s1 = (a1[0] + a1[1]) + (a1[2] + a1[3]);
+        s2 = (a2[0] + a2[1]) + (a2[2] + a2[3]);
+      } else {
+        m = kNegInf;
 #pragma unroll
         for (int i = 0; i < kBlocksM; ++i)
 #pragma unroll
-          for (int r = 0; r < kAccPerBlock; ++r) {
-            const int v = vbase + i * 16 + r;
-            // the target's own entry is left out (selected away, not subtracted)
-            const float e = ((full || v < V) && v != tgt) ? __expf(acc_get(acc, i, j, r) - m) : 0.f;
-            s1 += e;
-            s2 += e * e;
-          }
+          for (int r = 0; r < kAccPerBlock; ++r)
+            if (vbase + i * 16 + r < V) m = fmaxf(m, acc_get(acc, i, j, r));
+        m = fmaxf(m, __shfl_xor(m, 16));
+        m = fmaxf(m, __shfl_xor(m, 32));
+        s1 = 0.f;
+        s2 = 0.f;
+        if (m != kNegInf) {
+#pragma unroll
+          for (int i = 0; i < kBlocksM; ++i)
+#pragma unroll
+            for (int r = 0; r < kAccPerBlock; ++r) {
+              const int v = vbase + i * 16 + r;
+              // the target's own entry is left out (selected away, not subtracted)
+              const float e = (v < V && v != tgt) ? __expf(acc_get(acc, i, j, r) - m) : 0.f;
+              s1 += e;
+              s2 += e * e;
+            }
+        }
       }
       s1 += __shfl_xor(s1, 16);
       s1 += __shfl_xor(s1, 32);
@@ -260,11 +301,23 @@ int pspo_score_proxy(const uint16_t* hidden, const uint16_t* w_head, const int32
                      (int64_t)d, N, nullptr, nullptr, hk, pl.Npad, nullptr, (int64_t)0, (int64_t)kTileK);
   PSPO_HIP_CHECK(hipGetLastError());
   {
-    GemmShape g{wk, pl.Vpad, V, hk, pl.Npad, N, d, tiles_voc, tiles_tok};
-    EpiProxy e{V, N, pl.Npad, target, part_m, part_s1, part_s2, zt};
-    hipLaunchKernelGGL(gemm_nt_kernel<EpiProxy>, dim3(gemm_grid(tiles_voc, tiles_tok)), dim3(kGemmThreads), 0,
-                       stream, g, e);
-    PSPO_HIP_CHECK(hipGetLastError());
+    // the vocabulary tiles whose rows are all token ids, then a partial last one
+    const int tiles_full = V / kTileM;
+    if (tiles_full > 0) {
+      GemmShape g{wk, pl.Vpad, tiles_full * kTileM, hk, pl.Npad, N, d, tiles_full, tiles_tok};
+      EpiProxy<true> e{V, N, pl.Npad, 0, target, part_m, part_s1, part_s2, zt};
+      hipLaunchKernelGGL(gemm_nt_kernel<EpiProxy<true>>, dim3(gemm_grid(tiles_full, tiles_tok)), dim3(kGemmThreads),
+                         0, stream, g, e);
+      PSPO_HIP_CHECK(hipGetLastError());
+    }
+    if (tiles_full < tiles_voc) {
+      GemmShape g{wk + (int64_t)tiles_full * kTileM * kTileK, pl.Vpad, V - tiles_full * kTileM, hk, pl.Npad, N, d, 1,
+                  tiles_tok};
+      EpiProxy<false> e{V, N, pl.Npad, tiles_full, target, part_m, part_s1, part_s2, zt};
+      hipLaunchKernelGGL(gemm_nt_kernel<EpiProxy<false>>, dim3(gemm_grid(1, tiles_tok)), dim3(kGemmThreads), 0,
+                         stream, g, e);
+      PSPO_HIP_CHECK(hipGetLastError());
+    }
   }
   hipLaunchKernelGGL(row_sqnorm_kernel, dim3((unsigned)((N + 3) / 4)), dim3(256), 0, stream, hidden, N, d, hn);
   PSPO_HIP_CHECK(hipGetLastError());
