@@ -174,25 +174,54 @@ __global__ __launch_bounds__(64) void design_cutoffs_kernel(const double* __rest
     }
     return;
   }
-  // Pooling Adjacent Violators: a stack of blocks (start, length, summed weight)
+  // Pooling Adjacent Violators: a stack of blocks (start, length, summed
+  // weight); a new element pools with the block below it while that block's
+  // score sqrt(W / L) is below its own.  The top block and its score stay in
+  // registers (the memory stack holds the blocks under it), so an element
+  // that does not pool costs no memory round trip; every comparison and sum
+  // is the same expression as with the whole stack in memory.
   int32_t* st = bstart + a;
   int32_t* ln = blen + a;
   double* wv = bval + a;
-  int M = 0;
-  for (int t = 0; t < T; ++t) {
+  int M = 0;                       // blocks under the top
+  int ts = 0, tl = 1;              // the top block
+  double tw = wp[0];
+  double tsc = sqrt(tw / (double)tl);
+  for (int t = 1; t < T; ++t) {
     int s0 = t, L = 1;
     double W = wp[t];
-    while (M > 0 && sqrt(wv[M - 1] / (double)ln[M - 1]) < sqrt(W / (double)L)) {
-      --M;
-      s0 = st[M];
-      L += ln[M];
-      W = wv[M] + W;
+    double sc = sqrt(W / (double)L);
+    bool top = true;
+    while (top && tsc < sc) {      // pool the top into the new block
+      s0 = ts;
+      L += tl;
+      W = tw + W;
+      sc = sqrt(W / (double)L);
+      if (M > 0) {
+        --M;
+        ts = st[M];
+        tl = ln[M];
+        tw = wv[M];
+        tsc = sqrt(tw / (double)tl);
+      } else {
+        top = false;
+      }
     }
-    st[M] = s0;
-    ln[M] = L;
-    wv[M] = W;
-    ++M;
+    if (top) {                     // the old top goes under the new block
+      st[M] = ts;
+      ln[M] = tl;
+      wv[M] = tw;
+      ++M;
+    }
+    ts = s0;
+    tl = L;
+    tw = W;
+    tsc = sc;
   }
+  st[M] = ts;
+  ln[M] = tl;
+  wv[M] = tw;
+  ++M;
   // scores, then suffix sums of L_m s_m (accumulated from the last block)
   for (int m = 0; m < M; ++m) wv[m] = sqrt(wv[m] / (double)ln[m]);
   // first unsaturated block: kappa(m) = (B - sum_{j<m} L_j) / sum_{j>=m} L_j s_j, kappa(m) s_m <= 1
