@@ -28,6 +28,12 @@ MINI = {
     # tiles in every dimension and ragged tails (V = 151936 is not a multiple of 256)
     "mini7b": synth.custom("mini7b", "qwen7b", P=2, K=2, length_law=("uniform", 150, 420), data_seed=31),
     "mini1p5b": synth.custom("mini1p5b", "qwen1.5b", P=2, K=3, length_law=("uniform", 60, 300), data_seed=21),
+    # odd shapes: a vocabulary that is no multiple of 32 (2.6 tiles of 384, one chunk) with a width
+    # of 6 K steps, and one of three chunks whose last ends in a partial tile (7B width)
+    "odd_small": synth.custom("odd_small", "tiny", d=192, V=1000, P=2, K=3, length_law=("uniform", 20, 90),
+                              data_seed=41),
+    "odd_chunks": synth.custom("odd_chunks", "qwen7b", V=100003, P=2, K=3, length_law=("uniform", 60, 160),
+                               data_seed=49),
 }
 _CACHE = {}
 
@@ -113,7 +119,7 @@ def _compare_loss(out, ref):
 
 
 @pytest.mark.parametrize("name,seed", [("tiny", 0), ("tiny", 1), ("tiny", 123456789), ("tiny_full", 0),
-                                       ("mini1p5b", 0), ("mini7b", 3)])
+                                       ("mini1p5b", 0), ("mini7b", 3), ("odd_small", 0), ("odd_chunks", 2)])
 def test_loss_parity(name, seed):
     wl, lp = _workload(name)
     cfg = wl.cfg
@@ -185,7 +191,7 @@ def test_without_logp_is_identical(name):
     assert rel_l2(_to_np(b["d_w_head"]), ref["d_w"]) <= GRAD_REL_L2
 
 
-@pytest.mark.parametrize("name", ["tiny", "mini7b", "mini1p5b"])
+@pytest.mark.parametrize("name", ["tiny", "mini7b", "mini1p5b", "odd_small", "odd_chunks"])
 @pytest.mark.parametrize("want_logp", [True, False])
 def test_kept_logits_match_recompute(name, want_logp):
     """The forward keeps the first vocabulary chunk's fp32 logits and the backward turns
