@@ -146,6 +146,39 @@ __device__ __forceinline__ float max3(float a, float b, float c) {
   return r;
 }
 
+// The 384 x 256 fp32 tile of the accumulators as one contiguous block at
+// `base`: [24 blocks of 16 rows][256 columns][16].  An accumulator block is 16
+// rows x 16 columns and the lane's 4 rows of it one 16-byte piece, so each
+// store instruction writes 1 KB of whole 128-byte lines (a store of half lines
+// makes the L2 fetch the other half from memory); non-temporal stores.  AGPR
+// blocks are read by explicit v_accvgpr_read: taken as one 4-register value,
+// the compiler keeps a VGPR copy of the block live from the loop's end and
+// spills accumulators to make room.
+__device__ __forceinline__ void store_tile_rows16(const AccTile& acc, float* base, int wm, int wn, int lane) {
+  unsigned char* zb = reinterpret_cast<unsigned char*>(base);
+  const uint32_t lo = (uint32_t)(wm * (kWaveM / 16)) * (kTileN * 64u) + (uint32_t)(wn * kWaveN + (lane & 15)) * 64u +
+                      (uint32_t)(lane >> 4) * 16u;
+#pragma unroll
+  for (int i = 0; i < kBlocksM; ++i) {
+#pragma unroll
+    for (int j = 0; j < kBlocksN; ++j) {
+      f32x4 b;
+      if (i < kBlocksAgpr) {
+#pragma unroll
+        for (int r = 0; r < kAccPerBlock; ++r) {
+          float x;
+          asm volatile("v_accvgpr_read_b32 %0, %1" : "=v"(x) : "a"(acc.a[i][j][r]));
+          b[r] = x;
+        }
+      } else {
+        b = acc.v[i - kBlocksAgpr][j];
+      }
+      __builtin_nontemporal_store(b, reinterpret_cast<f32x4*>(zb + (lo + (uint32_t)(i * kTileN * 64 + j * 1024))));
+    }
+    __builtin_amdgcn_sched_barrier(0);   // one row block's stores at a time
+  }
+}
+
 __device__ __forceinline__ int chunk_swizzle(int row) { return ((row >> 1) ^ (row >> 2)) & 3; }
 
 // Tile of work-group blockIdx.x among the tiles_m x tiles_n tiles that cover
@@ -162,23 +195,109 @@ __device__ __forceinline__ int spread_row_tile(int l, int s, int T) {
   return c > cp ? c - 1 : s + l - c;
 }
 
-__device__ __forceinline__ bool map_tile(int tiles_m, int tiles_n, int M, int N, int& tm, int& tn,
-                                         int spread_m = 0) {
-  tiles_m = min(tiles_m, (M + kTileM - 1) / kTileM);
-  tiles_n = min(tiles_n, (N + kTileN - 1) / kTileN);
-  const int total = tiles_m * tiles_n;
-  const int per_xcd = (total + kNumXcd - 1) / kNumXcd;
-  const int bid = blockIdx.x;
-  if (bid / kNumXcd >= per_xcd) return false;
-  const int t = (bid % kNumXcd) * per_xcd + bid / kNumXcd;
-  if (t >= total) return false;
-  const int width = kGroupM * tiles_n;
+// M, N, K of a product after its device-side bound.
+__device__ __forceinline__ void bounded_dims(const GemmShape& g, int& M, int& N, int& K) {
+  M = g.M;
+  N = g.N;
+  K = g.K;
+  if (g.dyn != nullptr) {
+    const int v = max(__builtin_amdgcn_readfirstlane(*g.dyn), 0);
+    if (g.dyn_dim == kDynM) M = min(M, v);
+    else if (g.dyn_dim == kDynN) N = min(N, v);
+    else if (g.dyn_dim == kDynK) K = min(K, (v + kTileK - 1) / kTileK * kTileK);
+  }
+}
+
+// The tiles of a product bounded to M x N (tiles_m/n: the launch's extents);
+// each XCD runs the contiguous run of per_xcd positions of the grouped order
+// that starts at its index times per_xcd.
+struct TileGrid {
+  int tiles_m, tiles_n, total, per_xcd;
+};
+__device__ __forceinline__ TileGrid tile_grid(int tiles_m, int tiles_n, int M, int N) {
+  TileGrid tg;
+  tg.tiles_m = min(tiles_m, (M + kTileM - 1) / kTileM);
+  tg.tiles_n = min(tiles_n, (N + kTileN - 1) / kTileN);
+  tg.total = tg.tiles_m * tg.tiles_n;
+  tg.per_xcd = (tg.total + kNumXcd - 1) / kNumXcd;
+  return tg;
+}
+// Tile (tm, tn) at position t of the grouped order (kGroupM row tiles x all
+// column tiles per group).
+__device__ __forceinline__ void tile_at(const TileGrid& tg, int t, int spread_m, int& tm, int& tn) {
+  const int width = kGroupM * tg.tiles_n;
   const int first = (t / width) * kGroupM;
-  const int gsize = min(tiles_m - first, kGroupM);
+  const int gsize = min(tg.tiles_m - first, kGroupM);
   const int rem = t % width;
   tm = first + rem % gsize;
   tn = rem / gsize;
-  if (spread_m > 0) tm = spread_row_tile(tm, min(spread_m, tiles_m), tiles_m);
+  if (spread_m > 0) tm = spread_row_tile(tm, min(spread_m, tg.tiles_m), tg.tiles_m);
+}
+
+// How a launch covers the tiles.  A run of per_xcd positions on an XCD's 32
+// CUs that is no multiple of 32 ends in a partial round of whole tiles; a
+// product with long tiles can instead run its whole rounds in one launch and
+// the rest, split along K, in a second one whose parts fill the CUs.
+enum : int {
+  kLaunchWhole = 0,    // every position
+  kLaunchRounds = 1,   // each XCD's first 32 floor(per_xcd / 32) positions
+  kLaunchTail = 2,     // the rest, each tile in K parts (map_tail)
+};
+constexpr int kTailSlots = 64;   // work-groups per XCD of a tail launch (two rounds)
+
+__device__ __forceinline__ bool map_tile(int tiles_m, int tiles_n, int M, int N, int& tm, int& tn,
+                                         int spread_m = 0, bool rounds_only = false) {
+  const TileGrid tg = tile_grid(tiles_m, tiles_n, M, N);
+  const int bid = blockIdx.x, k = bid / kNumXcd;
+  if (k >= tg.per_xcd) return false;
+  if (rounds_only && k >= tg.per_xcd / 32 * 32) return false;
+  const int t = (bid % kNumXcd) * tg.per_xcd + k;
+  if (t >= tg.total) return false;
+  tile_at(tg, t, spread_m, tm, tn);
+  return true;
+}
+
+// K parts of each tail tile of an XCD with r tail tiles and nk K steps: the
+// S <= min(64 / r, nk) with the fewest rounds per part, ceil(r S / 32) / S
+// (the smaller S on ties).
+__device__ __forceinline__ int tail_parts(int r, int nk) {
+  int best = 1, best_rounds = (r + 31) / 32;
+  for (int s = 2; s * r <= kTailSlots && s <= nk; ++s) {
+    const int rounds = (r * s + 31) / 32;
+    if (rounds * best < best_rounds * s) {
+      best = s;
+      best_rounds = rounds;
+    }
+  }
+  return best;
+}
+
+// Epilogue of a tail launch: the part's accumulators to slab `blockIdx.x`.
+struct EpiSlab {
+  float* slab;
+  __device__ __forceinline__ void apply(const AccTile& acc, int, int, int wm, int wn, int lane, float*) const {
+    store_tile_rows16(acc, slab + (int64_t)blockIdx.x * (kTileM * kTileN), wm, wn, lane);
+  }
+};
+
+// Tail launch: work-group x + 8 k (x the XCD, k < 64) takes part k % S of the
+// XCD's tail tile k / S, K steps [part nk / S, (part + 1) nk / S).  The tail
+// tiles are the positions after the XCD's whole rounds.  Returns false for
+// work-groups without a part.
+__device__ __forceinline__ bool map_tail(const TileGrid& tg, int bid, int nk, int& tm, int& tn, int& kb, int& ke,
+                                         int* u_out = nullptr, int* parts_out = nullptr) {
+  const int x = bid % kNumXcd, k = bid / kNumXcd;
+  const int full = tg.per_xcd / 32 * 32;
+  const int r = min(tg.per_xcd, tg.total - x * tg.per_xcd) - full;
+  if (r <= 0 || k >= kTailSlots) return false;
+  const int parts = tail_parts(r, nk);
+  const int u = k / parts, part = k % parts;
+  if (u >= r) return false;
+  tile_at(tg, x * tg.per_xcd + full + u, 0, tm, tn);
+  kb = part * nk / parts;
+  ke = (part + 1) * nk / parts;
+  if (u_out) *u_out = u;
+  if (parts_out) *parts_out = parts;
   return true;
 }
 
@@ -238,20 +357,21 @@ __device__ __forceinline__ void stage_barrier() {
 // overwritten); smem is the (no longer needed) LDS ring, 160 KB, free for
 // reductions: every load into it has landed and all waves have passed a
 // barrier before the call.
-template <class Epi>
+template <class Epi, int kLaunch = kLaunchWhole>
 __global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_per_eu(1, 1)))
 void gemm_nt_kernel(GemmShape g, Epi epi) {
   __shared__ __attribute__((aligned(1024))) unsigned char lds[kLdsBytes];
 
-  int M = g.M, N = g.N, K = g.K;
-  if (g.dyn != nullptr) {
-    const int v = max(__builtin_amdgcn_readfirstlane(*g.dyn), 0);
-    if (g.dyn_dim == kDynM) M = min(M, v);
-    else if (g.dyn_dim == kDynN) N = min(N, v);
-    else if (g.dyn_dim == kDynK) K = min(K, (v + kTileK - 1) / kTileK * kTileK);
+  int M, N, K;
+  bounded_dims(g, M, N, K);
+  int tm, tn, kb = 0, nk = K / kTileK;
+  if constexpr (kLaunch == kLaunchTail) {
+    int ke;
+    if (!map_tail(tile_grid(g.tiles_m, g.tiles_n, M, N), blockIdx.x, nk, tm, tn, kb, ke)) return;
+    nk = ke - kb;
+  } else {
+    if (!map_tile(g.tiles_m, g.tiles_n, M, N, tm, tn, g.spread_m, kLaunch == kLaunchRounds)) return;
   }
-  int tm, tn;
-  if (!map_tile(g.tiles_m, g.tiles_n, M, N, tm, tn, g.spread_m)) return;
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -263,11 +383,11 @@ void gemm_nt_kernel(GemmShape g, Epi epi) {
   // logical chunk (l % 4) ^ swizzle(row) of that row's 64-byte K slice.  Wave w
   // loads A rows w*96 + q*16 (q < 6) and B rows w*64 + q*16 (q < 4).
   const uint32_t lane_off = (uint32_t)((lane >> 2) * kLdsRow + (((lane & 3) ^ chunk_swizzle(lane >> 2)) << 4));
-  const unsigned char* gA =
-      reinterpret_cast<const unsigned char*>(g.A) + ((int64_t)tm * kTileM + wave * (kTileM / 4)) * kLdsRow;
-  const unsigned char* gB =
-      reinterpret_cast<const unsigned char*>(g.B) + ((int64_t)tn * kTileN + wave * (kTileN / 4)) * kLdsRow;
   const int64_t kstep_a = g.rows_a * kLdsRow, kstep_b = g.rows_b * kLdsRow;   // bytes per K step
+  const unsigned char* gA = reinterpret_cast<const unsigned char*>(g.A) +
+                            ((int64_t)tm * kTileM + wave * (kTileM / 4)) * kLdsRow + (int64_t)kb * kstep_a;
+  const unsigned char* gB = reinterpret_cast<const unsigned char*>(g.B) +
+                            ((int64_t)tn * kTileN + wave * (kTileN / 4)) * kLdsRow + (int64_t)kb * kstep_b;
 
   // MFMA operand reads: block i of A is rows wm*192 + i*16 + lane%16, K chunk
   // lane/16 (8 bf16 of the 32-deep step).  The swizzle of row r + 16 i equals
@@ -286,7 +406,6 @@ void gemm_nt_kernel(GemmShape g, Epi epi) {
 #pragma unroll
     for (int j = 0; j < kBlocksN; ++j) acc.v[i][j] = f32x4{};
 
-  const int nk = K / kTileK;
 
   auto read_a = [&](int stage, int i) -> bf16x8 {
     return __builtin_bit_cast(bf16x8,

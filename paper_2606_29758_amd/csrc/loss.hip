@@ -85,39 +85,8 @@ struct EpiForward {
                                         float* smem) const {
     float* red = smem;  // [2 wave rows][256 columns][m, l]
     const int tm = kFull ? tm_launch : tm0 + tm_launch;
-    if (zk != nullptr && tm < kept_tiles) {
-      // the tile's fp32 logits, kept for the first backward chunk, as one
-      // contiguous 384 x 256 block (few address translations per tile):
-      // [24 blocks of 16 vocabulary rows][256 columns][16].  An accumulator
-      // block is 16 rows x 16 columns, the lane's 4 rows one 16-byte piece:
-      // each store instruction writes 1 KB of whole 128-byte lines (a store
-      // of half lines makes the L2 fetch the other half from memory)
-      unsigned char* zb = reinterpret_cast<unsigned char*>(zk + ((int64_t)tm * kept_cols + tn) * (kTileM * kTileN));
-      const uint32_t lo = (uint32_t)(wm * (kWaveM / 16)) * (kTileN * 64u) +
-                          (uint32_t)(wn * kWaveN + (lane & 15)) * 64u + (uint32_t)(lane >> 4) * 16u;
-#pragma unroll
-      for (int i = 0; i < kBlocksM; ++i) {
-#pragma unroll
-        for (int j = 0; j < kBlocksN; ++j) {
-          // AGPR blocks are read by explicit v_accvgpr_read: taken as one
-          // 4-register value, the compiler keeps a VGPR copy of the block
-          // live from the loop's end and spills accumulators to make room
-          f32x4 b;
-          if (i < kBlocksAgpr) {
-#pragma unroll
-            for (int r = 0; r < kAccPerBlock; ++r) {
-              float x;
-              asm volatile("v_accvgpr_read_b32 %0, %1" : "=v"(x) : "a"(acc.a[i][j][r]));
-              b[r] = x;
-            }
-          } else {
-            b = acc.v[i - kBlocksAgpr][j];
-          }
-          __builtin_nontemporal_store(b, reinterpret_cast<f32x4*>(zb + (lo + (uint32_t)(i * kTileN * 64 + j * 1024))));
-        }
-        __builtin_amdgcn_sched_barrier(0);   // one row block's stores at a time
-      }
-    }
+    if (zk != nullptr && tm < kept_tiles)   // the tile's fp32 logits, kept for the first backward chunk
+      store_tile_rows16(acc, zk + ((int64_t)tm * kept_cols + tn) * (kTileM * kTileN), wm, wn, lane);
     __builtin_amdgcn_sched_barrier(0);
     const int n = min(N, __builtin_amdgcn_readfirstlane(*n_dev));
     const int vbase = tm * kTileM + acc_row(wm, 0, 0, lane);   // this lane's rows: vbase + i*16 + r
@@ -808,6 +777,75 @@ __global__ __launch_bounds__(kFinThreads) void reduce_loss_kernel(int nblk, cons
   }
 }
 
+// The tail tiles of a product launched as whole rounds plus a K-split tail
+// (gemm_nt_kernel with kLaunchRounds, then kLaunchTail + EpiSlab): each tail
+// tile's K parts are summed in order from the slabs of its work-groups
+// x + 8 (u S + p) and handed to `out` row by row, 16 values at a time.
+// Grid (24 blocks of 16 rows, 8 XCDs x 32 tail tiles), 256 threads.
+template <class Out>
+__global__ __launch_bounds__(256) void tail_reduce_kernel(GemmShape g, const float* __restrict__ slab, Out out) {
+  __shared__ float rows[16][kTileN + 4];
+  int M, N, K;
+  bounded_dims(g, M, N, K);
+  const TileGrid tg = tile_grid(g.tiles_m, g.tiles_n, M, N);
+  const int x = blockIdx.y % kNumXcd, u = blockIdx.y / kNumXcd;
+  const int full = tg.per_xcd / 32 * 32;
+  const int r = min(tg.per_xcd, tg.total - x * tg.per_xcd) - full;
+  if (u >= r) return;
+  const int parts = tail_parts(r, K / kTileK);
+  int tm, tn;
+  tile_at(tg, x * tg.per_xcd + full + u, 0, tm, tn);
+  const int rb = blockIdx.x, tid = threadIdx.x;
+  // the slab layout [24 blocks of 16 rows][256 columns][16]: column tid of row
+  // block rb is 16 consecutive floats
+  f32x4 sum[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) sum[q] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int p = 0; p < parts; ++p) {
+    const f32x4* src = reinterpret_cast<const f32x4*>(slab + (int64_t)(x + kNumXcd * (u * parts + p)) * (kTileM * kTileN) +
+                                                      rb * (16 * kTileN) + tid * 16);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) sum[q] += __builtin_nontemporal_load(src + q);
+  }
+#pragma unroll
+  for (int q = 0; q < 4; ++q)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) rows[q * 4 + e][tid] = sum[q][e];
+  __syncthreads();
+  const int lr = tid >> 4, c0 = (tid & 15) * 16;
+  out(tm * kTileM + rb * 16 + lr, tn * kTileN + c0, &rows[lr][c0]);
+}
+
+// dW rows v0 + row (< V), as EpiDW writes them: (accumulate ? old : 0) + sum.
+struct TailDW {
+  int V, d, v0;
+  float* dW;
+  bool accumulate;
+  __device__ __forceinline__ void operator()(int row, int col0, const float* v) const {
+    if (v0 + row >= V) return;
+    float* o = dW + (int64_t)(v0 + row) * d;
+#pragma unroll
+    for (int e = 0; e < 16; ++e)
+      if (col0 + e < d) o[col0 + e] = (accumulate ? o[col0 + e] : 0.f) + v[e];
+  }
+};
+
+// d_hidden row tok[row] (row < n), as EpiDH writes it: (first ? 0 : old) + sum.
+struct TailDH {
+  int N, d;
+  float* dH;
+  bool first;
+  const int32_t* tok;
+  const int32_t* n_dev;
+  __device__ __forceinline__ void operator()(int row, int col0, const float* v) const {
+    if (row >= min(N, *n_dev)) return;
+    float* o = dH + (int64_t)tok[row] * d;
+#pragma unroll
+    for (int e = 0; e < 16; ++e)
+      if (col0 + e < d) o[col0 + e] = (first ? 0.f : o[col0 + e]) + v[e];
+  }
+};
+
 // Per backward column a < min(N, *n_dev) (token act[a]): its forward column
 // (where the kept logits sit), target, lse and delta, in column order, so the
 // backward kernels fetch a column's data in one contiguous round trip.
@@ -837,7 +875,7 @@ __global__ __launch_bounds__(256) void gather_backward_kernel(int N, const int32
 struct Plan {
   int64_t Npad, Vpad, dpad, Vc, ntv, nfin;
   int64_t off_pm, off_pl, off_zt, off_lse, off_delta, off_fidx, off_fpos, off_nfwd, off_idx, off_nact, off_afwd, off_ctgt, off_clse, off_cdelta, off_ftgt, off_cnt, off_blk, off_wk,
-      off_hk, off_ht, off_wt, off_dn, off_dt, off_zk, total;
+      off_hk, off_ht, off_wt, off_dn, off_dt, off_slab, off_zk, total;
   bool keep;   // the forward keeps the first chunk's fp32 logits
 };
 
@@ -891,6 +929,7 @@ Plan make_plan(int64_t N, int64_t d, int64_t V, bool keep) {
   p.off_wt = take(p.dpad * ((p.Vpad + p.Vc - 1) / p.Vc) * p.Vc * 2);  // per chunk: W^T [Vc/32][dpad][32]
   p.off_dn = take(p.Npad * p.Vc * 2);                                 // K-blocked [Vc/32][Npad][32]
   p.off_dt = take(p.Vc * p.Npad * 2);                                 // K-blocked [Npad/32][Vc][32]
+  p.off_slab = take((int64_t)kNumXcd * kTailSlots * kTileM * kTileN * 4);   // K parts of tail tiles
   p.keep = keep;
   p.off_zk = take(keep ? p.Vc * p.Npad * 4 : 0);                      // kept fp32 logits, one block per forward tile
   p.total = o;
@@ -901,6 +940,23 @@ template <class Epi>
 int launch_gemm(const GemmShape& g, const Epi& epi, hipStream_t stream) {
   hipLaunchKernelGGL(gemm_nt_kernel<Epi>, dim3(gemm_grid(g.tiles_m, g.tiles_n)), dim3(kGemmThreads), 0, stream, g,
                      epi);
+  PSPO_HIP_CHECK(hipGetLastError());
+  return PSPO_OK;
+}
+
+// A product with long tiles as whole rounds (epilogue `epi`), then the
+// remaining tiles split along K into slabs, then their sums (written by `out`
+// as `epi` would write them): the CUs stay busy through the last round.
+template <class Epi, class Out>
+int launch_gemm_split_tail(const GemmShape& g, const Epi& epi, const Out& out, float* slab, hipStream_t stream) {
+  hipLaunchKernelGGL((gemm_nt_kernel<Epi, kLaunchRounds>), dim3(gemm_grid(g.tiles_m, g.tiles_n)), dim3(kGemmThreads),
+                     0, stream, g, epi);
+  PSPO_HIP_CHECK(hipGetLastError());
+  hipLaunchKernelGGL((gemm_nt_kernel<EpiSlab, kLaunchTail>), dim3(kNumXcd * kTailSlots), dim3(kGemmThreads), 0,
+                     stream, g, EpiSlab{slab});
+  PSPO_HIP_CHECK(hipGetLastError());
+  hipLaunchKernelGGL(tail_reduce_kernel<Out>, dim3(kTileM / 16, kNumXcd * 32), dim3(256), 0, stream, g,
+                     (const float*)slab, out);
   PSPO_HIP_CHECK(hipGetLastError());
   return PSPO_OK;
 }
@@ -990,6 +1046,7 @@ int pspo_loss_fwd_bwd(const uint16_t* hidden, const uint16_t* w_head, const int3
   uint16_t* dN = reinterpret_cast<uint16_t*>(ws + pl.off_dn);
   uint16_t* dT = reinterpret_cast<uint16_t*>(ws + pl.off_dt);
   float* zk = pl.keep ? reinterpret_cast<float*>(ws + pl.off_zk) : nullptr;
+  float* slab = reinterpret_cast<float*>(ws + pl.off_slab);
 
   const int tiles_tok_n = (int)(pl.Npad / kTileN);    // tokens on the B side
   const int tiles_tok_m = (int)(pl.Npad / kTileM);    // tokens on the A side
@@ -1071,13 +1128,15 @@ int pspo_loss_fwd_bwd(const uint16_t* hidden, const uint16_t* w_head, const int3
     {
       GemmShape g{dT, pl.Vc, (int)vc, hT, pl.dpad, d, (int)pl.Npad, ctiles, tiles_d, n_act, kDynK};
       EpiDW e{V, d, (int)v0, d_w_head, accumulate};
-      if (int rc = launch_gemm(g, e, stream)) return rc;
+      if (int rc = launch_gemm_split_tail(g, e, TailDW{V, d, (int)v0, d_w_head, accumulate}, slab, stream))
+        return rc;
     }
     {
       GemmShape g{dN, pl.Npad, (int)pl.Npad, wT + (v0 / pl.Vc) * pl.dpad * pl.Vc, pl.dpad, d, (int)vc, tiles_tok_m,
                   tiles_d, n_act, kDynM};
       EpiDH e{N, d, d_hidden, v0 == 0, act_idx, n_act};
-      if (int rc = launch_gemm(g, e, stream)) return rc;
+      if (int rc = launch_gemm_split_tail(g, e, TailDH{N, d, d_hidden, v0 == 0, act_idx, n_act}, slab, stream))
+        return rc;
     }
   }
   return PSPO_OK;
