@@ -190,7 +190,7 @@ __device__ __forceinline__ int chunk_swizzle(int row) { return ((row >> 1) ^ (ro
 // spread: position l holds one of them iff the count ceil((l + 1) s / T) of
 // such slots up to l grows at l (slots evenly spaced, in increasing order);
 // the other tiles keep their order.  A bijection on [0, T).
-__device__ __forceinline__ int spread_row_tile(int l, int s, int T) {
+__host__ __device__ inline int spread_row_tile(int l, int s, int T) {
   const int c = ((l + 1) * s + T - 1) / T, cp = (l * s + T - 1) / T;
   return c > cp ? c - 1 : s + l - c;
 }
@@ -214,7 +214,7 @@ __device__ __forceinline__ void bounded_dims(const GemmShape& g, int& M, int& N,
 struct TileGrid {
   int tiles_m, tiles_n, total, per_xcd;
 };
-__device__ __forceinline__ TileGrid tile_grid(int tiles_m, int tiles_n, int M, int N) {
+__host__ __device__ inline TileGrid tile_grid(int tiles_m, int tiles_n, int M, int N) {
   TileGrid tg;
   tg.tiles_m = min(tiles_m, (M + kTileM - 1) / kTileM);
   tg.tiles_n = min(tiles_n, (N + kTileN - 1) / kTileN);
@@ -224,7 +224,7 @@ __device__ __forceinline__ TileGrid tile_grid(int tiles_m, int tiles_n, int M, i
 }
 // Tile (tm, tn) at position t of the grouped order (kGroupM row tiles x all
 // column tiles per group).
-__device__ __forceinline__ void tile_at(const TileGrid& tg, int t, int spread_m, int& tm, int& tn) {
+__host__ __device__ inline void tile_at(const TileGrid& tg, int t, int spread_m, int& tm, int& tn) {
   const int width = kGroupM * tg.tiles_n;
   const int first = (t / width) * kGroupM;
   const int gsize = min(tg.tiles_m - first, kGroupM);
@@ -245,10 +245,11 @@ enum : int {
 };
 constexpr int kTailSlots = 64;   // work-groups per XCD of a tail launch (two rounds)
 
-__device__ __forceinline__ bool map_tile(int tiles_m, int tiles_n, int M, int N, int& tm, int& tn,
-                                         int spread_m = 0, bool rounds_only = false) {
+// Tile of work-group `bid` of a whole or whole-rounds launch.
+__host__ __device__ inline bool map_tile_at(int bid, int tiles_m, int tiles_n, int M, int N, int& tm, int& tn,
+                                            int spread_m, bool rounds_only) {
   const TileGrid tg = tile_grid(tiles_m, tiles_n, M, N);
-  const int bid = blockIdx.x, k = bid / kNumXcd;
+  const int k = bid / kNumXcd;
   if (k >= tg.per_xcd) return false;
   if (rounds_only && k >= tg.per_xcd / 32 * 32) return false;
   const int t = (bid % kNumXcd) * tg.per_xcd + k;
@@ -256,11 +257,15 @@ __device__ __forceinline__ bool map_tile(int tiles_m, int tiles_n, int M, int N,
   tile_at(tg, t, spread_m, tm, tn);
   return true;
 }
+__device__ __forceinline__ bool map_tile(int tiles_m, int tiles_n, int M, int N, int& tm, int& tn,
+                                         int spread_m = 0, bool rounds_only = false) {
+  return map_tile_at(blockIdx.x, tiles_m, tiles_n, M, N, tm, tn, spread_m, rounds_only);
+}
 
 // K parts of each tail tile of an XCD with r tail tiles and nk K steps: the
 // S <= min(64 / r, nk) with the fewest rounds per part, ceil(r S / 32) / S
 // (the smaller S on ties).
-__device__ __forceinline__ int tail_parts(int r, int nk) {
+__host__ __device__ inline int tail_parts(int r, int nk) {
   int best = 1, best_rounds = (r + 31) / 32;
   for (int s = 2; s * r <= kTailSlots && s <= nk; ++s) {
     const int rounds = (r * s + 31) / 32;
@@ -284,7 +289,7 @@ struct EpiSlab {
 // XCD's tail tile k / S, K steps [part nk / S, (part + 1) nk / S).  The tail
 // tiles are the positions after the XCD's whole rounds.  Returns false for
 // work-groups without a part.
-__device__ __forceinline__ bool map_tail(const TileGrid& tg, int bid, int nk, int& tm, int& tn, int& kb, int& ke,
+__host__ __device__ inline bool map_tail(const TileGrid& tg, int bid, int nk, int& tm, int& tn, int& kb, int& ke,
                                          int* u_out = nullptr, int* parts_out = nullptr) {
   const int x = bid % kNumXcd, k = bid / kNumXcd;
   const int full = tg.per_xcd / 32 * 32;
