@@ -61,8 +61,9 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
 
 // Forward: rows = vocabulary (A = W), columns = the tokens whose logits are
 // needed (B = their hidden rows, gathered; column t is token tok[t]); writes
-// per-column softmax partials of each 384-row vocabulary tile and the target
-// logit.
+// per-column softmax partials of each 384-row vocabulary tile.  (The target
+// logits come from target_logit_kernel: picking one accumulator per column out
+// of the 48 a lane holds costs a compare and a select for each of them.)
 // kFull: every row of every tile is a token id (no per-row mask); otherwise
 // the launch is the partial last vocabulary tile, tm0 its index (the product's
 // row tile 0).  Two instantiations rather than a branch in one: with a branch
@@ -74,8 +75,6 @@ struct EpiForward {
   int tm0;
   float* part_m;
   float* part_l;
-  float* zt;
-  const int32_t* ftgt;   // target id of column t (columns t < *n_dev), in column order
   const int32_t* n_dev;
   float* zk;             // kept fp32 logits of vocabulary tiles tm < kept_tiles, or NULL:
   int kept_tiles;        //   per tile (tm, tn) a block at (tm * kept_cols + tn) * 384 * 256,
@@ -90,21 +89,20 @@ struct EpiForward {
     __builtin_amdgcn_sched_barrier(0);
     const int n = min(N, __builtin_amdgcn_readfirstlane(*n_dev));
     const int vbase = tm * kTileM + acc_row(wm, 0, 0, lane);   // this lane's rows: vbase + i*16 + r
-    // the targets of the lane's 8 columns: one load each, issued before the
-    // column loop (fenced so they are not sunk to their use) and used after it,
-    // so their latency hides behind the maxima and exponentials
-    int tgts[kBlocksN];
-#pragma unroll
-    for (int j = 0; j < kBlocksN; ++j) {
-      const int t = tn * kTileN + acc_col(wn, j, lane);
-      tgts[j] = t < n ? ftgt[t] : -1;
-    }
-    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int j = 0; j < kBlocksN; ++j) {
       const int cl = acc_col(wn, j, lane);
-      // value q = 4 i + r of the lane's column (row vbase + 16 i + r)
-      auto x = [&](int q) { return acc_get(acc, q >> 2, j, q & 3); };
+      // the lane's 48 values of column j (q = 4 i + r: row vbase + 16 i + r),
+      // the AGPR ones read once into VGPRs for both passes below
+      float xs[kBlocksM * kAccPerBlock];
+#pragma unroll
+      for (int q = 0; q < kBlocksM * kAccPerBlock; ++q) {
+        if ((q >> 2) < kBlocksAgpr)
+          asm volatile("v_accvgpr_read_b32 %0, %1" : "=v"(xs[q]) : "a"(acc.a[q >> 2][j][q & 3]));
+        else
+          xs[q] = acc.v[(q >> 2) - kBlocksAgpr][j][q & 3];
+      }
+      auto x = [&](int q) { return xs[q]; };
       float m, l;
       if constexpr (kFull) {
         // every row is a token id: three-input maxima (no per-value select),
@@ -150,16 +148,6 @@ struct EpiForward {
         red[(wm * kTileN + cl) * 2 + 1] = l;
       }
     }
-    // the target logits (each picked by the one lane whose rows hold it),
-    // stored after the picks: a conditional store among them makes the
-    // compiler keep far more accumulator copies live
-    float zvs[kBlocksN];
-    bool has[kBlocksN];
-#pragma unroll
-    for (int j = 0; j < kBlocksN; ++j) has[j] = acc_pick(acc, j, tgts[j] - vbase, zvs[j]);
-#pragma unroll
-    for (int j = 0; j < kBlocksN; ++j)
-      if (has[j]) zt[tn * kTileN + acc_col(wn, j, lane)] = zvs[j];
     __syncthreads();
     const int c = threadIdx.x;
     const float m0 = red[c * 2], l0 = red[c * 2 + 1];
@@ -176,19 +164,57 @@ struct EpiForward {
   }
 };
 
+// Target logit of forward column t < min(N, *n_dev): z[t] = W[tgt[t]] . h[idx[t]]
+// (idx: the column's token row, tgt: its target id, both in column order), the
+// exact bf16 products summed in fp32: one wave per column, lane l taking the
+// 8-element pieces l, l + 64, ..., then a fixed butterfly over the lanes.  The
+// same value as the forward product's accumulator up to the order of the fp32
+// additions.  A target outside [0, V) reads nothing and gives 0 (the finalize
+// flags it and never uses the value).  Grid ceil(Npad / 4), 256 threads.
+__global__ __launch_bounds__(256) void target_logit_kernel(const uint16_t* __restrict__ hidden,
+                                                           const uint16_t* __restrict__ w, int d, int V, int N,
+                                                           const int32_t* __restrict__ idx,
+                                                           const int32_t* __restrict__ tgt,
+                                                           const int32_t* __restrict__ n_dev, float* __restrict__ zt) {
+  const int n = min(N, *n_dev);
+  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (t >= n) return;   // uniform over the wave
+  const int o = tgt[t];
+  float sum = 0.f;
+  if (o >= 0 && o < V) {
+    const u32x4* hr = reinterpret_cast<const u32x4*>(hidden + (int64_t)idx[t] * d);
+    const u32x4* wr = reinterpret_cast<const u32x4*>(w + (int64_t)o * d);
+    for (int c = lane; c < d / 8; c += 64) {
+      const u32x4 a = hr[c], b = wr[c];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        sum = fmaf(__uint_as_float(a[e] << 16), __uint_as_float(b[e] << 16), sum);
+        sum = fmaf(__uint_as_float(a[e] & 0xFFFF0000u), __uint_as_float(b[e] & 0xFFFF0000u), sum);
+      }
+    }
+  }
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) sum += __shfl_xor(sum, off);
+  if (lane == 0) zt[t] = sum;
+}
+
 // Lane exchanges (all lanes active): DPP inside a quad (lane l ^ 1, l ^ 2) and
-// inside a 16-lane row (the value of lane l + 4 / l - 4).
+// inside a 16-lane row (the value of lane l + 4 / l - 4).  A lane whose source
+// lies outside its row reads 0 (bound_ctrl), so no destination needs an
+// initial value (with an explicit "old" operand of 0 the compiler zeroes a
+// register before every move); callers use only lanes with a valid source.
 __device__ __forceinline__ uint32_t quad_xor1(uint32_t x) {
-  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0xB1, 0xF, 0xF, false);
+  return (uint32_t)__builtin_amdgcn_mov_dpp((int)x, 0xB1, 0xF, 0xF, true);
 }
 __device__ __forceinline__ uint32_t quad_xor2(uint32_t x) {
-  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x4E, 0xF, 0xF, false);
+  return (uint32_t)__builtin_amdgcn_mov_dpp((int)x, 0x4E, 0xF, 0xF, true);
 }
 __device__ __forceinline__ uint32_t row_from_plus4(uint32_t x) {
-  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x104, 0xF, 0xF, false);   // row_shl:4
+  return (uint32_t)__builtin_amdgcn_mov_dpp((int)x, 0x104, 0xF, 0xF, true);   // row_shl:4
 }
 __device__ __forceinline__ uint32_t row_from_minus4(uint32_t x) {
-  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x114, 0xF, 0xF, false);   // row_shr:4
+  return (uint32_t)__builtin_amdgcn_mov_dpp((int)x, 0x114, 0xF, 0xF, true);   // row_shr:4
 }
 
 // 4 x 4 transpose of bf16 pairs inside a quad of lanes: lane k holds rows 0..3 of
@@ -222,8 +248,12 @@ __device__ __forceinline__ u32x2 quad_transpose(u32x2 p, int k) {
 //   * vocabulary-major: a 4 x 4 transpose inside each quad of lanes gives a
 //     lane 4 consecutive tokens of one row; exchanging with the quad 4 lanes
 //     away (DPP row shift) between the two column blocks gives it 8.
+// kFull: every row of every tile is a token id (no per-row mask; the only kind
+// when V is a multiple of 384); otherwise the launch is the partial last
+// vocabulary tile, tm0 its chunk row tile (the product's row tile 0).
+template <bool kFull>
 struct EpiDelta {
-  int V, N, v0;
+  int V, N, v0, tm0;
   uint16_t* dT;          // K-blocked [Npad/32][rT][32]: rows = vocabulary entries of the chunk, K = tokens
   int64_t rT;
   uint16_t* dN;          // K-blocked [Vc/32][rN][32]: rows = tokens, K = vocabulary entries of the chunk
@@ -233,11 +263,11 @@ struct EpiDelta {
   const float* cdelta;
   const int32_t* n_dev;
 
-  __device__ __forceinline__ void apply(AccTile& acc, int tm, int tn, int wm, int wn, int lane, float*) const {
+  __device__ __forceinline__ void apply(AccTile& acc, int tm_launch, int tn, int wm, int wn, int lane, float*) const {
     const int n = min(N, __builtin_amdgcn_readfirstlane(*n_dev));
+    const int tm = kFull ? tm_launch : tm0 + tm_launch;
     const int vl0 = tm * kTileM + acc_row(wm, 0, 0, lane);   // chunk rows of this lane: vl0 + i*16 + r
     const int vbase = v0 + vl0;
-    const bool full = v0 + (tm + 1) * kTileM <= V;            // every row of the tile is a token id
     // per-column token data of the lane's 8 columns, fetched together (one
     // round trip: the arrays are in column order)
     float dls[kBlocksN], lss[kBlocksN];
@@ -288,24 +318,11 @@ struct EpiDelta {
             for (int r = 0; r < kAccPerBlock; ++r) {
               const int v = vbase + i * 16 + r;
               x[r] = logit_grad(acc_get(acc, i, j, r), lss[j], dls[j], v == tgs[j]);
-              if (!full) x[r] = (v < V) ? x[r] : 0.f;
+              if constexpr (!kFull) x[r] = (v < V) ? x[r] : 0.f;
             }
             blk[ii][jj].x = pack_bf16x2(x[0], x[1]);
             blk[ii][jj].y = pack_bf16x2(x[2], x[3]);
           }
-        // token-major stores, one per column block
-#pragma unroll
-        for (int jj = 0; jj < 2; ++jj) {
-          const auto sx = __builtin_amdgcn_permlane16_swap(blk[0][jj].x, blk[1][jj].x, false, false);
-          const auto sy = __builtin_amdgcn_permlane16_swap(blk[0][jj].y, blk[1][jj].y, false, false);
-          u32x4 o;
-          o.x = sx[0];
-          o.y = sy[0];
-          o.z = sx[1];
-          o.w = sy[1];
-          *reinterpret_cast<u32x4*>(nbase + (noff + (uint32_t)ip * kstepN +
-                                             (uint32_t)((2 * jp + jj) * 16 * kTileK * 2))) = o;
-        }
         // vocabulary-major stores, one per row block
 #pragma unroll
         for (int ii = 0; ii < 2; ++ii) {
@@ -327,6 +344,20 @@ struct EpiDelta {
           o.w = qeven ? recv.y : t1.y;
           *reinterpret_cast<u32x4*>(tbase + (toff + (uint32_t)jp * kstepT +
                                              (uint32_t)((2 * ip + ii) * 16 * kTileK * 2))) = o;
+        }
+        // token-major stores, one per column block (after the vocabulary-major
+        // ones: the in-place row swaps then consume the packed values without copies)
+#pragma unroll
+        for (int jj = 0; jj < 2; ++jj) {
+          const auto sx = __builtin_amdgcn_permlane16_swap(blk[0][jj].x, blk[1][jj].x, false, false);
+          const auto sy = __builtin_amdgcn_permlane16_swap(blk[0][jj].y, blk[1][jj].y, false, false);
+          u32x4 o;
+          o.x = sx[0];
+          o.y = sy[0];
+          o.z = sx[1];
+          o.w = sy[1];
+          *reinterpret_cast<u32x4*>(nbase + (noff + (uint32_t)ip * kstepN +
+                                             (uint32_t)((2 * jp + jj) * 16 * kTileK * 2))) = o;
         }
         __builtin_amdgcn_sched_barrier(0);   // one group's values live at a time
       }
@@ -1067,7 +1098,7 @@ int pspo_loss_fwd_bwd(const uint16_t* hidden, const uint16_t* w_head, const int3
   hipLaunchKernelGGL(kblock_rows_kernel, dim3(ctiles64, (unsigned)(pl.Npad / 32)), dim3(256), 0, stream, hidden,
                      (int64_t)d, N, fwd_idx, n_fwd, hk, pl.Npad, nullptr, (int64_t)0, (int64_t)kTileK);
   PSPO_HIP_CHECK(hipGetLastError());
-  // 2. forward logits -> per-tile softmax partials and target logits: the
+  // 2. forward logits -> per-tile softmax partials (target logits apart): the
   //    vocabulary tiles whose rows are all token ids, then a partial last one
   {
     const int tiles_full = V / kTileM, kept_tiles = zk != nullptr ? (int)(pl.Vc / kTileM) : 0;
@@ -1075,16 +1106,19 @@ int pspo_loss_fwd_bwd(const uint16_t* hidden, const uint16_t* w_head, const int3
       // the kept tiles' stores spread over the XCDs
       GemmShape g{wk, pl.Vpad, tiles_full * kTileM, hk, pl.Npad, N, d, tiles_full, tiles_tok_n, n_fwd, kDynN,
                   kept_tiles < tiles_full ? kept_tiles : tiles_full};
-      EpiForward<true> e{V, N, pl.Npad, 0, part_m, part_l, zt, fwd_tgt, n_fwd, zk, kept_tiles, tiles_tok_n};
+      EpiForward<true> e{V, N, pl.Npad, 0, part_m, part_l, n_fwd, zk, kept_tiles, tiles_tok_n};
       if (int rc = launch_gemm(g, e, stream)) return rc;
     }
     if (tiles_full < tiles_voc) {
       GemmShape g{wk + (int64_t)tiles_full * kTileM * kTileK, pl.Vpad, V - tiles_full * kTileM, hk, pl.Npad, N, d, 1,
                   tiles_tok_n, n_fwd, kDynN};
-      EpiForward<false> e{V, N, pl.Npad, tiles_full, part_m, part_l, zt, fwd_tgt, n_fwd, zk, kept_tiles, tiles_tok_n};
+      EpiForward<false> e{V, N, pl.Npad, tiles_full, part_m, part_l, n_fwd, zk, kept_tiles, tiles_tok_n};
       if (int rc = launch_gemm(g, e, stream)) return rc;
     }
   }
+  hipLaunchKernelGGL(target_logit_kernel, dim3((unsigned)(pl.Npad / 4)), dim3(256), 0, stream, hidden, w_head, d, V,
+                     N, fwd_idx, fwd_tgt, n_fwd, zt);
+  PSPO_HIP_CHECK(hipGetLastError());
   // 3. lse, PPO terms, delta, loss
   hipLaunchKernelGGL(finalize_kernel, dim3((unsigned)pl.nfin), dim3(kFinThreads), 0, stream, N, V, R, tiles_voc,
                      pl.Npad, part_m, part_l, zt, fwd_pos, target, logp_old, weight, seq_id, advantage, eps_low,
@@ -1121,9 +1155,21 @@ int pspo_loss_fwd_bwd(const uint16_t* hidden, const uint16_t* w_head, const int3
                          pl.Vc);
       PSPO_HIP_CHECK(hipGetLastError());
     } else {
-      GemmShape g{wk + v0 * kTileK, pl.Vpad, (int)(V - v0), hk, pl.Npad, N, d, ctiles, tiles_tok_n, n_act, kDynN};
-      EpiDelta e{V, N, (int)v0, dT, pl.Vc, dN, pl.Npad, act_tgt, act_lse, act_delta, n_act};
-      if (int rc = launch_gemm(g, e, stream)) return rc;
+      // the chunk's vocabulary tiles whose rows are all token ids, then a
+      // partial last one (the last chunk's, when 384 does not divide V)
+      const int64_t rows = (V - v0) < vc ? (V - v0) : vc;
+      const int tfull = (int)(rows / kTileM);
+      if (tfull > 0) {
+        GemmShape g{wk + v0 * kTileK, pl.Vpad, tfull * kTileM, hk, pl.Npad, N, d, tfull, tiles_tok_n, n_act, kDynN};
+        EpiDelta<true> e{V, N, (int)v0, 0, dT, pl.Vc, dN, pl.Npad, act_tgt, act_lse, act_delta, n_act};
+        if (int rc = launch_gemm(g, e, stream)) return rc;
+      }
+      if (tfull < ctiles) {
+        const int64_t vp = v0 + (int64_t)tfull * kTileM;   // first row of the partial tile
+        GemmShape g{wk + vp * kTileK, pl.Vpad, (int)(V - vp), hk, pl.Npad, N, d, 1, tiles_tok_n, n_act, kDynN};
+        EpiDelta<false> e{V, N, (int)v0, tfull, dT, pl.Vc, dN, pl.Npad, act_tgt, act_lse, act_delta, n_act};
+        if (int rc = launch_gemm(g, e, stream)) return rc;
+      }
     }
     {
       GemmShape g{dT, pl.Vc, (int)vc, hT, pl.dpad, d, (int)pl.Npad, ctiles, tiles_d, n_act, kDynK};
