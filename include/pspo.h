@@ -58,9 +58,11 @@ typedef enum {
 /* Flags of pspo_loss_fwd_bwd. */
 #define PSPO_ACCUMULATE_DW   1u /* d_w_head += gradient instead of d_w_head = gradient */
 #define PSPO_RECOMPUTE_LOGITS 2u /* recompute every logit tile in the backward instead of keeping the
-                                    first vocabulary chunk's fp32 logits from the forward: the same
-                                    results (bitwise), a smaller workspace (by Vc x Npad x 4 bytes),
-                                    more matrix-core work */
+                                    first vocabulary chunk's logits from the forward (as fp16 offsets
+                                    from each tile's per-column maximum): the same loss, log-probs and
+                                    stats (bitwise), gradients that differ by ~1e-4 relative (the fp16
+                                    rounding of the kept offsets), a smaller workspace (by Vc x Npad x 2
+                                    bytes), more matrix-core work */
 
 /* Human-readable name of a status code (static storage). */
 const char* pspo_status_string(int status);
@@ -166,8 +168,9 @@ size_t pspo_loss_workspace_bytes(int32_t N, int32_t d, int32_t V, uint32_t flags
  *   d_hidden[i] = G_i W,   d_w_head = sum_i G_i^T h_i.
  * The [N, V] logits are never written to memory whole: the workspace holds
  * per-token softmax statistics, one vocabulary chunk of bf16 logit gradients
- * (in two layouts) and the fp32 logits of the first chunk, kept by the forward
- * so that the backward recomputes the logit tiles of the other chunks only.
+ * (in two layouts) and the logits of the first chunk (fp16 offsets from each
+ * 384-row tile's per-column maximum), kept by the forward so that the backward
+ * recomputes the logit tiles of the other chunks only.
  * The chunk is Vc = 384 * 256 / gcd(ceil(d / 256), 256) vocabulary rows (the
  * whole padded vocabulary if that is smaller); 49152 at d = 3584.
  *

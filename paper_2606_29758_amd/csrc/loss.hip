@@ -59,6 +59,57 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{lo, hi}, bf16x2));
 }
 
+// Two floats as packed fp16 (round to nearest even), and one fp16 back.
+__device__ __forceinline__ uint32_t pack_f16x2(float lo, float hi) {
+  typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{lo, hi}, f16x2));
+}
+__device__ __forceinline__ float f16_bits_to_f32(uint32_t bits) {
+  return (float)__builtin_bit_cast(_Float16, (uint16_t)(bits & 0xFFFFu));
+}
+
+// A forward tile's logits kept for the first backward chunk, as fp16 offsets
+// from the tile's per-column maximum M (the value the forward writes to its
+// partial maxima, taken here from the same two wave maxima in `red`):
+// [24 blocks of 16 rows][256 columns][16 rows] fp16 at `base`.  The lane's 4
+// rows of accumulator block (i, j) are one 8-byte piece, so each store
+// instruction writes 512 contiguous bytes (whole 128-byte lines).  Every kept
+// value is <= 0 and the large softmax entries sit near 0, where fp16 holds an
+// offset to ~2^-11 relative: the logit gradient rebuilt from it stays far
+// inside the bf16 rounding the gradient gets anyway, at half the bytes of the
+// fp32 logits.
+__device__ __forceinline__ void store_kept_f16(const AccTile& acc, const float* red, uint16_t* base, int wm, int wn,
+                                               int lane) {
+  unsigned char* zb = reinterpret_cast<unsigned char*>(base);
+  float M[kBlocksN];
+#pragma unroll
+  for (int j = 0; j < kBlocksN; ++j) {
+    const int cl = acc_col(wn, j, lane);
+    M[j] = fmaxf(red[cl * 2], red[(kTileN + cl) * 2]);
+  }
+  const uint32_t lo = (uint32_t)(wm * (kWaveM / 16)) * (kTileN * 32u) + (uint32_t)(wn * kWaveN + (lane & 15)) * 32u +
+                      (uint32_t)(lane >> 4) * 8u;
+#pragma unroll
+  for (int i = 0; i < kBlocksM; ++i) {
+#pragma unroll
+    for (int j = 0; j < kBlocksN; ++j) {
+      float x[kAccPerBlock];
+#pragma unroll
+      for (int r = 0; r < kAccPerBlock; ++r) {
+        if (i < kBlocksAgpr)
+          asm volatile("v_accvgpr_read_b32 %0, %1" : "=v"(x[r]) : "a"(acc.a[i][j][r]));
+        else
+          x[r] = acc.v[i - kBlocksAgpr][j][r];
+      }
+      u32x2 h;
+      h.x = pack_f16x2(x[0] - M[j], x[1] - M[j]);
+      h.y = pack_f16x2(x[2] - M[j], x[3] - M[j]);
+      __builtin_nontemporal_store(h, reinterpret_cast<u32x2*>(zb + (lo + (uint32_t)(i * kTileN * 32 + j * 512))));
+    }
+    __builtin_amdgcn_sched_barrier(0);   // one row block's stores at a time
+  }
+}
+
 // Forward: rows = vocabulary (A = W), columns = the tokens whose logits are
 // needed (B = their hidden rows, gathered; column t is token tok[t]); writes
 // per-column softmax partials of each 384-row vocabulary tile.  (The target
@@ -76,17 +127,14 @@ struct EpiForward {
   float* part_m;
   float* part_l;
   const int32_t* n_dev;
-  float* zk;             // kept fp32 logits of vocabulary tiles tm < kept_tiles, or NULL:
-  int kept_tiles;        //   per tile (tm, tn) a block at (tm * kept_cols + tn) * 384 * 256,
-  int kept_cols;         //   [24 blocks of 16 rows][256 columns][16]
+  uint16_t* zk;          // kept fp16 logit offsets of vocabulary tiles tm < kept_tiles, or NULL:
+  int kept_tiles;        //   per tile (tm, tn) a block at (tm * kept_cols + tn) * 384 * 256
+  int kept_cols;         //   (store_kept_f16)
 
   __device__ __forceinline__ void apply(const AccTile& acc, int tm_launch, int tn, int wm, int wn, int lane,
                                         float* smem) const {
     float* red = smem;  // [2 wave rows][256 columns][m, l]
     const int tm = kFull ? tm_launch : tm0 + tm_launch;
-    if (zk != nullptr && tm < kept_tiles)   // the tile's fp32 logits, kept for the first backward chunk
-      store_tile_rows16(acc, zk + ((int64_t)tm * kept_cols + tn) * (kTileM * kTileN), wm, wn, lane);
-    __builtin_amdgcn_sched_barrier(0);
     const int n = min(N, __builtin_amdgcn_readfirstlane(*n_dev));
     const int vbase = tm * kTileM + acc_row(wm, 0, 0, lane);   // this lane's rows: vbase + i*16 + r
 #pragma unroll
@@ -161,6 +209,8 @@ struct EpiForward {
       part_m[tm * ldp + t] = M;
       part_l[tm * ldp + t] = L;
     }
+    if (zk != nullptr && tm < kept_tiles)   // the tile's logits, kept for the first backward chunk
+      store_kept_f16(acc, red, zk + ((int64_t)tm * kept_cols + tn) * (kTileM * kTileN), wm, wn, lane);
   }
 };
 
@@ -366,29 +416,24 @@ struct EpiDelta {
 };
 
 // The logit gradient of the first vocabulary chunk from the forward's kept
-// fp32 logits (zk: per 384 x 256 forward tile (tm, tn) a block at
-// (tm * kept_cols + tn) * 384 * 256, [24 blocks of 16 rows][256 columns][16])
-// instead of a recomputing product: the values and layouts the
-// logit-gradient epilogue writes for that chunk.  Backward column a < n =
-// min(N, *n_dev) has the target, lse and delta ctgt[a], clse[a], cdelta[a] and
-// its logits sit in forward column afwd[a];
-// columns n <= a < round_up(n, 32) are written as the zero gradient of a
-// padding column (the dW product reads whole 32-token K steps); rows v >= V
-// are zero.
-// Grid (ceil(Vc / (128 kConvSeg)), Npad / 32), 256 threads: 32 backward
-// tokens x up to kConvSeg segments of 128 vocabulary entries per block, every
-// segment's logits loaded before the first is converted.  (One segment per
-// block: with four, twice the bytes in flight per thread, the kernel ran no
-// faster; it moves its bytes at ~5 TB/s, reads and writes mixed.)  Load q of
-// segment sg of thread `tid` takes the 16-byte quarter tid % 4 of token
-// (tid % 128) / 4's 64-byte piece of 16-row block 2q + tid / 128, so one load
-// instruction reads whole runs of consecutive tokens' pieces; each segment's
-// gradient goes through LDS and out in both layouts as 16-byte stores of whole
-// 64-byte K rows.
-constexpr int kConvSeg = 1;
-
-__global__ __launch_bounds__(256) void logit_grad_kept_kernel(const float* __restrict__ zk, int kept_cols, int Vc,
-                                                              int V, int N, const int32_t* __restrict__ n_dev,
+// fp16 logit offsets (zk: per 384 x 256 forward tile (tm, tn) a block at
+// (tm * kept_cols + tn) * 384 * 256, [24 blocks of 16 rows][256 columns][16];
+// the logit is M + offset with M the tile's per-column maximum in part_m)
+// instead of a recomputing product: the values and layouts the logit-gradient
+// epilogue writes for that chunk.  Backward column a < n = min(N, *n_dev) has
+// the target, lse and delta ctgt[a], clse[a], cdelta[a] and its logits sit in
+// forward column afwd[a]; columns n <= a < round_up(n, 32) are written as the
+// zero gradient of a padding column (the dW product reads whole 32-token K
+// steps); rows v >= V are zero.
+// Grid (Vc / 128, Npad / 32), 256 threads: 32 backward tokens x 128 vocabulary
+// entries per block; thread tid takes token tid % 32's 32-byte piece (16 rows)
+// of 16-row block tid / 32, so 32 consecutive threads read the pieces of 32
+// consecutive backward tokens; the gradient goes through LDS and out in both
+// layouts as 16-byte stores of whole 64-byte K rows.
+__global__ __launch_bounds__(256) void logit_grad_kept_kernel(const uint16_t* __restrict__ zk,
+                                                              const float* __restrict__ part_m, int64_t ldp,
+                                                              int kept_cols, int Vc, int V, int N,
+                                                              const int32_t* __restrict__ n_dev,
                                                               const int32_t* __restrict__ afwd,
                                                               const int32_t* __restrict__ ctgt,
                                                               const float* __restrict__ clse,
@@ -397,71 +442,56 @@ __global__ __launch_bounds__(256) void logit_grad_kept_kernel(const float* __res
                                                               uint16_t* __restrict__ dT, int64_t rT) {
   __shared__ uint16_t tile[32][128 + 8];   // [token][entry]; padded rows: the column reads hit distinct banks
   const int n = min(N, *n_dev);
-  const int a0 = blockIdx.y * 32, vb = blockIdx.x * (128 * kConvSeg);
+  const int a0 = blockIdx.y * 32, v0 = blockIdx.x * 128;   // Vc is a multiple of 128
   if (a0 >= n) return;
-  const int nseg = min(kConvSeg, (Vc - vb) / 128);   // Vc is a multiple of 128
   const int tid = threadIdx.x;
-  const int al = (tid & 127) >> 2, qt = tid & 3, a = a0 + al;
-  float dl = 0.f, ls = 0.f;
-  int tg = -1;
-  f32x4 z[kConvSeg][4];
-#pragma unroll
-  for (int sg = 0; sg < kConvSeg; ++sg)
-#pragma unroll
-    for (int q = 0; q < 4; ++q) z[sg][q] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const int al = tid & 31, a = a0 + al;
+  const int vl = (tid >> 5) * 16, v = v0 + vl;   // this thread's 16 rows
+  uint32_t w[8] = {0u, 0u, 0u, 0u, 0u, 0u, 0u, 0u};   // 16 bf16 (zero for padding columns)
   if (a < n) {
     const int f = afwd[a];
+    const int vt = v / kTileM;
+    const uint16_t* src = zk + ((int64_t)vt * kept_cols + (f >> 8)) * (kTileM * kTileN) +
+                          (((v - vt * kTileM) >> 4) * kTileN + (f & (kTileN - 1))) * 16;
+    const u32x4 h0 = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src));
+    const u32x4 h1 = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src + 8));
+    const float M = part_m[vt * ldp + f];
+    const float dl = cdelta[a];
+    const float ls = clse[a] * kLog2e;   // lse log2(e), as the recomputing epilogue takes it
+    const int tg = ctgt[a];
 #pragma unroll
-    for (int sg = 0; sg < kConvSeg; ++sg) {
-      if (sg < nseg) {
+    for (int e2 = 0; e2 < 8; ++e2) {
+      const uint32_t hb = e2 < 4 ? h0[e2] : h1[e2 - 4];
+      float x[2];
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int v = vb + sg * 128 + (2 * q + (tid >> 7)) * 16, vt = v / kTileM;
-          const float* src = zk + ((int64_t)vt * kept_cols + (f >> 8)) * (kTileM * kTileN) +
-                             ((((v - vt * kTileM) >> 4) * kTileN + (f & (kTileN - 1))) * 16 + qt * 4);
-          z[sg][q] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(src));
-        }
+      for (int u = 0; u < 2; ++u) {
+        const int e = 2 * e2 + u;
+        x[u] = logit_grad(M + f16_bits_to_f32(hb >> (16 * u)), ls, dl, v + e == tg);
+        if (v + e >= V) x[u] = 0.f;
       }
+      w[e2] = pack_bf16x2(x[0], x[1]);
     }
-    dl = cdelta[a];
-    ls = clse[a] * kLog2e;   // lse log2(e), as the recomputing epilogue takes it
-    tg = ctgt[a];
   }
+  *reinterpret_cast<u32x4*>(&tile[al][vl]) = u32x4{w[0], w[1], w[2], w[3]};
+  *reinterpret_cast<u32x4*>(&tile[al][vl + 8]) = u32x4{w[4], w[5], w[6], w[7]};
+  __syncthreads();
+  // token-major: token a0 + tid / 8, entries v0 + (tid % 8) * 16 .. +15
+  {
+    const int tl = tid >> 3, ol = (tid & 7) * 16, ov = v0 + ol;
+    uint16_t* pn = dN + ((int64_t)(ov >> 5) * rN + a0 + tl) * kTileK + (ov & 31);
+    *reinterpret_cast<u32x4*>(pn) = *reinterpret_cast<const u32x4*>(&tile[tl][ol]);
+    *reinterpret_cast<u32x4*>(pn + 8) = *reinterpret_cast<const u32x4*>(&tile[tl][ol + 8]);
+  }
+  // vocabulary-major: entry v0 + tid / 2 of tokens a0 + (tid % 2) * 16 .. +15
+  {
+    const int ol = tid >> 1, ap = (tid & 1) * 16;
+    uint32_t q[8];
 #pragma unroll
-  for (int sg = 0; sg < kConvSeg; ++sg) {
-    if (sg >= nseg) break;
-    const int v0 = vb + sg * 128;
-    if (sg > 0) __syncthreads();   // the previous segment's LDS reads are done
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int vl = (2 * q + (tid >> 7)) * 16 + qt * 4, v = v0 + vl;
-      float x[4];
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        x[e] = logit_grad(z[sg][q][e], ls, dl, v + e == tg);
-        if (v + e >= V) x[e] = 0.f;
-      }
-      *reinterpret_cast<uint2*>(&tile[al][vl]) = make_uint2(pack_bf16x2(x[0], x[1]), pack_bf16x2(x[2], x[3]));
-    }
-    __syncthreads();
-    // token-major: token a0 + tid / 8, entries v0 + (tid % 8) * 16 .. +15
-    {
-      const int tl = tid >> 3, vl = (tid & 7) * 16, v = v0 + vl;
-      uint16_t* pn = dN + ((int64_t)(v >> 5) * rN + a0 + tl) * kTileK + (v & 31);
-      *reinterpret_cast<u32x4*>(pn) = *reinterpret_cast<const u32x4*>(&tile[tl][vl]);
-      *reinterpret_cast<u32x4*>(pn + 8) = *reinterpret_cast<const u32x4*>(&tile[tl][vl + 8]);
-    }
-    // vocabulary-major: entry v0 + tid / 2 of tokens a0 + (tid % 2) * 16 .. +15
-    {
-      const int vl = tid >> 1, ap = (tid & 1) * 16;
-      uint32_t w[8];
-#pragma unroll
-      for (int e = 0; e < 8; ++e)
-        w[e] = (uint32_t)tile[ap + 2 * e][vl] | ((uint32_t)tile[ap + 2 * e + 1][vl] << 16);
-      uint16_t* pt = dT + ((int64_t)(a0 >> 5) * rT + v0 + vl) * kTileK + ap;
-      *reinterpret_cast<u32x4*>(pt) = u32x4{w[0], w[1], w[2], w[3]};
-      *reinterpret_cast<u32x4*>(pt + 8) = u32x4{w[4], w[5], w[6], w[7]};
-    }
+    for (int e = 0; e < 8; ++e)
+      q[e] = (uint32_t)tile[ap + 2 * e][ol] | ((uint32_t)tile[ap + 2 * e + 1][ol] << 16);
+    uint16_t* pt = dT + ((int64_t)(a0 >> 5) * rT + v0 + ol) * kTileK + ap;
+    *reinterpret_cast<u32x4*>(pt) = u32x4{q[0], q[1], q[2], q[3]};
+    *reinterpret_cast<u32x4*>(pt + 8) = u32x4{q[4], q[5], q[6], q[7]};
   }
 }
 
@@ -907,7 +937,7 @@ struct Plan {
   int64_t Npad, Vpad, dpad, Vc, ntv, nfin;
   int64_t off_pm, off_pl, off_zt, off_lse, off_delta, off_fidx, off_fpos, off_nfwd, off_idx, off_nact, off_afwd, off_ctgt, off_clse, off_cdelta, off_ftgt, off_cnt, off_blk, off_wk,
       off_hk, off_ht, off_wt, off_dn, off_dt, off_slab, off_zk, total;
-  bool keep;   // the forward keeps the first chunk's fp32 logits
+  bool keep;   // the forward keeps the first chunk's logits (fp16 offsets from the tile maxima)
 };
 
 Plan make_plan(int64_t N, int64_t d, int64_t V, bool keep) {
@@ -962,7 +992,7 @@ Plan make_plan(int64_t N, int64_t d, int64_t V, bool keep) {
   p.off_dt = take(p.Vc * p.Npad * 2);                                 // K-blocked [Npad/32][Vc][32]
   p.off_slab = take((int64_t)kNumXcd * kTailSlots * kTileM * kTileN * 4);   // K parts of tail tiles
   p.keep = keep;
-  p.off_zk = take(keep ? p.Vc * p.Npad * 4 : 0);                      // kept fp32 logits, one block per forward tile
+  p.off_zk = take(keep ? p.Vc * p.Npad * 2 : 0);                      // kept fp16 logit offsets, one block per forward tile
   p.total = o;
   return p;
 }
@@ -1076,7 +1106,7 @@ int pspo_loss_fwd_bwd(const uint16_t* hidden, const uint16_t* w_head, const int3
   uint16_t* wT = reinterpret_cast<uint16_t*>(ws + pl.off_wt);
   uint16_t* dN = reinterpret_cast<uint16_t*>(ws + pl.off_dn);
   uint16_t* dT = reinterpret_cast<uint16_t*>(ws + pl.off_dt);
-  float* zk = pl.keep ? reinterpret_cast<float*>(ws + pl.off_zk) : nullptr;
+  uint16_t* zk = pl.keep ? reinterpret_cast<uint16_t*>(ws + pl.off_zk) : nullptr;
   float* slab = reinterpret_cast<float*>(ws + pl.off_slab);
 
   const int tiles_tok_n = (int)(pl.Npad / kTileN);    // tokens on the B side
@@ -1148,11 +1178,9 @@ int pspo_loss_fwd_bwd(const uint16_t* hidden, const uint16_t* w_head, const int3
     const int64_t vc = (pl.Vpad - v0) < pl.Vc ? (pl.Vpad - v0) : pl.Vc;
     const int ctiles = (int)(vc / kTileM);
     if (v0 == 0 && zk != nullptr) {
-      hipLaunchKernelGGL(logit_grad_kept_kernel,
-                         dim3((unsigned)((pl.Vc + 128 * kConvSeg - 1) / (128 * kConvSeg)), (unsigned)(pl.Npad / 32)),
-                         dim3(256), 0, stream, zk, tiles_tok_n, (int)pl.Vc, V, N, n_act, act_fwd, act_tgt, act_lse,
-                         act_delta, dN, pl.Npad, dT,
-                         pl.Vc);
+      hipLaunchKernelGGL(logit_grad_kept_kernel, dim3((unsigned)(pl.Vc / 128), (unsigned)(pl.Npad / 32)), dim3(256), 0,
+                         stream, zk, part_m, pl.Npad, tiles_tok_n, (int)pl.Vc, V, N, n_act, act_fwd, act_tgt, act_lse,
+                         act_delta, dN, pl.Npad, dT, pl.Vc);
       PSPO_HIP_CHECK(hipGetLastError());
     } else {
       // the chunk's vocabulary tiles whose rows are all token ids, then a

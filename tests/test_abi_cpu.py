@@ -140,13 +140,13 @@ def test_loss_argument_errors(lib):
 
 def test_workspace_bytes_recompute_flag(lib):
     # without PSPO_RECOMPUTE_LOGITS the forward keeps the first vocabulary
-    # chunk's fp32 logits: Vc x round_up(N, 768) x 4 bytes more (Vc = 49152 at
+    # chunk's logits as fp16 offsets: Vc x round_up(N, 768) x 2 bytes more (Vc = 49152 at
     # d = 3584, the whole padded vocabulary when that is smaller)
     for N, d, V, vc in ((1000, 3584, 152064, 49152), (300, 128, 2048, 2304), (5000, 4096, 151936, 6144)):
         keep = lib.pspo_loss_workspace_bytes(N, d, V, 0)
         lean = lib.pspo_loss_workspace_bytes(N, d, V, 2)
         npad = -(-N // 768) * 768
-        assert keep - lean == vc * npad * 4, (N, d, V)
+        assert keep - lean == vc * npad * 2, (N, d, V)
 
 
 def test_workspace_bytes(lib):
