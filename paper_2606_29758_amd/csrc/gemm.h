@@ -116,25 +116,6 @@ __device__ __forceinline__ int acc_row(int wm, int i, int r, int lane) {
 }
 __device__ __forceinline__ int acc_col(int wn, int j, int lane) { return wn * kWaveN + j * 16 + (lane & 15); }
 
-// The accumulator of column block j that sits in row `rel` of this lane's rows
-// (rel = row - (wm * 192 + (lane / 16) * 4); the lane holds rows i * 16 + r,
-// i < 12, r < 4), picked with selects only (no divergent branch per value).
-// Returns whether the lane holds that row.
-__device__ __forceinline__ bool acc_pick(const AccTile& acc, int j, int rel, float& value) {
-  float z = 0.f;
-  bool has = false;
-#pragma unroll
-  for (int i = 0; i < kBlocksM; ++i)
-#pragma unroll
-    for (int r = 0; r < kAccPerBlock; ++r) {
-      const bool hit = rel == i * 16 + r;
-      z = hit ? acc_get(acc, i, j, r) : z;
-      has = has || hit;
-    }
-  value = z;
-  return has;
-}
-
 constexpr float kLog2e = 1.4426950408889634f;
 
 // max(a, b, c) in one instruction (v_max3_f32, IEEE maxNum semantics: a NaN

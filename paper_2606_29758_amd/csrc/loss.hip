@@ -33,6 +33,7 @@
 #include "common.h"
 #include "gemm.h"
 #include "layout.h"
+#include "rowdot.h"
 
 namespace pspo {
 namespace {
@@ -113,7 +114,7 @@ __device__ __forceinline__ void store_kept_f16(const AccTile& acc, const float* 
 // Forward: rows = vocabulary (A = W), columns = the tokens whose logits are
 // needed (B = their hidden rows, gathered; column t is token tok[t]); writes
 // per-column softmax partials of each 384-row vocabulary tile.  (The target
-// logits come from target_logit_kernel: picking one accumulator per column out
+// logits come from row_dots_kernel: picking one accumulator per column out
 // of the 48 a lane holds costs a compare and a select for each of them.)
 // kFull: every row of every tile is a token id (no per-row mask); otherwise
 // the launch is the partial last vocabulary tile, tm0 its index (the product's
@@ -213,41 +214,6 @@ struct EpiForward {
       store_kept_f16(acc, red, zk + ((int64_t)tm * kept_cols + tn) * (kTileM * kTileN), wm, wn, lane);
   }
 };
-
-// Target logit of forward column t < min(N, *n_dev): z[t] = W[tgt[t]] . h[idx[t]]
-// (idx: the column's token row, tgt: its target id, both in column order), the
-// exact bf16 products summed in fp32: one wave per column, lane l taking the
-// 8-element pieces l, l + 64, ..., then a fixed butterfly over the lanes.  The
-// same value as the forward product's accumulator up to the order of the fp32
-// additions.  A target outside [0, V) reads nothing and gives 0 (the finalize
-// flags it and never uses the value).  Grid ceil(Npad / 4), 256 threads.
-__global__ __launch_bounds__(256) void target_logit_kernel(const uint16_t* __restrict__ hidden,
-                                                           const uint16_t* __restrict__ w, int d, int V, int N,
-                                                           const int32_t* __restrict__ idx,
-                                                           const int32_t* __restrict__ tgt,
-                                                           const int32_t* __restrict__ n_dev, float* __restrict__ zt) {
-  const int n = min(N, *n_dev);
-  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
-  const int lane = threadIdx.x & 63;
-  if (t >= n) return;   // uniform over the wave
-  const int o = tgt[t];
-  float sum = 0.f;
-  if (o >= 0 && o < V) {
-    const u32x4* hr = reinterpret_cast<const u32x4*>(hidden + (int64_t)idx[t] * d);
-    const u32x4* wr = reinterpret_cast<const u32x4*>(w + (int64_t)o * d);
-    for (int c = lane; c < d / 8; c += 64) {
-      const u32x4 a = hr[c], b = wr[c];
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        sum = fmaf(__uint_as_float(a[e] << 16), __uint_as_float(b[e] << 16), sum);
-        sum = fmaf(__uint_as_float(a[e] & 0xFFFF0000u), __uint_as_float(b[e] & 0xFFFF0000u), sum);
-      }
-    }
-  }
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) sum += __shfl_xor(sum, off);
-  if (lane == 0) zt[t] = sum;
-}
 
 // Lane exchanges (all lanes active): DPP inside a quad (lane l ^ 1, l ^ 2) and
 // inside a 16-lane row (the value of lane l + 4 / l - 4).  A lane whose source
@@ -1146,8 +1112,9 @@ int pspo_loss_fwd_bwd(const uint16_t* hidden, const uint16_t* w_head, const int3
       if (int rc = launch_gemm(g, e, stream)) return rc;
     }
   }
-  hipLaunchKernelGGL(target_logit_kernel, dim3((unsigned)(pl.Npad / 4)), dim3(256), 0, stream, hidden, w_head, d, V,
-                     N, fwd_idx, fwd_tgt, n_fwd, zt);
+  // the target logit of each forward column (the column's token row and target)
+  hipLaunchKernelGGL(row_dots_kernel, dim3((unsigned)(pl.Npad / 4)), dim3(256), 0, stream, hidden, w_head, d, V, N,
+                     fwd_idx, fwd_tgt, n_fwd, zt, nullptr);
   PSPO_HIP_CHECK(hipGetLastError());
   // 3. lse, PPO terms, delta, loss
   hipLaunchKernelGGL(finalize_kernel, dim3((unsigned)pl.nfin), dim3(kFinThreads), 0, stream, N, V, R, tiles_voc,

@@ -24,6 +24,7 @@
 #include "common.h"
 #include "gemm.h"
 #include "layout.h"
+#include "rowdot.h"
 
 namespace pspo {
 namespace {
@@ -32,7 +33,9 @@ constexpr float kNegInf = -INFINITY;
 
 // rows = vocabulary (A = W), columns = tokens (B = H).  Writes, per column and
 // 384-row vocabulary tile, (m, S1, S2) over the tile's rows other than the
-// column's target, and the target logit.
+// column's target.  (The target logits come from row_dots_kernel: picking one
+// accumulator per column out of the 48 a lane holds costs a compare and a
+// select for each of them.)
 // kFull: every row of every tile is a token id (no per-row mask); otherwise
 // the launch is the partial last vocabulary tile, tm0 its index.  Two
 // instantiations rather than a branch in one: with a branch the compiler
@@ -46,7 +49,6 @@ struct EpiProxy {
   float* part_m;
   float* part_s1;
   float* part_s2;
-  float* zt;
 
   __device__ __forceinline__ void apply(const AccTile& acc, int tm_launch, int tn, int wm, int wn, int,
                                         float* smem) const {
@@ -65,17 +67,21 @@ struct EpiProxy {
     }
 #pragma unroll
     for (int j = 0; j < kBlocksN; ++j) asm volatile("" ::"v"(tgts[j]));   // keep the batch: no sinking
-    // the target logits are stored after the column loop (a conditional store
-    // inside it makes the compiler keep far more accumulator copies live)
-    float zvs[kBlocksN];
-    bool has[kBlocksN];
 #pragma unroll
     for (int j = 0; j < kBlocksN; ++j) {
       const int cl = acc_col(wn, j, lane);
       const int tgt = tgts[j];
-      has[j] = acc_pick(acc, j, tgt - vbase, zvs[j]);
-      // value q = 4 i + r of the lane's column (row vbase + 16 i + r)
-      auto x = [&](int q) { return acc_get(acc, q >> 2, j, q & 3); };
+      // the lane's 48 values of column j (q = 4 i + r: row vbase + 16 i + r),
+      // the AGPR ones read once into VGPRs for both passes below
+      float xs[kBlocksM * kAccPerBlock];
+#pragma unroll
+      for (int q = 0; q < kBlocksM * kAccPerBlock; ++q) {
+        if ((q >> 2) < kBlocksAgpr)
+          asm volatile("v_accvgpr_read_b32 %0, %1" : "=v"(xs[q]) : "a"(acc.a[q >> 2][j][q & 3]));
+        else
+          xs[q] = acc.v[(q >> 2) - kBlocksAgpr][j][q & 3];
+      }
+      auto x = [&](int q) { return xs[q]; };
       float m, s1, s2;
       if constexpr (kFull) {
         // every row is a token id: three-input maxima, exp2(z log2e - m log2e)
@@ -108,7 +114,7 @@ struct EpiProxy {
         for (int i = 0; i < kBlocksM; ++i)
 #pragma unroll
           for (int r = 0; r < kAccPerBlock; ++r)
-            if (vbase + i * 16 + r < V) m = fmaxf(m, acc_get(acc, i, j, r));
+            if (vbase + i * 16 + r < V) m = fmaxf(m, x(i * kAccPerBlock + r));
         m = fmaxf(m, __shfl_xor(m, 16));
         m = fmaxf(m, __shfl_xor(m, 32));
         s1 = 0.f;
@@ -120,7 +126,7 @@ struct EpiProxy {
             for (int r = 0; r < kAccPerBlock; ++r) {
               const int v = vbase + i * 16 + r;
               // the target's own entry is left out (selected away, not subtracted)
-              const float e = (v < V && v != tgt) ? __expf(acc_get(acc, i, j, r) - m) : 0.f;
+              const float e = (v < V && v != tgt) ? __expf(x(i * kAccPerBlock + r) - m) : 0.f;
               s1 += e;
               s2 += e * e;
             }
@@ -137,9 +143,6 @@ struct EpiProxy {
         o[2] = s2;
       }
     }
-#pragma unroll
-    for (int j = 0; j < kBlocksN; ++j)
-      if (has[j]) zt[tn * kTileN + acc_col(wn, j, lane)] = zvs[j];
     __syncthreads();
     const int c = threadIdx.x;
     const float* a = red + c * 3;
@@ -164,26 +167,6 @@ struct EpiProxy {
     }
   }
 };
-
-// ||h||^2 of each bf16 row, one wave per row (16-byte loads), float32 sums.
-__global__ __launch_bounds__(256) void row_sqnorm_kernel(const uint16_t* __restrict__ h, int N, int d,
-                                                         float* __restrict__ out) {
-  const int row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
-  if (row >= N) return;
-  const u32x4* p = reinterpret_cast<const u32x4*>(h + (int64_t)row * d);
-  float s = 0.f;
-  for (int c = lane; c < d / 8; c += 64) {
-    const u32x4 v = p[c];
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const float lo = __uint_as_float(v[k] << 16), hi = __uint_as_float(v[k] & 0xFFFF0000u);
-      s += lo * lo + hi * hi;
-    }
-  }
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o);
-  if (lane == 0) out[row] = s;
-}
 
 // Merge the vocabulary-tile partials of each token and form gamma, log p(o), ||p||^2.
 __global__ __launch_bounds__(256) void proxy_finalize_kernel(int N, int V, int ntv, int64_t ldp,
@@ -305,7 +288,7 @@ int pspo_score_proxy(const uint16_t* hidden, const uint16_t* w_head, const int32
     const int tiles_full = V / kTileM;
     if (tiles_full > 0) {
       GemmShape g{wk, pl.Vpad, tiles_full * kTileM, hk, pl.Npad, N, d, tiles_full, tiles_tok};
-      EpiProxy<true> e{V, N, pl.Npad, 0, target, part_m, part_s1, part_s2, zt};
+      EpiProxy<true> e{V, N, pl.Npad, 0, target, part_m, part_s1, part_s2};
       hipLaunchKernelGGL(gemm_nt_kernel<EpiProxy<true>>, dim3(gemm_grid(tiles_full, tiles_tok)), dim3(kGemmThreads),
                          0, stream, g, e);
       PSPO_HIP_CHECK(hipGetLastError());
@@ -313,13 +296,15 @@ int pspo_score_proxy(const uint16_t* hidden, const uint16_t* w_head, const int32
     if (tiles_full < tiles_voc) {
       GemmShape g{wk + (int64_t)tiles_full * kTileM * kTileK, pl.Vpad, V - tiles_full * kTileM, hk, pl.Npad, N, d, 1,
                   tiles_tok};
-      EpiProxy<false> e{V, N, pl.Npad, tiles_full, target, part_m, part_s1, part_s2, zt};
+      EpiProxy<false> e{V, N, pl.Npad, tiles_full, target, part_m, part_s1, part_s2};
       hipLaunchKernelGGL(gemm_nt_kernel<EpiProxy<false>>, dim3(gemm_grid(1, tiles_tok)), dim3(kGemmThreads), 0,
                          stream, g, e);
       PSPO_HIP_CHECK(hipGetLastError());
     }
   }
-  hipLaunchKernelGGL(row_sqnorm_kernel, dim3((unsigned)((N + 3) / 4)), dim3(256), 0, stream, hidden, N, d, hn);
+  // the target logit and ||h||^2 of every token, one pass over its hidden row
+  hipLaunchKernelGGL(row_dots_kernel, dim3((unsigned)((N + 3) / 4)), dim3(256), 0, stream, hidden, w_head, d, V, N,
+                     nullptr, target, nullptr, zt, hn);
   PSPO_HIP_CHECK(hipGetLastError());
   hipLaunchKernelGGL(proxy_finalize_kernel, dim3((unsigned)((N + 255) / 256)), dim3(256), 0, stream, N, V,
                      tiles_voc, pl.Npad, part_m, part_s1, part_s2, zt, hn, target, gamma, logp, p_sq, err_flag);
