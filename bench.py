@@ -53,13 +53,18 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "loss_fwd_bwd_qwen7b_traffic.json"
 
 
 def source_hash():
-    """Digest of the HIP/C++ sources of libpspo (identifies the kernels counters were taken on)."""
+    """Digest of the HIP/C++ sources of libpspo with comments and whitespace removed
+    (identifies the kernels counters were taken on; a comment edit changes no kernel)."""
     import hashlib
+    import re
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2606_29758_amd", "csrc")
     for name in sorted(os.listdir(csrc)):
-        with open(os.path.join(csrc, name), "rb") as f:
-            h.update(name.encode() + f.read())
+        with open(os.path.join(csrc, name), encoding="utf-8") as f:
+            text = f.read()
+        text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+        text = re.sub(r"//[^\n]*", " ", text)
+        h.update(name.encode() + " ".join(text.split()).encode())
     return h.hexdigest()[:16]
 
 

@@ -14,7 +14,8 @@
 //      layout of the matrix-core products);
 //   2. forward product z^T = W H^T in 384 x 256 tiles; the epilogue reduces
 //      each tile column (one token) to a partial (max, sum exp) over the tile's
-//      384 vocabulary rows and picks up the target logit;
+//      384 vocabulary rows; the target logits come from a one-wave-per-row
+//      dot product W[o] . h;
 //   3. finalize: merge the partials into lse, then l, rho, the clip mask, delta
 //      and a deterministic float64 loss reduction;
 //   4. K-blocked copies of the backward tokens' hidden rows and of their
@@ -24,8 +25,9 @@
 //      Delta = delta (e_o - exp(z - lse)) of the chunk in both layouts
 //      ([Npad x Vc] and [Vc x Npad]), then dW[chunk] = Delta^T H and
 //      dH += Delta W[chunk] as two more matrix-core products.  The first
-//      chunk's fp32 logits are kept by the forward (one chunk, the size of the
-//      Delta buffers), so its Delta is a memory-bound conversion; the other
+//      chunk's logits are kept by the forward (one chunk, as fp16 offsets from
+//      each tile's per-column maximum), so its Delta is a memory-bound
+//      conversion; the other
 //      chunks recompute their logit tiles on the matrix cores (every chunk
 //      does with PSPO_RECOMPUTE_LOGITS).
 #include <cmath>
