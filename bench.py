@@ -260,7 +260,7 @@ def bench_proxy(args):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1",
+        print(json.dumps({"error": "this implementation runs on one GPU only (no multi-GPU path); --gpus must be 1",
                           "n_gpus_requested": args.gpus}), flush=True)
         sys.exit(2)
     if args.copy_calibration:
