@@ -17,7 +17,7 @@ from oracle import ppo_head as ohead
 from paper_2606_29758_amd import pipeline, pspo, synth
 
 from parity_util import (GRAD_REL_L2, LOGP_ATOL, LOSS_RTOL, ambiguous_clip, f32, logp_old_for,
-                         oracle_loss, oracle_sample_pack, rel_l2)
+                         oracle_logp_old, oracle_loss, oracle_sample_pack, rel_l2)
 
 pytestmark = pytest.mark.gpu
 
@@ -34,6 +34,9 @@ MINI = {
                               data_seed=41),
     "odd_chunks": synth.custom("odd_chunks", "qwen7b", V=100003, P=2, K=3, length_law=("uniform", 60, 160),
                                data_seed=49),
+    # the 7B width and vocabulary with short completions (the oracle's logp_old of a rescaled head
+    # is recomputed per test)
+    "short7b": synth.custom("short7b", "qwen7b", P=2, K=2, length_law=("uniform", 40, 90), data_seed=33),
 }
 _CACHE = {}
 
@@ -224,6 +227,42 @@ def test_kept_logits_match_recompute(name, want_logp):
     for out in (ka, b):
         assert rel_l2(_to_np(out["d_hidden"]), ref["d_hidden"]) <= GRAD_REL_L2
         assert rel_l2(_to_np(out["d_w_head"]), ref["d_w"]) <= GRAD_REL_L2
+
+
+def _scaled_w(wl, k):
+    """The same workload with W multiplied by 2^k (exact in bf16, so the logits are exactly
+    2^k times larger); logp_old recomputed by the oracle for the new head."""
+    f = (wl.w_bits.astype(np.uint32) << 16).view(np.float32) * np.float32(2.0 ** k)
+    wl2 = synth.Workload(**{**wl.__dict__, "w_bits": (f.view(np.uint32) >> 16).astype(np.uint16)})
+    return wl2, oracle_logp_old(wl2)
+
+
+@pytest.mark.parametrize("name,k,seed", [("tiny", 7, 0), ("short7b", 4, 3)])
+def test_large_logits(name, k, seed):
+    """Logits of standard deviation ~20-30 (W scaled by 2^k): peaked softmax rows, targets
+    dozens of nats below the tile maxima, kept fp16 offsets far into their coarse range.
+    The default path (kept first chunk) and the recompute path both match the oracle, agree
+    with each other to ~1e-4 on the gradients, and bitwise on loss and log-probs."""
+    wl, _ = _workload(name)
+    wl, lp = _scaled_w(wl, k)
+    cfg = wl.cfg
+    step = pipeline.Step(pipeline.upload(wl, lp))
+    out = step(seed=seed)
+    ka = {key: out[key].clone() for key in ("loss", "d_hidden", "d_w_head", "logp_new", "stats")}
+    torch.cuda.synchronize()
+    H, pk = oracle_sample_pack(wl, lp, seed)
+    ref = oracle_loss(wl, pk)
+    assert not ambiguous_clip(ref, cfg.eps_low, cfg.eps_high).any()
+    assert np.median(ref["logp_new"]) < -10.0   # the regime this test is for
+    _compare_loss(ka, ref)
+    pkg = step.sample_and_pack(seed)
+    N = int(pkg["n_tokens"].item())
+    b = step.loss(pkg, N, flags=pspo.PSPO_RECOMPUTE_LOGITS)
+    torch.cuda.synchronize()
+    assert torch.equal(ka["loss"], b["loss"]) and torch.equal(ka["logp_new"], b["logp_new"])
+    for key in ("d_hidden", "d_w_head"):
+        assert rel_l2(_to_np(ka[key]), _to_np(b[key]).astype(np.float64)) <= 1e-3, key
+    assert int(step.err.item()) == 0
 
 
 def test_deterministic():
