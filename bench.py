@@ -26,9 +26,11 @@ gradient products over every token would need for the same throughput.
 cutoff draws: that mean must equal one weighted full-trajectory call (the
 estimator is linear in the keep indicators), and its distance from the plain
 full update is reported next to the paper's diagonal variance prediction.
-`recompute_logits_control` times the same loss calls with PSPO_RECOMPUTE_LOGITS
-(the backward recomputes every logit tile instead of converting the first
-vocabulary chunk's logits that the forward kept), and `mfma_loop_peak` is the
+The headline path stores no logit at all (the backward recomputes every logit
+tile).  `keep_logits_control` times the same loss calls with the opt-in
+PSPO_KEEP_LOGITS (the forward keeps the first vocabulary chunk's logits as
+fp16 offsets and the backward converts them instead of recomputing that
+chunk: less matrix-core work for Vc x N x 2 bytes of workspace), and `mfma_loop_peak` is the
 matrix cores' sustained bf16 rate on the products' MFMA form with no memory
 traffic (the ceiling at the clock the chip holds, next to the published peak).
 `cpu_baseline` times the float64 CPU oracle on a bounded sample of the same step
@@ -80,8 +82,8 @@ def parse():
     ap.add_argument("--no-full-control", action="store_true",
                     help="skip the full-trajectory control on the same batch: its timing (every xi = 1) "
                          "and the reseed check")
-    ap.add_argument("--no-recompute-control", action="store_true",
-                    help="skip the timing of the same calls with PSPO_RECOMPUTE_LOGITS (profiling runs)")
+    ap.add_argument("--no-keep-control", action="store_true",
+                    help="skip the timing of the same calls with PSPO_KEEP_LOGITS (profiling runs)")
     ap.add_argument("--no-mfma-peak", action="store_true",
                     help="skip the matrix-core rate probe (profiling runs)")
     ap.add_argument("--reseeds", type=int, default=64,
@@ -143,6 +145,43 @@ def cpu_baseline(wl, logp_old, ntok, seed):
             "single_core": {"value": n1 / dt1, "unit": "prefix tokens/s",
                             "sample": f"loss + gradients of the first {n1} packed tokens on one BLAS thread "
                                       f"({dt1:.1f} s)"}}
+
+
+def reseed_summary(dw, res):
+    """Scalars of a pipeline.reseed_mean result (a report of the benchmark, not a step of the path).
+
+    identity: how far the S-draw mean is from the weighted full call (rounding only):
+    loss relative error, dW and dH relative L2 errors.  mean_vs_full: the relative
+    distance of the mean dW from the full update G, and App. C's diagonal prediction of
+    it, sqrt(sum_t (1/xi_t - 1) ||g_t||^2 / S) / ||G||, with ||g_t||^2 = delta_t^2 ||h_t||^2
+    ||e_o - p_t||^2 = delta_t^2 gamma_t (gamma from the score proxy, delta_t the token's
+    logit-gradient scale at weight 1, from the full call's log-probs).  Needs
+    res['logp_full'] (reseed_mean(..., want_logp=True)).
+    """
+    import torch
+    from paper_2606_29758_amd import pspo
+    f32 = lambda x: float(np.float32(x))
+    rel = lambda a, b: float(torch.linalg.vector_norm((a - b).double()) / torch.linalg.vector_norm(b.double()))
+    S = res["seeds"]
+    total = res["tokens"]
+    G = res["full_dw"]
+    gamma = pspo.score_proxy(dw.hidden_full, dw.w_head, dw.target_full, total, want_logp=False)["gamma"].double()
+    rho = torch.exp(res["logp_full"].double() - dw.logp_old_full[:total].double())
+    seq = torch.repeat_interleave(torch.arange(dw.P * dw.K, device=G.device), dw.lengths.long())
+    A = dw.advantage.double()[seq]
+    mu = ((A > 0) & (rho <= 1 + f32(dw.eps_high))) | ((A < 0) & (rho >= 1 - f32(dw.eps_low)))
+    delta = -f32(dw.loss_scale) * mu.double() * rho * A
+    var = torch.sum((res["weight_full"].double() - 1.0) * delta ** 2 * gamma) / S
+    return {
+        "seeds": S,
+        "tokens": total,
+        "identity": {"loss_rel": abs(res["mean_loss"] - res["weighted_loss"]) / abs(res["weighted_loss"]),
+                     "dw_rel_l2": rel(res["mean_dw"], res["weighted_dw"]),
+                     "dh_rel_l2": rel(res["mean_dh"], res["weighted_dh"])},
+        "mean_vs_full": {"dw_rel_dev": rel(res["mean_dw"], G),
+                         "app_c_diagonal_prediction": float(torch.sqrt(var) / torch.linalg.vector_norm(G.double())),
+                         "loss_mean": res["mean_loss"], "loss_full": res["full_loss"]},
+    }
 
 
 def mfma_loop_peak(iters=32768, blocks=1024):
@@ -315,21 +354,23 @@ def main():
     pack_avg = float(np.mean([a.elapsed_time(b) for a, b in pack_marks]))
     assert int(step.err.item()) == 0, "device error flag raised"
     peak_bytes = torch.cuda.max_memory_allocated()
+    ws_bytes = int(step.workspace.numel())
 
-    # the same loss calls with every logit tile recomputed in the backward
-    # (PSPO_RECOMPUTE_LOGITS: no logits stored at all, a smaller workspace)
-    recompute_ms = None
-    if not args.no_recompute_control:
-        step.loss(pk, N, flags=pspo.PSPO_RECOMPUTE_LOGITS, want_logp=False)
+    # the same loss calls with the opt-in PSPO_KEEP_LOGITS (the first vocabulary
+    # chunk's logits kept by the forward as fp16 offsets, converted by the backward)
+    keep = None
+    if not args.no_keep_control:
+        step.loss(pk, N, flags=pspo.PSPO_KEEP_LOGITS, want_logp=False)
         torch.cuda.synchronize()
         rs, re_ = ev(), ev()
         nrep = max(3, args.steps // 2)
         rs.record(stream)
         for _ in range(nrep):
-            step.loss(pk, N, flags=pspo.PSPO_RECOMPUTE_LOGITS, want_logp=False)
+            step.loss(pk, N, flags=pspo.PSPO_KEEP_LOGITS, want_logp=False)
         re_.record(stream)
         torch.cuda.synchronize()
-        recompute_ms = rs.elapsed_time(re_) / nrep
+        keep = {"loss_call_ms": rs.elapsed_time(re_) / nrep,
+                "workspace_bytes": int(pspo.loss_workspace_bytes(N, cfg.d, cfg.V, pspo.PSPO_KEEP_LOGITS))}
     mfma_peak = None if args.no_mfma_peak else mfma_loop_peak()
 
     # the full-trajectory control on the same batch (every xi = 1: the standard, untruncated
@@ -359,7 +400,7 @@ def main():
     if not args.no_full_control and args.reseeds > 0:
         t0 = time.perf_counter()
         res = pipeline.reseed_mean(step, range(args.reseeds), want_logp=True)
-        reseed = pipeline.reseed_summary(dw, res)
+        reseed = reseed_summary(dw, res)
         del res
         torch.cuda.synchronize()
         reseed["seconds"] = time.perf_counter() - t0
@@ -411,14 +452,14 @@ def main():
         "loss_call_ms": loss_avg,
         "sample_pack_ms": pack_avg,
         "memory": {"peak_device_bytes": int(peak_bytes),
-                   "loss_workspace_bytes": int(step.workspace.numel()),
+                   "loss_workspace_bytes": ws_bytes,
                    "logits_fp32_bytes_avoided": int(N) * int(cfg.V) * 4},
         "pct_bf16_peak": 100.0 * achieved / PEAK_BF16_TFLOPS,
         "dense_equivalent_tflops": dense_equiv,
         "roofline": {
             "bound": "mfma",
-            "kernel": "pspo_loss_fwd_bwd (forward, logit-gradient, dW and dH bf16 MFMA kernels; the first "
-                      "vocabulary chunk's logit gradient converted from the forward's kept logits)",
+            "kernel": "pspo_loss_fwd_bwd (forward, logit-gradient recompute, dW and dH bf16 MFMA kernels; "
+                      "no logit stored)",
             "flops": "(2 n_fwd + 4 n_bwd) V d per call: forward over the tokens of completions with "
                      "A != 0, dH and dW over the tokens with a nonzero logit gradient",
             "achieved": achieved,
@@ -428,13 +469,11 @@ def main():
             "traffic": traffic,
         },
     }
-    if recompute_ms is not None:
-        result["recompute_logits_control"] = {
-            "loss_call_ms": recompute_ms,
-            "pct_bf16_peak": 100.0 * flops / (recompute_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
-            "what": "the same calls with PSPO_RECOMPUTE_LOGITS: every logit tile recomputed in the "
-                    "backward, no logits stored",
-        }
+    if keep is not None:
+        result["keep_logits_control"] = dict(
+            keep, pct_bf16_peak=100.0 * flops / (keep["loss_call_ms"] * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
+            what="the same calls with PSPO_KEEP_LOGITS: the first vocabulary chunk's logits kept by the "
+                 "forward (fp16 offsets, Vc x N x 2 bytes) and converted instead of recomputed")
     if mfma_peak is not None:
         result["mfma_loop_peak"] = mfma_peak
     if full is not None:

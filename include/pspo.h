@@ -54,15 +54,19 @@ typedef enum {
 #define PSPO_DEVERR_BAD_XI   2  /* a xi value outside (0,1] or an increase along t */
 #define PSPO_DEVERR_CAPACITY 4  /* sum of cutoffs exceeds `capacity`; nothing past it is written */
 #define PSPO_DEVERR_SEQ_ID   8  /* a seq_id outside [0, R); that token's loss and gradient are 0 */
+#define PSPO_DEVERR_NONFINITE 16 /* pspo_loss_fwd_bwd: a non-finite lse, ratio, loss term or delta in a token
+                                    whose loss term is computed (e.g. a NaN or Inf hidden row, head row, old
+                                    log-prob or weight); the loss and gradients are then not finite either */
 
 /* Flags of pspo_loss_fwd_bwd. */
 #define PSPO_ACCUMULATE_DW   1u /* d_w_head += gradient instead of d_w_head = gradient */
-#define PSPO_RECOMPUTE_LOGITS 2u /* recompute every logit tile in the backward instead of keeping the
-                                    first vocabulary chunk's logits from the forward (as fp16 offsets
-                                    from each tile's per-column maximum): the same loss, log-probs and
-                                    stats (bitwise), gradients that differ by ~1e-4 relative (the fp16
-                                    rounding of the kept offsets), a smaller workspace (by Vc x Npad x 2
-                                    bytes), more matrix-core work */
+#define PSPO_KEEP_LOGITS     4u /* opt-in trade of memory for matrix-core work: the forward keeps the
+                                    logits of the first vocabulary chunk (Vc x N of them, as fp16 offsets
+                                    from each 384-row tile's per-column maximum) and the backward converts
+                                    them instead of recomputing that chunk's logit tiles.  The same loss,
+                                    log-probs and stats (bitwise), gradients within ~1e-5 relative (the
+                                    fp16 rounding of the kept offsets), a workspace larger by Vc x Npad x 2
+                                    bytes.  Without it no logit is ever stored.  (Bit 2 is retired.) */
 
 /* Human-readable name of a status code (static storage). */
 const char* pspo_status_string(int status);
@@ -166,24 +170,27 @@ size_t pspo_loss_workspace_bytes(int32_t N, int32_t d, int32_t V, uint32_t flags
  *             (A > 0 and rho <= 1+eps_high, or A < 0 and rho >= 1-eps_low);
  *   G_i     = delta_i (e_{o_i} - softmax(z_i))     (App. D: grad log p(o) = (e_o - p) h^T)
  *   d_hidden[i] = G_i W,   d_w_head = sum_i G_i^T h_i.
- * The [N, V] logits are never written to memory whole: the workspace holds
- * per-token softmax statistics, one vocabulary chunk of bf16 logit gradients
- * (in two layouts) and the logits of the first chunk (fp16 offsets from each
- * 384-row tile's per-column maximum), kept by the forward so that the backward
- * recomputes the logit tiles of the other chunks only.
+ * The [N, V] logits are never written to memory: the forward keeps per-token
+ * softmax statistics only, and the backward recomputes the logit tiles one
+ * vocabulary chunk at a time.  G is applied in two parts: -delta_i p_i as one
+ * chunk of bf16 values at a time (in two layouts) through the matrix cores,
+ * and the one-hot part delta_i e_{o_i} in float32 (d_hidden[i] += delta_i W[o_i];
+ * d_w_head[v] += sum_{i : o_i = v} delta_i h_i, each row's terms summed in token
+ * order), so the largest entry of each row of G is never rounded to bf16.
  * The chunk is Vc = 384 * 256 / gcd(ceil(d / 256), 256) vocabulary rows (the
- * whole padded vocabulary if that is smaller); 49152 at d = 3584.
+ * whole padded vocabulary if that is smaller); 49152 at d = 3584.  Every
+ * result is deterministic (no floating-point atomics).
  *
  *  hidden     device, bf16 bits [N, d] row-major (packed prefix tokens).
  *  w_head     device, bf16 bits [V, d] row-major.
  *  target     device, int32 [N]; logp_old, weight: device float32 [N];
  *  seq_id     device, int32 [N] in [0, R);  advantage: device float32 [R].
- *  N >= 0, R >= 1 if N > 0, V >= 1, d > 0 with d % 64 == 0.  All device
+ *  N >= 0, R >= 1 if N > 0, V >= 1, d > 0 with d % 8 == 0.  All device
  *  pointers 16-byte aligned.
  *  eps_low, eps_high in [0, 1); loss_scale finite (e.g. 1/(P*K)).
- *  flags      PSPO_ACCUMULATE_DW | PSPO_RECOMPUTE_LOGITS or 0.
+ *  flags      PSPO_ACCUMULATE_DW | PSPO_KEEP_LOGITS or 0.
  *  loss       device, float64 [1] out.
- *  d_hidden   device, float32 [N, d] out.
+ *  d_hidden   device, float32 [>= N rows, d] out (rows 0 .. N-1 written).
  *  d_w_head   device, float32 [V, d] out (or accumulated, see flags).
  *  logp_new   device, float32 [N] out, or NULL.  When NULL, the forward
  *             computes logits only for the tokens of completions with A != 0:
@@ -195,7 +202,8 @@ size_t pspo_loss_workspace_bytes(int32_t N, int32_t d, int32_t V, uint32_t flags
  *             of tokens enters the backward products: every other token has
  *             delta_i = 0, hence a zero row of G, a zero d_hidden row and no
  *             d_w_head term, so skipping it is exact.
- *  err_flag   device, int32 [1] or NULL (PSPO_DEVERR_TARGET, PSPO_DEVERR_SEQ_ID).
+ *  err_flag   device, int32 [1] or NULL (PSPO_DEVERR_TARGET, PSPO_DEVERR_SEQ_ID,
+ *             PSPO_DEVERR_NONFINITE).
  *  workspace  device, >= pspo_loss_workspace_bytes(N, d, V, flags) bytes,
  *             256-byte aligned; its contents on entry are ignored.
  * N = 0 is valid: loss = 0 and d_w_head is zeroed (unless accumulating).
@@ -227,7 +235,7 @@ size_t pspo_score_proxy_workspace_bytes(int32_t N, int32_t d, int32_t V);
  *
  *  hidden     device, bf16 bits [N, d] row-major; w_head: device, bf16 bits [V, d].
  *  target     device, int32 [N]: the generated token of each row.
- *  N >= 0, V >= 1, d > 0 with d % 64 == 0; device pointers 16-byte aligned.
+ *  N >= 0, V >= 1, d > 0 with d % 8 == 0; device pointers 16-byte aligned.
  *  gamma      device, float32 [N] out.
  *  logp       device, float32 [N] out, or NULL: log p_i(o_i) (the old-policy
  *             log-probs the update later consumes).
@@ -318,13 +326,19 @@ int pspo_design_cutoffs(const double* w, const int64_t* xi_off, int32_t P, int64
                         void* workspace, size_t workspace_bytes, int32_t* err_flag,
                         hipStream_t stream);
 
+/* ------------------------------------------------------------------------
+ * Measurement entry point.  Not a step of the method and not used by any
+ * call above: it exists so that a benchmark can report the sustained
+ * matrix-core rate next to the products' achieved rate.
+ * ------------------------------------------------------------------------ */
+
 /*
- * Measurement helper, not a step of the method: `blocks` work-groups of 256
- * threads each run `iters` rounds of 16 independent v_mfma_f32_16x16x32_bf16
- * per wave (the block form and tied accumulators of the loss products, random
- * bf16 operands alternating between consecutive MFMAs), with
- * no memory traffic, so that a caller timing it with stream events gets the
- * sustained bf16 matrix-core rate: blocks * 4 * iters * 16 * 16384 flops.
+ * `blocks` work-groups of 256 threads each run `iters` rounds of 16
+ * independent v_mfma_f32_16x16x32_bf16 per wave (the block form and tied
+ * accumulators of the loss products, random bf16 operands alternating between
+ * consecutive MFMAs), with no memory traffic, so that a caller timing it with
+ * stream events gets the sustained bf16 matrix-core rate:
+ * blocks * 4 * iters * 16 * 16384 flops.
  *  iters, blocks  >= 1.
  *  out            device, float32 [blocks * 256], written (values meaningless).
  */

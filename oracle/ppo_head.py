@@ -117,3 +117,51 @@ def loss_fwd_bwd(hidden, w, target, logp_old, weight, seq_id, advantage,
     loss = -loss_scale * float(np.sum(c * surr))
     return dict(loss=loss, d_hidden=dH, d_w=dW, logp_new=logp, lse=lse, rho=rho, mu=mu,
                 delta=delta, surrogate=surr, abs_mass=loss_scale * float(np.sum(np.abs(c * surr))))
+
+
+def loss_terms(logp, logp_old, weight, seq_id, advantage, eps_low: float, eps_high: float, loss_scale: float):
+    """The per-token PPO terms and the loss from given log-probs (the part of
+    loss_fwd_bwd after the log-softmax): rho = exp(l - l_old) (Sec. 3.1 ratio),
+    s = min(rho A, clip(rho) A) (Sec. 3.1 objective), loss = -loss_scale sum c s
+    (Sec. 3.2 / 3.3 reweighted estimator), mu and delta = -loss_scale c mu rho A.
+    Lets a caller form the exact loss of a large batch from stored log-probs."""
+    l = np.asarray(logp, dtype=np.float64)
+    lo = np.asarray(logp_old, dtype=np.float64)
+    c = np.asarray(weight, dtype=np.float64)
+    A = np.asarray(advantage, dtype=np.float64)[np.asarray(seq_id, dtype=np.int64)]
+    rho = np.exp(l - lo)
+    s = np.minimum(rho * A, np.clip(rho, 1.0 - eps_low, 1.0 + eps_high) * A)
+    mu = (((A > 0) & (rho <= 1.0 + eps_high)) | ((A < 0) & (rho >= 1.0 - eps_low))).astype(np.float64)
+    delta = -loss_scale * c * mu * rho * A
+    return dict(rho=rho, mu=mu, delta=delta, surrogate=s, loss=-loss_scale * float(np.sum(c * s)),
+                abs_mass=loss_scale * float(np.sum(np.abs(c * s))))
+
+
+def target_logits(hidden, w, target, chunk: int = 4096) -> np.ndarray:
+    """z_{i, o_i} = W[o_i] . h_i in float64 (App. D logits at the sampled token)."""
+    target = np.asarray(target, dtype=np.int64)
+    out = np.empty(len(target))
+    for s in range(0, len(target), chunk):
+        e = min(len(target), s + chunk)
+        out[s:e] = np.einsum("ij,ij->i", as_f64(hidden[s:e]), as_f64(w[target[s:e]]))
+    return out
+
+
+def grad_w_rows(hidden, w, target, lse, delta, rows, chunk: int = 4096) -> np.ndarray:
+    """Selected rows of dW = sum_i G_i^T h_i with G_{i,v} = delta_i (1[v = o_i] - exp(z_{i,v} - lse_i))
+    (App. D head score times dL/dl_i), given every token's lse and delta: O(N d) per row, so
+    rows of a large batch can be checked without its [N, V] logits."""
+    rows = np.asarray(rows, dtype=np.int64)
+    target = np.asarray(target, dtype=np.int64)
+    lse = np.asarray(lse, dtype=np.float64)
+    delta = np.asarray(delta, dtype=np.float64)
+    Wr = as_f64(np.asarray(w)[rows])                      # [R, d]
+    out = np.zeros((len(rows), Wr.shape[1]))
+    for s in range(0, len(target), chunk):
+        e = min(len(target), s + chunk)
+        h = as_f64(hidden[s:e])
+        z = h @ Wr.T                                        # [c, R]
+        G = -delta[s:e, None] * np.exp(z - lse[s:e, None])
+        G += delta[s:e, None] * (target[s:e, None] == rows[None, :])
+        out += G.T @ h
+    return out

@@ -49,7 +49,7 @@ const char* pspo_status_string(int status) {
 
 const char* pspo_last_error(void) { return pspo::g_last_error.c_str(); }
 
-int pspo_abi_version(void) { return 4; }
+int pspo_abi_version(void) { return 5; }
 
 int pspo_validate_xi_host(const double* xi, const int64_t* xi_off, int32_t P) {
   using pspo::fail;

@@ -10,20 +10,25 @@ namespace pspo {
 namespace {
 
 // K-blocked copies of (selected) bf16 rows, in one pass over the source.
-// Row t of the copy is row idx[t] (or t) of the row-major `src` (cols columns,
-// a multiple of 64) for t < n, where n = min(rows, *n_dev) (or rows), and zero
-// for n <= t.  With n_dev, 32-row blocks at or past the next multiple of
-// kTileLcm above n are not written (no product reads them).
+// Row t of the copy is row idx[t] (or t) of the row-major `src` (row stride
+// ld_src elements, `cols` columns, cols % 8 == 0) for t < n, where
+// n = min(rows, *n_dev) (or rows), and zero for n <= t.  Columns cols ..
+// round_up(cols, 64) - 1 of the copy are zero (the K padding the products
+// need).  With n_dev, 32-row blocks at or past the next multiple of kTileLcm
+// above n are not written (no product reads them).
 //   dst_kb (if not NULL): the rows K-blocked with R_kb rows per K block:
 //     element (t, c) at ((c / 32) * R_kb + t) * 32 + c % 32;
 //   dst_t (if not NULL): their transpose, in blocks of `chunk` rows (a
-//     multiple of 32), each K-blocked with R_t >= cols rows per K block:
-//     element (t, c) at (t / chunk) * R_t * chunk + (((t % chunk) / 32) * R_t + c) * 32 + t % 32
-//     (rows cols .. R_t-1 of each K block are left unwritten).
-// Grid (cols / 64, rows_pad / 32), 256 threads: a 32 x 64 tile, one 16-byte
-// piece per thread in and out; the transposed pieces go through LDS and are
-// written as whole 64-byte K rows (each output row of the tile is 32 source rows).
-__global__ __launch_bounds__(256) void kblock_rows_kernel(const uint16_t* __restrict__ src, int64_t ld_src, int rows,
+//     multiple of 32), each K-blocked with R_t >= round_up(cols, 64) rows per
+//     K block: element (t, c) at
+//     (t / chunk) * R_t * chunk + (((t % chunk) / 32) * R_t + c) * 32 + t % 32
+//     (rows round_up(cols, 64) .. R_t-1 of each K block are left unwritten).
+// Grid (ceil(cols / 64), rows_pad / 32), 256 threads: a 32 x 64 tile, one
+// 16-byte piece per thread in and out; the transposed pieces go through LDS
+// and are written as whole 64-byte K rows (each output row of the tile is 32
+// source rows).
+__global__ __launch_bounds__(256) void kblock_rows_kernel(const uint16_t* __restrict__ src, int64_t ld_src, int cols,
+                                                          int rows,
                                                           const int32_t* __restrict__ idx,
                                                           const int32_t* __restrict__ n_dev,
                                                           uint16_t* __restrict__ dst_kb, int64_t R_kb,
@@ -40,7 +45,7 @@ __global__ __launch_bounds__(256) void kblock_rows_kernel(const uint16_t* __rest
   {
     const int r = r0 + (tid >> 3), cp = (tid & 7) * 8;
     u32x4 v = {0u, 0u, 0u, 0u};
-    if (r < n) {
+    if (r < n && c0 + cp < cols) {   // an 8-column piece lies wholly inside or outside (cols % 8 == 0)
       const int64_t s = idx != nullptr ? idx[r] : r;
       v = *reinterpret_cast<const u32x4*>(src + s * ld_src + c0 + cp);
     }

@@ -21,15 +21,23 @@
 //   4. K-blocked copies of the backward tokens' hidden rows and of their
 //      transpose H^T [d x Npad] (K-contiguous operands of the gradient
 //      products);
-//   5. per vocabulary chunk of Vc rows: the bf16 logit gradient
-//      Delta = delta (e_o - exp(z - lse)) of the chunk in both layouts
-//      ([Npad x Vc] and [Vc x Npad]), then dW[chunk] = Delta^T H and
-//      dH += Delta W[chunk] as two more matrix-core products.  The first
-//      chunk's logits are kept by the forward (one chunk, as fp16 offsets from
-//      each tile's per-column maximum), so its Delta is a memory-bound
-//      conversion; the other
-//      chunks recompute their logit tiles on the matrix cores (every chunk
-//      does with PSPO_RECOMPUTE_LOGITS).
+//   5. per vocabulary chunk of Vc rows: the bf16 logit gradient without its
+//      target entries, Delta_{i,v} = -delta_i exp(z_{i,v} - lse_i) for
+//      v != o_i (0 at v = o_i), recomputed tile by tile on the matrix cores and
+//      stored in both layouts ([Npad x Vc] and [Vc x Npad]); then
+//      dW[chunk] = Delta^T H and dH += Delta W[chunk] as two more matrix-core
+//      products.  With PSPO_KEEP_LOGITS the forward keeps the first chunk's
+//      logits (fp16 offsets from each tile's per-column maximum) and a
+//      memory-bound conversion replaces that chunk's recompute;
+//   6. the target entries in float32, g_i = G_{i,o_i} = delta_i (1 - p_i(o_i))
+//      = -delta_i expm1(l_i): dH_i += g_i W[o_i], and
+//      dW[v] += sum_{i : o_i = v} g_i h_i with each row's terms summed in token
+//      order (a stable bucketing of the backward tokens by target; no
+//      floating-point atomics).  The target entry is the largest of its row
+//      when the softmax is flat and the result of a cancellation when it is
+//      peaked; carried in float32 it is rounded neither to 8 bits nor after a
+//      cancellation.
+#include <algorithm>
 #include <cmath>
 
 #include "common.h"
@@ -46,15 +54,16 @@ constexpr float kNegInf = -INFINITY;
 // Epilogues
 // ---------------------------------------------------------------------------
 
-// One entry of the logit gradient, delta (1[v = o] - exp(z - lse)) (the
-// objective of Sec. 3.1 differentiated through the log-softmax of App. D),
-// with lsb = lse log2(e): p = exp2(min(z log2(e) - lsb, 0)) (one fma; the min
-// keeps p <= 1 and finite for padding columns, whose delta is 0), then
-// delta [v = o] - delta p as one fma.  The recomputing product and the
+// One entry of the logit gradient delta (1[v = o] - exp(z - lse)) (the
+// objective of Sec. 3.1 differentiated through the log-softmax of App. D) away
+// from the target, -delta exp(z - lse), and 0 at the target (that entry is
+// added in float32 by the target-entry kernels), with lsb = lse log2(e):
+// p = exp2(min(z log2(e) - lsb, 0)) (one fma; the min keeps p <= 1 and finite
+// for padding columns, whose delta is 0).  The recomputing product and the
 // kept-logit conversion both use it, so they produce the same bits.
 __device__ __forceinline__ float logit_grad(float z, float lsb, float delta, bool is_target) {
   const float p = __builtin_amdgcn_exp2f(fminf(fmaf(z, kLog2e, -lsb), 0.f));
-  return fmaf(-delta, p, is_target ? delta : 0.f);
+  return is_target ? 0.f : -delta * p;
 }
 
 // Two floats as packed bf16 (round to nearest even): one v_cvt_pk_bf16_f32.
@@ -253,9 +262,9 @@ __device__ __forceinline__ u32x2 quad_transpose(u32x2 p, int k) {
   return o;
 }
 
-// Backward logit gradient for one vocabulary chunk: rows = vocabulary rows
-// v0 + vl (A = W[v0:]), columns = the compacted tokens that carry gradient
-// (column t is token tok[t], t < *n_dev).  Writes bf16 Delta in both K-blocked
+// Backward logit gradient (without its target entries) for one vocabulary chunk:
+// rows = vocabulary rows v0 + vl (A = W[v0:]), columns = the compacted tokens
+// that carry gradient (column t < *n_dev).  Writes bf16 Delta in both K-blocked
 // layouts (vocabulary rows for dW, token rows for dH); zero outside t < *n_dev,
 // v < V.  Straight from registers, as 16-byte stores of which each instruction
 // fills 16 whole 64-byte K rows (1 KB contiguous).  Blocks are taken two row
@@ -553,6 +562,11 @@ __global__ void fill_f32_kernel(float* __restrict__ p, int64_t n, float v) {
     p[i] = v;
 }
 
+__global__ void fill_i32_kernel(int32_t* __restrict__ p, int64_t n, int32_t v) {
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+    p[i] = v;
+}
+
 constexpr int kFinThreads = 256;
 constexpr int kCompactThreads = 256, kCompactPer = 8, kCompactSpan = kCompactThreads * kCompactPer;
 
@@ -748,6 +762,10 @@ __global__ __launch_bounds__(kFinThreads) void finalize_kernel(
       s = fminf(rho * A, clipped * A);
       mu = (A > 0.f && rho <= 1.f + eps_high) || (A < 0.f && rho >= 1.f - eps_low);
       dl = mu ? -loss_scale * c * rho * A : 0.f;
+      // a non-finite hidden row, head row, old log-prob or weight shows up in
+      // lse, rho, the loss term or delta (and would spread into the gradients)
+      if (err_flag && !(std::isfinite(lse) && std::isfinite(rho) && std::isfinite(c * s) && std::isfinite(dl)))
+        atomicOr(err_flag, PSPO_DEVERR_NONFINITE);
     } else if (!valid && err_flag) {
       atomicOr(err_flag, (tgt >= 0 && tgt < V) ? PSPO_DEVERR_SEQ_ID : PSPO_DEVERR_TARGET);
     }
@@ -877,22 +895,209 @@ struct TailDH {
 
 // Per backward column a < min(N, *n_dev) (token act[a]): its forward column
 // (where the kept logits sit), target, lse and delta, in column order, so the
-// backward kernels fetch a column's data in one contiguous round trip.
+// backward kernels fetch a column's data in one contiguous round trip; and the
+// target entry of its logit-gradient row, G_{o} = delta (1 - p(o)), as
+// -delta expm1(l) with l = z_o - lse the token's log-prob (no cancellation as
+// p(o) -> 1).  A backward token has delta != 0, hence a forward column.
 __global__ __launch_bounds__(256) void gather_backward_kernel(int N, const int32_t* __restrict__ n_dev,
                                                               const int32_t* __restrict__ act,
                                                               const int32_t* __restrict__ fpos,
                                                               const int32_t* __restrict__ target,
                                                               const float* __restrict__ lse,
                                                               const float* __restrict__ delta,
+                                                              const float* __restrict__ zt,
                                                               int32_t* __restrict__ afwd, int32_t* __restrict__ ctgt,
-                                                              float* __restrict__ clse, float* __restrict__ cdelta) {
+                                                              float* __restrict__ clse, float* __restrict__ cdelta,
+                                                              float* __restrict__ cg1) {
   const int n = min(N, *n_dev);
   for (int a = blockIdx.x * 256 + threadIdx.x; a < n; a += gridDim.x * 256) {
     const int t = act[a];
-    afwd[a] = fpos[t];
+    const int f = fpos[t];
+    afwd[a] = f;
     ctgt[a] = target[t];
     clse[a] = lse[t];
     cdelta[a] = delta[t];
+    cg1[a] = -delta[t] * expm1f(zt[f] - lse[t]);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Target entries of the logit gradient, g_i = G_{i,o_i} = delta_i (1 - p_i(o_i)),
+// in float32, after the chunked products that carried the other entries in bf16
+// ---------------------------------------------------------------------------
+
+// bf16 pair (one 32-bit word) to two floats, exactly.
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+
+// d_hidden[act[a]] += cg1[a] * W[ctgt[a]] for every backward column
+// a < min(N, *n_dev) (App. D: the target entry of the head score's row, times
+// that row of W).  One wave per column, 8 features per lane and step.
+// d % 8 == 0.
+// Grid ceil(N / 4), 256 threads.
+__global__ __launch_bounds__(256) void onehot_dh_kernel(int N, int d, const int32_t* __restrict__ n_dev,
+                                                        const int32_t* __restrict__ act,
+                                                        const int32_t* __restrict__ ctgt,
+                                                        const float* __restrict__ cg1,
+                                                        const uint16_t* __restrict__ w, float* __restrict__ dH) {
+  const int n = min(N, *n_dev);
+  const int a = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (a >= n) return;   // uniform over the wave
+  const float dl = cg1[a];
+  const u32x4* wr = reinterpret_cast<const u32x4*>(w + (int64_t)ctgt[a] * d);
+  f32x4* hr = reinterpret_cast<f32x4*>(dH + (int64_t)act[a] * d);
+  for (int c = lane; c < d / 8; c += 64) {
+    const u32x4 wv = wr[c];
+    f32x4 lo = hr[2 * c], hi = hr[2 * c + 1];
+    lo[0] = fmaf(dl, bf16_lo(wv[0]), lo[0]);
+    lo[1] = fmaf(dl, bf16_hi(wv[0]), lo[1]);
+    lo[2] = fmaf(dl, bf16_lo(wv[1]), lo[2]);
+    lo[3] = fmaf(dl, bf16_hi(wv[1]), lo[3]);
+    hi[0] = fmaf(dl, bf16_lo(wv[2]), hi[0]);
+    hi[1] = fmaf(dl, bf16_hi(wv[2]), hi[1]);
+    hi[2] = fmaf(dl, bf16_lo(wv[3]), hi[2]);
+    hi[3] = fmaf(dl, bf16_hi(wv[3]), hi[3]);
+    hr[2 * c] = lo;
+    hr[2 * c + 1] = hi;
+  }
+}
+
+// The dW side groups the backward columns by target id.  Stable bucketing in
+// four launches, every result independent of scheduling:
+//   count:  cnt[v] = #{a : ctgt[a] = v}                    (integer atomics)
+//   scan:   start[v] = sum_{u < v} cnt[u]; cursor = start;   the non-empty ids
+//           in increasing order in rows[0 .. *nrows)
+//   fill:   each column takes a slot of its bucket           (arbitrary order)
+//   rank:   column a goes to start[v] + #{b in bucket v : b < a} of `sorted`,
+//           i.e. the bucket in increasing column order.
+// The rank pass reads a column's whole bucket: O(sum_v cnt[v]^2) reads in all,
+// from a bucket that the waves sharing it read together (a few microseconds
+// for uniform targets; about a millisecond if every column had one target).
+__global__ __launch_bounds__(256) void onehot_count_kernel(int N, const int32_t* __restrict__ n_dev,
+                                                           const int32_t* __restrict__ ctgt,
+                                                           int32_t* __restrict__ cnt) {
+  const int n = min(N, *n_dev);
+  for (int a = blockIdx.x * 256 + threadIdx.x; a < n; a += gridDim.x * 256) atomicAdd(&cnt[ctgt[a]], 1);
+}
+
+constexpr int kScanThreads = 1024;
+
+// One work-group: thread k scans ids [k s, (k + 1) s), s = ceil(V / 1024), in
+// two passes (its own totals, then the outputs after a work-group scan of them).
+__global__ __launch_bounds__(kScanThreads) void onehot_scan_kernel(int V, const int32_t* __restrict__ cnt,
+                                                                   int32_t* __restrict__ start,
+                                                                   int32_t* __restrict__ cursor,
+                                                                   int32_t* __restrict__ rows,
+                                                                   int32_t* __restrict__ nrows) {
+  __shared__ int sh_c[kScanThreads], sh_r[kScanThreads];
+  const int tid = threadIdx.x;
+  const int span = (V + kScanThreads - 1) / kScanThreads;
+  const int v0 = min(V, tid * span), v1 = min(V, v0 + span);
+  int c = 0, r = 0;
+  for (int v = v0; v < v1; ++v) {
+    const int k = cnt[v];
+    c += k;
+    r += k > 0 ? 1 : 0;
+  }
+  sh_c[tid] = c;
+  sh_r[tid] = r;
+  __syncthreads();
+  for (int off = 1; off < kScanThreads; off <<= 1) {   // inclusive scans
+    const int ac = tid >= off ? sh_c[tid - off] : 0, ar = tid >= off ? sh_r[tid - off] : 0;
+    __syncthreads();
+    sh_c[tid] += ac;
+    sh_r[tid] += ar;
+    __syncthreads();
+  }
+  c = sh_c[tid] - c;
+  r = sh_r[tid] - r;
+  for (int v = v0; v < v1; ++v) {
+    const int k = cnt[v];
+    start[v] = c;
+    cursor[v] = c;
+    if (k > 0) rows[r++] = v;
+    c += k;
+  }
+  if (tid == kScanThreads - 1) *nrows = sh_r[kScanThreads - 1];
+}
+
+__global__ __launch_bounds__(256) void onehot_fill_kernel(int N, const int32_t* __restrict__ n_dev,
+                                                          const int32_t* __restrict__ ctgt,
+                                                          int32_t* __restrict__ cursor, int32_t* __restrict__ tmp) {
+  const int n = min(N, *n_dev);
+  for (int a = blockIdx.x * 256 + threadIdx.x; a < n; a += gridDim.x * 256) tmp[atomicAdd(&cursor[ctgt[a]], 1)] = a;
+}
+
+__global__ __launch_bounds__(256) void onehot_rank_kernel(int N, const int32_t* __restrict__ n_dev,
+                                                          const int32_t* __restrict__ ctgt,
+                                                          const int32_t* __restrict__ start,
+                                                          const int32_t* __restrict__ cnt,
+                                                          const int32_t* __restrict__ tmp,
+                                                          int32_t* __restrict__ sorted) {
+  const int n = min(N, *n_dev);
+  for (int a = blockIdx.x * 256 + threadIdx.x; a < n; a += gridDim.x * 256) {
+    const int v = ctgt[a], s = start[v], e = s + cnt[v];
+    int rank = 0;
+    for (int k = s; k < e; ++k) rank += tmp[k] < a ? 1 : 0;
+    sorted[s + rank] = a;
+  }
+}
+
+// dW[v] += sum over the bucket of v, in increasing column order, of
+// cg1[a] * h[act[a]] (App. D: the target entries of the head scores), the sum
+// accumulated in float32 and then added to the row.  One wave per non-empty
+// id rows[k], k < *nrows (<= the launch's row bound); 8 features per lane and
+// step, kOnehotSteps steps of the row per pass over the bucket.  d % 8 == 0.
+// Grid ceil(bound / 4), 256 threads.
+constexpr int kOnehotSteps = 8;   // 8 x 8 features per lane: 4096 of the row per pass over the bucket
+
+__global__ __launch_bounds__(256) void onehot_dw_kernel(int bound, int d, const int32_t* __restrict__ nrows,
+                                                        const int32_t* __restrict__ rows,
+                                                        const int32_t* __restrict__ start,
+                                                        const int32_t* __restrict__ cnt,
+                                                        const int32_t* __restrict__ sorted,
+                                                        const int32_t* __restrict__ act,
+                                                        const float* __restrict__ cg1,
+                                                        const uint16_t* __restrict__ hidden, float* __restrict__ dW) {
+  const int k = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (k >= min(bound, *nrows)) return;   // uniform over the wave
+  const int v = rows[k], s = start[v], e = s + cnt[v];
+  const int d8 = d / 8;
+  f32x4* out = reinterpret_cast<f32x4*>(dW + (int64_t)v * d);
+  for (int c0 = 0; c0 < d8; c0 += 64 * kOnehotSteps) {
+    f32x4 lo[kOnehotSteps], hi[kOnehotSteps];
+#pragma unroll
+    for (int q = 0; q < kOnehotSteps; ++q) lo[q] = hi[q] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int b = s; b < e; ++b) {
+      const int a = sorted[b];
+      const float dl = cg1[a];
+      const u32x4* hr = reinterpret_cast<const u32x4*>(hidden + (int64_t)act[a] * d);
+#pragma unroll
+      for (int q = 0; q < kOnehotSteps; ++q) {
+        const int c = c0 + q * 64 + lane;
+        if (c < d8) {
+          const u32x4 hv = hr[c];
+          lo[q][0] = fmaf(dl, bf16_lo(hv[0]), lo[q][0]);
+          lo[q][1] = fmaf(dl, bf16_hi(hv[0]), lo[q][1]);
+          lo[q][2] = fmaf(dl, bf16_lo(hv[1]), lo[q][2]);
+          lo[q][3] = fmaf(dl, bf16_hi(hv[1]), lo[q][3]);
+          hi[q][0] = fmaf(dl, bf16_lo(hv[2]), hi[q][0]);
+          hi[q][1] = fmaf(dl, bf16_hi(hv[2]), hi[q][1]);
+          hi[q][2] = fmaf(dl, bf16_lo(hv[3]), hi[q][2]);
+          hi[q][3] = fmaf(dl, bf16_hi(hv[3]), hi[q][3]);
+        }
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < kOnehotSteps; ++q) {
+      const int c = c0 + q * 64 + lane;
+      if (c < d8) {
+        out[2 * c] += lo[q];
+        out[2 * c + 1] += hi[q];
+      }
+    }
   }
 }
 
@@ -903,8 +1108,11 @@ __global__ __launch_bounds__(256) void gather_backward_kernel(int N, const int32
 
 struct Plan {
   int64_t Npad, Vpad, dpad, Vc, ntv, nfin;
-  int64_t off_pm, off_pl, off_zt, off_lse, off_delta, off_fidx, off_fpos, off_nfwd, off_idx, off_nact, off_afwd, off_ctgt, off_clse, off_cdelta, off_ftgt, off_cnt, off_blk, off_wk,
-      off_hk, off_ht, off_wt, off_dn, off_dt, off_slab, off_zk, total;
+  int64_t Dk;   // K of the products over the hidden features: d rounded up to 32 (zero padding)
+  int64_t off_pm, off_pl, off_zt, off_lse, off_delta, off_fidx, off_fpos, off_nfwd, off_idx, off_nact, off_afwd,
+      off_ctgt, off_clse, off_cdelta, off_cg1, off_ftgt, off_cnt, off_blk, off_wk, off_hk, off_ht, off_wt, off_dn, off_dt,
+      off_slab, off_zk, off_oh_cnt, off_oh_start, off_oh_cursor, off_oh_rows, off_oh_nrows, off_oh_tmp,
+      off_oh_sorted, total;
   bool keep;   // the forward keeps the first chunk's logits (fp16 offsets from the tile maxima)
 };
 
@@ -913,6 +1121,8 @@ Plan make_plan(int64_t N, int64_t d, int64_t V, bool keep) {
   p.Npad = round_up(N > 0 ? N : 1, kTileLcm);   // token rows: tiles of 256 (B side) and 384 (A side)
   p.Vpad = round_up(V, kTileM);
   p.dpad = round_up(d, kTileN);
+  p.Dk = round_up(d, kTileK);
+  const int64_t d64 = round_up(d, 64);   // columns the K-blocked copies write (64 per copy tile)
   // Vocabulary rows per backward chunk: a multiple of 384-row tiles such that
   // the dW product of a chunk ((Vc / 384) x ceil(d / 256) tiles of very long
   // K) fills whole rounds of the 256 CUs (d = 3584: 14 column tiles, 128 row
@@ -949,11 +1159,12 @@ Plan make_plan(int64_t N, int64_t d, int64_t V, bool keep) {
   p.off_ctgt = take(p.Npad * 4);                                      //   target, lse, delta
   p.off_clse = take(p.Npad * 4);
   p.off_cdelta = take(p.Npad * 4);
+  p.off_cg1 = take(p.Npad * 4);                                       //   and target entry of the gradient row
   p.off_ftgt = take(p.Npad * 4);                                      // forward columns: target
   p.off_cnt = take((p.Npad + kCompactSpan - 1) / kCompactSpan * 4);   // per-block counts of a compaction
   p.off_blk = take((p.nfin > 0 ? p.nfin : 1) * 5 * 8);
-  p.off_wk = take(d * p.Vpad * 2);                                    // W, K-blocked [d/32][Vpad][32]
-  p.off_hk = take(d * p.Npad * 2);                                    // gathered hidden rows [d/32][Npad][32]
+  p.off_wk = take(d64 * p.Vpad * 2);                                  // W, K-blocked [d64/32][Vpad][32]
+  p.off_hk = take(d64 * p.Npad * 2);                                  // gathered hidden rows [d64/32][Npad][32]
   p.off_ht = take(p.dpad * p.Npad * 2);                               // H[bwd]^T [Npad/32][dpad][32]
   p.off_wt = take(p.dpad * ((p.Vpad + p.Vc - 1) / p.Vc) * p.Vc * 2);  // per chunk: W^T [Vc/32][dpad][32]
   p.off_dn = take(p.Npad * p.Vc * 2);                                 // K-blocked [Vc/32][Npad][32]
@@ -961,6 +1172,13 @@ Plan make_plan(int64_t N, int64_t d, int64_t V, bool keep) {
   p.off_slab = take((int64_t)kNumXcd * kTailSlots * kTileM * kTileN * 4);   // K parts of tail tiles
   p.keep = keep;
   p.off_zk = take(keep ? p.Vc * p.Npad * 2 : 0);                      // kept fp16 logit offsets, one block per forward tile
+  p.off_oh_cnt = take(V * 4);                                         // one-hot part: backward columns per target id,
+  p.off_oh_start = take(V * 4);                                       //   bucket starts, fill cursors,
+  p.off_oh_cursor = take(V * 4);
+  p.off_oh_rows = take(V * 4);                                        //   non-empty ids and their count,
+  p.off_oh_nrows = take(4);
+  p.off_oh_tmp = take(p.Npad * 4);                                    //   buckets unordered, then in column order
+  p.off_oh_sorted = take(p.Npad * 4);
   p.total = o;
   return p;
 }
@@ -997,7 +1215,7 @@ extern "C" {
 
 size_t pspo_loss_workspace_bytes(int32_t N, int32_t d, int32_t V, uint32_t flags) {
   if (N < 0 || d <= 0 || V <= 0) return 0;
-  return (size_t)pspo::make_plan(N, d, V, (flags & PSPO_RECOMPUTE_LOGITS) == 0).total;
+  return (size_t)pspo::make_plan(N, d, V, (flags & PSPO_KEEP_LOGITS) != 0).total;
 }
 
 int pspo_loss_fwd_bwd(const uint16_t* hidden, const uint16_t* w_head, const int32_t* target, const float* logp_old,
@@ -1009,9 +1227,9 @@ int pspo_loss_fwd_bwd(const uint16_t* hidden, const uint16_t* w_head, const int3
   clear_last_error();
   PSPO_REQUIRE(N >= 0 && R >= 0, PSPO_ERR_INVALID_ARG, "N and R must be >= 0");
   PSPO_REQUIRE(d > 0 && V > 0, PSPO_ERR_INVALID_ARG, "d and V must be > 0");
-  PSPO_REQUIRE(d % 64 == 0, PSPO_ERR_UNSUPPORTED, "d must be a multiple of 64");
+  PSPO_REQUIRE(d % 8 == 0, PSPO_ERR_UNSUPPORTED, "d must be a multiple of 8");
   PSPO_REQUIRE(N == 0 || R > 0, PSPO_ERR_INVALID_ARG, "R must be > 0 when N > 0");
-  PSPO_REQUIRE((flags & ~(PSPO_ACCUMULATE_DW | PSPO_RECOMPUTE_LOGITS)) == 0, PSPO_ERR_INVALID_ARG,
+  PSPO_REQUIRE((flags & ~(PSPO_ACCUMULATE_DW | PSPO_KEEP_LOGITS)) == 0, PSPO_ERR_INVALID_ARG,
                "unknown flag bits");
   PSPO_REQUIRE(std::isfinite(eps_low) && eps_low >= 0.f && eps_low < 1.f, PSPO_ERR_INVALID_ARG,
                "eps_low must lie in [0, 1)");
@@ -1032,7 +1250,7 @@ int pspo_loss_fwd_bwd(const uint16_t* hidden, const uint16_t* w_head, const int3
                  "workspace must be non-NULL and 256-byte aligned");
   }
   if (stats) PSPO_REQUIRE(aligned(stats, 8), PSPO_ERR_INVALID_ARG, "misaligned stats");
-  const Plan pl = make_plan(N, d, V, (flags & PSPO_RECOMPUTE_LOGITS) == 0);
+  const Plan pl = make_plan(N, d, V, (flags & PSPO_KEEP_LOGITS) != 0);
   PSPO_REQUIRE(N == 0 || workspace_bytes >= (size_t)pl.total, PSPO_ERR_WORKSPACE,
                "workspace too small: need " + std::to_string(pl.total) + " bytes");
   PSPO_REQUIRE(pl.Npad <= INT32_MAX && pl.Vpad <= INT32_MAX, PSPO_ERR_UNSUPPORTED, "problem too large");
@@ -1066,6 +1284,7 @@ int pspo_loss_fwd_bwd(const uint16_t* hidden, const uint16_t* w_head, const int3
   int32_t* act_tgt = reinterpret_cast<int32_t*>(ws + pl.off_ctgt);
   float* act_lse = reinterpret_cast<float*>(ws + pl.off_clse);
   float* act_delta = reinterpret_cast<float*>(ws + pl.off_cdelta);
+  float* act_g1 = reinterpret_cast<float*>(ws + pl.off_cg1);
   int32_t* fwd_tgt = reinterpret_cast<int32_t*>(ws + pl.off_ftgt);
   double* blk = reinterpret_cast<double*>(ws + pl.off_blk);
   uint16_t* wk = reinterpret_cast<uint16_t*>(ws + pl.off_wk);
@@ -1076,12 +1295,20 @@ int pspo_loss_fwd_bwd(const uint16_t* hidden, const uint16_t* w_head, const int3
   uint16_t* dT = reinterpret_cast<uint16_t*>(ws + pl.off_dt);
   uint16_t* zk = pl.keep ? reinterpret_cast<uint16_t*>(ws + pl.off_zk) : nullptr;
   float* slab = reinterpret_cast<float*>(ws + pl.off_slab);
+  int32_t* oh_cnt = reinterpret_cast<int32_t*>(ws + pl.off_oh_cnt);
+  int32_t* oh_start = reinterpret_cast<int32_t*>(ws + pl.off_oh_start);
+  int32_t* oh_cursor = reinterpret_cast<int32_t*>(ws + pl.off_oh_cursor);
+  int32_t* oh_rows = reinterpret_cast<int32_t*>(ws + pl.off_oh_rows);
+  int32_t* oh_nrows = reinterpret_cast<int32_t*>(ws + pl.off_oh_nrows);
+  int32_t* oh_tmp = reinterpret_cast<int32_t*>(ws + pl.off_oh_tmp);
+  int32_t* oh_sorted = reinterpret_cast<int32_t*>(ws + pl.off_oh_sorted);
+  const int Dk = (int)pl.Dk;
 
   const int tiles_tok_n = (int)(pl.Npad / kTileN);    // tokens on the B side
   const int tiles_tok_m = (int)(pl.Npad / kTileM);    // tokens on the A side
   const int tiles_voc = (int)pl.ntv;
   const int tiles_d = (int)(pl.dpad / kTileN);
-  const unsigned ctiles64 = (unsigned)(d / 64);
+  const unsigned ctiles64 = (unsigned)((d + 63) / 64);
 
   // 1. the tokens whose logits are needed (all of them if logp_new is wanted);
   //    W and their hidden rows as K-blocked operands
@@ -1091,10 +1318,10 @@ int pspo_loss_fwd_bwd(const uint16_t* hidden, const uint16_t* w_head, const int3
   // W K-blocked (forward and logit-gradient products) and, per vocabulary
   // chunk, W[chunk]^T (dH product), in one pass over W
   hipLaunchKernelGGL(kblock_rows_kernel, dim3(ctiles64, (unsigned)(pl.Vpad / 32)), dim3(256), 0, stream, w_head,
-                     (int64_t)d, V, nullptr, nullptr, wk, pl.Vpad, wT, pl.dpad, pl.Vc);
+                     (int64_t)d, d, V, nullptr, nullptr, wk, pl.Vpad, wT, pl.dpad, pl.Vc);
   PSPO_HIP_CHECK(hipGetLastError());
   hipLaunchKernelGGL(kblock_rows_kernel, dim3(ctiles64, (unsigned)(pl.Npad / 32)), dim3(256), 0, stream, hidden,
-                     (int64_t)d, N, fwd_idx, n_fwd, hk, pl.Npad, nullptr, (int64_t)0, (int64_t)kTileK);
+                     (int64_t)d, d, N, fwd_idx, n_fwd, hk, pl.Npad, nullptr, (int64_t)0, (int64_t)kTileK);
   PSPO_HIP_CHECK(hipGetLastError());
   // 2. forward logits -> per-tile softmax partials (target logits apart): the
   //    vocabulary tiles whose rows are all token ids, then a partial last one
@@ -1102,13 +1329,13 @@ int pspo_loss_fwd_bwd(const uint16_t* hidden, const uint16_t* w_head, const int3
     const int tiles_full = V / kTileM, kept_tiles = zk != nullptr ? (int)(pl.Vc / kTileM) : 0;
     if (tiles_full > 0) {
       // the kept tiles' stores spread over the XCDs
-      GemmShape g{wk, pl.Vpad, tiles_full * kTileM, hk, pl.Npad, N, d, tiles_full, tiles_tok_n, n_fwd, kDynN,
+      GemmShape g{wk, pl.Vpad, tiles_full * kTileM, hk, pl.Npad, N, Dk, tiles_full, tiles_tok_n, n_fwd, kDynN,
                   kept_tiles < tiles_full ? kept_tiles : tiles_full};
       EpiForward<true> e{V, N, pl.Npad, 0, part_m, part_l, n_fwd, zk, kept_tiles, tiles_tok_n};
       if (int rc = launch_gemm(g, e, stream)) return rc;
     }
     if (tiles_full < tiles_voc) {
-      GemmShape g{wk + (int64_t)tiles_full * kTileM * kTileK, pl.Vpad, V - tiles_full * kTileM, hk, pl.Npad, N, d, 1,
+      GemmShape g{wk + (int64_t)tiles_full * kTileM * kTileK, pl.Vpad, V - tiles_full * kTileM, hk, pl.Npad, N, Dk, 1,
                   tiles_tok_n, n_fwd, kDynN};
       EpiForward<false> e{V, N, pl.Npad, tiles_full, part_m, part_l, n_fwd, zk, kept_tiles, tiles_tok_n};
       if (int rc = launch_gemm(g, e, stream)) return rc;
@@ -1131,7 +1358,7 @@ int pspo_loss_fwd_bwd(const uint16_t* hidden, const uint16_t* w_head, const int3
   if (int rc = launch_compact(N, KeepActive{delta}, cnt, act_idx, nullptr, nullptr, nullptr, n_act, stats, stream))
     return rc;
   hipLaunchKernelGGL(gather_backward_kernel, dim3((unsigned)((pl.Npad + 255) / 256)), dim3(256), 0, stream, N, n_act,
-                     act_idx, fwd_pos, target, lse, delta, act_fwd, act_tgt, act_lse, act_delta);
+                     act_idx, fwd_pos, target, lse, delta, zt, act_fwd, act_tgt, act_lse, act_delta, act_g1);
   PSPO_HIP_CHECK(hipGetLastError());
   hipLaunchKernelGGL(zero_inactive_rows_kernel, dim3((unsigned)N), dim3(256), 0, stream, d, delta, d_hidden);
   PSPO_HIP_CHECK(hipGetLastError());
@@ -1139,7 +1366,7 @@ int pspo_loss_fwd_bwd(const uint16_t* hidden, const uint16_t* w_head, const int3
   //    (K-blocked, in the forward's buffer) and their transpose H[bwd]^T
   //    [dpad x Npad], in one pass
   hipLaunchKernelGGL(kblock_rows_kernel, dim3(ctiles64, (unsigned)(pl.Npad / 32)), dim3(256), 0, stream, hidden,
-                     (int64_t)d, N, act_idx, n_act, hk, pl.Npad, hT, pl.dpad, pl.Npad);
+                     (int64_t)d, d, N, act_idx, n_act, hk, pl.Npad, hT, pl.dpad, pl.Npad);
   PSPO_HIP_CHECK(hipGetLastError());
   // 6. backward, one vocabulary chunk at a time; every product is bounded by
   //    the active-token count in device memory
@@ -1157,13 +1384,13 @@ int pspo_loss_fwd_bwd(const uint16_t* hidden, const uint16_t* w_head, const int3
       const int64_t rows = (V - v0) < vc ? (V - v0) : vc;
       const int tfull = (int)(rows / kTileM);
       if (tfull > 0) {
-        GemmShape g{wk + v0 * kTileK, pl.Vpad, tfull * kTileM, hk, pl.Npad, N, d, tfull, tiles_tok_n, n_act, kDynN};
+        GemmShape g{wk + v0 * kTileK, pl.Vpad, tfull * kTileM, hk, pl.Npad, N, Dk, tfull, tiles_tok_n, n_act, kDynN};
         EpiDelta<true> e{V, N, (int)v0, 0, dT, pl.Vc, dN, pl.Npad, act_tgt, act_lse, act_delta, n_act};
         if (int rc = launch_gemm(g, e, stream)) return rc;
       }
       if (tfull < ctiles) {
         const int64_t vp = v0 + (int64_t)tfull * kTileM;   // first row of the partial tile
-        GemmShape g{wk + vp * kTileK, pl.Vpad, (int)(V - vp), hk, pl.Npad, N, d, 1, tiles_tok_n, n_act, kDynN};
+        GemmShape g{wk + vp * kTileK, pl.Vpad, (int)(V - vp), hk, pl.Npad, N, Dk, 1, tiles_tok_n, n_act, kDynN};
         EpiDelta<false> e{V, N, (int)v0, tfull, dT, pl.Vc, dN, pl.Npad, act_tgt, act_lse, act_delta, n_act};
         if (int rc = launch_gemm(g, e, stream)) return rc;
       }
@@ -1181,6 +1408,32 @@ int pspo_loss_fwd_bwd(const uint16_t* hidden, const uint16_t* w_head, const int3
       if (int rc = launch_gemm_split_tail(g, e, TailDH{N, d, d_hidden, v0 == 0, act_idx, n_act}, slab, stream))
         return rc;
     }
+  }
+  // 7. the target entries of the logit gradient, in float32: the backward
+  //    columns bucketed by target id in column order, then dW[v] += the sum
+  //    of each bucket's g h rows and d_hidden += g W[o] row by row
+  {
+    const unsigned gcols = (unsigned)std::min<int64_t>((pl.Npad + 255) / 256, 1024);
+    hipLaunchKernelGGL(fill_i32_kernel, dim3((unsigned)std::min<int64_t>((V + 255) / 256, 1024)), dim3(256), 0,
+                       stream, oh_cnt, (int64_t)V, 0);
+    PSPO_HIP_CHECK(hipGetLastError());
+    hipLaunchKernelGGL(onehot_count_kernel, dim3(gcols), dim3(256), 0, stream, N, n_act, act_tgt, oh_cnt);
+    PSPO_HIP_CHECK(hipGetLastError());
+    hipLaunchKernelGGL(onehot_scan_kernel, dim3(1), dim3(kScanThreads), 0, stream, V, oh_cnt, oh_start, oh_cursor,
+                       oh_rows, oh_nrows);
+    PSPO_HIP_CHECK(hipGetLastError());
+    hipLaunchKernelGGL(onehot_fill_kernel, dim3(gcols), dim3(256), 0, stream, N, n_act, act_tgt, oh_cursor, oh_tmp);
+    PSPO_HIP_CHECK(hipGetLastError());
+    hipLaunchKernelGGL(onehot_rank_kernel, dim3(gcols), dim3(256), 0, stream, N, n_act, act_tgt, oh_start, oh_cnt,
+                       oh_tmp, oh_sorted);
+    PSPO_HIP_CHECK(hipGetLastError());
+    const int rows_bound = std::min(N, V);
+    hipLaunchKernelGGL(onehot_dw_kernel, dim3((unsigned)((rows_bound + 3) / 4)), dim3(256), 0, stream, rows_bound, d,
+                       oh_nrows, oh_rows, oh_start, oh_cnt, oh_sorted, act_idx, act_g1, hidden, d_w_head);
+    PSPO_HIP_CHECK(hipGetLastError());
+    hipLaunchKernelGGL(onehot_dh_kernel, dim3((unsigned)((N + 3) / 4)), dim3(256), 0, stream, N, d, n_act, act_idx,
+                       act_tgt, act_g1, w_head, d_hidden);
+    PSPO_HIP_CHECK(hipGetLastError());
   }
   return PSPO_OK;
 }

@@ -227,8 +227,9 @@ ProxyPlan make_proxy_plan(int64_t N, int64_t d, int64_t V) {
   p.off_s2 = take(p.ntv * p.Npad * 4);
   p.off_zt = take(p.Npad * 4);
   p.off_hn = take(p.Npad * 4);
-  p.off_wk = take(d * p.Vpad * 2);   // W, K-blocked [d/32][Vpad][32]
-  p.off_hk = take(d * p.Npad * 2);   // hidden rows, K-blocked [d/32][Npad][32]
+  const int64_t d64 = round_up(d, 64);   // columns the K-blocked copies write (zero past d)
+  p.off_wk = take(d64 * p.Vpad * 2);     // W, K-blocked [d64/32][Vpad][32]
+  p.off_hk = take(d64 * p.Npad * 2);     // hidden rows, K-blocked [d64/32][Npad][32]
   p.total = o;
   return p;
 }
@@ -250,7 +251,7 @@ int pspo_score_proxy(const uint16_t* hidden, const uint16_t* w_head, const int32
   clear_last_error();
   PSPO_REQUIRE(N >= 0, PSPO_ERR_INVALID_ARG, "N must be >= 0");
   PSPO_REQUIRE(d > 0 && V > 0, PSPO_ERR_INVALID_ARG, "d and V must be > 0");
-  PSPO_REQUIRE(d % 64 == 0, PSPO_ERR_UNSUPPORTED, "d must be a multiple of 64");
+  PSPO_REQUIRE(d % 8 == 0, PSPO_ERR_UNSUPPORTED, "d must be a multiple of 8");
   if (N == 0) return PSPO_OK;
   PSPO_REQUIRE(hidden && w_head && target && gamma, PSPO_ERR_INVALID_ARG, "null input or gamma pointer");
   PSPO_REQUIRE(aligned(hidden, 16) && aligned(w_head, 16), PSPO_ERR_INVALID_ARG,
@@ -276,25 +277,26 @@ int pspo_score_proxy(const uint16_t* hidden, const uint16_t* w_head, const int32
 
   const int tiles_tok = (int)(pl.Npad / kTileN);
   const int tiles_voc = (int)pl.ntv;
-  const unsigned ctiles64 = (unsigned)(d / 64);
+  const unsigned ctiles64 = (unsigned)((d + 63) / 64);
+  const int Dk = (int)round_up(d, kTileK);   // K of the product: d with zero padding to whole K steps
   hipLaunchKernelGGL(kblock_rows_kernel, dim3(ctiles64, (unsigned)(pl.Vpad / 32)), dim3(256), 0, stream, w_head,
-                     (int64_t)d, V, nullptr, nullptr, wk, pl.Vpad, nullptr, (int64_t)0, (int64_t)kTileK);
+                     (int64_t)d, d, V, nullptr, nullptr, wk, pl.Vpad, nullptr, (int64_t)0, (int64_t)kTileK);
   PSPO_HIP_CHECK(hipGetLastError());
   hipLaunchKernelGGL(kblock_rows_kernel, dim3(ctiles64, (unsigned)(pl.Npad / 32)), dim3(256), 0, stream, hidden,
-                     (int64_t)d, N, nullptr, nullptr, hk, pl.Npad, nullptr, (int64_t)0, (int64_t)kTileK);
+                     (int64_t)d, d, N, nullptr, nullptr, hk, pl.Npad, nullptr, (int64_t)0, (int64_t)kTileK);
   PSPO_HIP_CHECK(hipGetLastError());
   {
     // the vocabulary tiles whose rows are all token ids, then a partial last one
     const int tiles_full = V / kTileM;
     if (tiles_full > 0) {
-      GemmShape g{wk, pl.Vpad, tiles_full * kTileM, hk, pl.Npad, N, d, tiles_full, tiles_tok};
+      GemmShape g{wk, pl.Vpad, tiles_full * kTileM, hk, pl.Npad, N, Dk, tiles_full, tiles_tok};
       EpiProxy<true> e{V, N, pl.Npad, 0, target, part_m, part_s1, part_s2};
       hipLaunchKernelGGL(gemm_nt_kernel<EpiProxy<true>>, dim3(gemm_grid(tiles_full, tiles_tok)), dim3(kGemmThreads),
                          0, stream, g, e);
       PSPO_HIP_CHECK(hipGetLastError());
     }
     if (tiles_full < tiles_voc) {
-      GemmShape g{wk + (int64_t)tiles_full * kTileM * kTileK, pl.Vpad, V - tiles_full * kTileM, hk, pl.Npad, N, d, 1,
+      GemmShape g{wk + (int64_t)tiles_full * kTileM * kTileK, pl.Vpad, V - tiles_full * kTileM, hk, pl.Npad, N, Dk, 1,
                   tiles_tok};
       EpiProxy<false> e{V, N, pl.Npad, tiles_full, target, part_m, part_s1, part_s2};
       hipLaunchKernelGGL(gemm_nt_kernel<EpiProxy<false>>, dim3(gemm_grid(1, tiles_tok)), dim3(kGemmThreads), 0,

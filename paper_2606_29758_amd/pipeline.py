@@ -50,17 +50,34 @@ def upload(wl, logp_old_full: np.ndarray, device="cuda") -> DeviceWorkload:
 
 
 class Step:
-    """Reusable buffers for repeated passes over one DeviceWorkload."""
+    """Reusable buffers for repeated passes over one DeviceWorkload.
 
-    def __init__(self, dw: DeviceWorkload):
+    The loss workspace and the d_hidden buffer are sized by the packed token
+    count N of the calls made so far (grown when a call needs more), not by the
+    batch's total token count: a truncated step needs only its prefixes' share.
+    """
+
+    def __init__(self, dw: DeviceWorkload, flags: int = 0):
         self.dw = dw
+        self.flags = flags
         dev = dw.lengths.device
         self.cutoffs = torch.empty(dw.P * dw.K, dtype=torch.int32, device=dev)
         self.err = torch.zeros(1, dtype=torch.int32, device=dev)
         self.d_w = torch.empty((dw.V, dw.d), dtype=torch.float32, device=dev)
-        self.d_h = torch.empty((max(dw.capacity, 1), dw.d), dtype=torch.float32, device=dev)
-        self.workspace = torch.empty(max(pspo.loss_workspace_bytes(dw.capacity, dw.d, dw.V), 256),
-                                     dtype=torch.uint8, device=dev)
+        self.d_h = torch.empty((0, dw.d), dtype=torch.float32, device=dev)
+        self.workspace = torch.empty(0, dtype=torch.uint8, device=dev)
+
+    def reserve(self, N: int, flags: int = 0) -> None:
+        """Grows the d_hidden buffer and the workspace to what a call over N tokens needs."""
+        dw = self.dw
+        dev = dw.lengths.device
+        if self.d_h.shape[0] < max(N, 1):
+            self.d_h = None
+            self.d_h = torch.empty((max(N, 1), dw.d), dtype=torch.float32, device=dev)
+        need = max(pspo.loss_workspace_bytes(N, dw.d, dw.V, flags), 256)
+        if self.workspace.numel() < need:
+            self.workspace = None
+            self.workspace = torch.empty(need, dtype=torch.uint8, device=dev)
 
     def sample_and_pack(self, seed: int, offset: int = 0) -> dict:
         dw = self.dw
@@ -70,16 +87,19 @@ class Step:
                                   target_full=dw.target_full, logp_old_full=dw.logp_old_full,
                                   hidden_full=dw.hidden_full, err_flag=self.err)
 
-    def loss(self, pk: dict, N: int, flags: int = 0, want_logp: bool = True) -> dict:
+    def loss(self, pk: dict, N: int, flags: Optional[int] = None, want_logp: bool = True) -> dict:
         """want_logp=False: no per-token log-probs, and the forward skips the tokens of
-        zero-advantage completions (their loss terms and gradients are exactly zero)."""
+        zero-advantage completions (their loss terms and gradients are exactly zero).
+        flags: the library's loss flags (default: the Step's)."""
         dw = self.dw
+        flags = self.flags if flags is None else flags
+        self.reserve(N, flags)
         return pspo.loss_fwd_bwd(pk["hidden"], dw.w_head, pk["target"], pk["logp_old"], pk["weight"],
                                  pk["seq_id"], dw.advantage, N, dw.eps_low, dw.eps_high, dw.loss_scale,
                                  flags=flags, d_w_head=self.d_w, d_hidden=self.d_h,
                                  workspace=self.workspace, err_flag=self.err, want_logp=want_logp)
 
-    def __call__(self, seed: int, offset: int = 0, flags: int = 0, want_logp: bool = True) -> dict:
+    def __call__(self, seed: int, offset: int = 0, flags: Optional[int] = None, want_logp: bool = True) -> dict:
         pk = self.sample_and_pack(seed, offset)
         N = int(pk["n_tokens"].item())   # the one host sync of a step
         out = self.loss(pk, N, flags, want_logp)
@@ -121,7 +141,7 @@ def reseed_mean(step: "Step", seeds, want_logp: bool = False) -> dict:
     for i, s in enumerate(seeds):
         pk = step.sample_and_pack(s)
         N = int(pk["n_tokens"].item())
-        out = step.loss(pk, N, flags=pspo.PSPO_ACCUMULATE_DW if i > 0 else 0, want_logp=False)
+        out = step.loss(pk, N, flags=step.flags | (pspo.PSPO_ACCUMULATE_DW if i > 0 else 0), want_logp=False)
         loss_sum += float(out["loss"].item())
         if N > 0:
             src = pk["src_row"][:N].long()
@@ -147,38 +167,3 @@ def reseed_mean(step: "Step", seeds, want_logp: bool = False) -> dict:
                 mean_dw=acc_dw / S, weighted_dw=wdw, full_dw=fdw,
                 mean_dh=acc_dh[:total] / S, weighted_dh=wdh, full_dh=fdh,
                 kept=kept[:total], weight_full=c_full, logp_full=flp, tokens=total, seeds=S)
-
-
-def reseed_summary(dw: DeviceWorkload, res: dict) -> dict:
-    """Scalars of a reseed_mean result.
-
-    identity: how far the S-draw mean is from the weighted full call (rounding only):
-    loss relative error, dW and dH relative L2 errors.  mean_vs_full: the relative
-    distance of the mean dW from the full update G, and App. C's diagonal prediction of
-    it, sqrt(sum_t (1/xi_t - 1) ||g_t||^2 / S) / ||G||, with ||g_t||^2 = delta_t^2 ||h_t||^2
-    ||e_o - p_t||^2 = delta_t^2 gamma_t (gamma from the score proxy, delta_t the token's
-    logit-gradient scale at weight 1, from the full call's log-probs).  Needs
-    res['logp_full'] (reseed_mean(..., want_logp=True)).
-    """
-    f32 = lambda x: float(np.float32(x))
-    rel = lambda a, b: float(torch.linalg.vector_norm((a - b).double()) / torch.linalg.vector_norm(b.double()))
-    S = res["seeds"]
-    total = res["tokens"]
-    G = res["full_dw"]
-    gamma = pspo.score_proxy(dw.hidden_full, dw.w_head, dw.target_full, total, want_logp=False)["gamma"].double()
-    rho = torch.exp(res["logp_full"].double() - dw.logp_old_full[:total].double())
-    seq = torch.repeat_interleave(torch.arange(dw.P * dw.K, device=G.device), dw.lengths.long())
-    A = dw.advantage.double()[seq]
-    mu = ((A > 0) & (rho <= 1 + f32(dw.eps_high))) | ((A < 0) & (rho >= 1 - f32(dw.eps_low)))
-    delta = -f32(dw.loss_scale) * mu.double() * rho * A
-    var = torch.sum((res["weight_full"].double() - 1.0) * delta ** 2 * gamma) / S
-    return {
-        "seeds": S,
-        "tokens": total,
-        "identity": {"loss_rel": abs(res["mean_loss"] - res["weighted_loss"]) / abs(res["weighted_loss"]),
-                     "dw_rel_l2": rel(res["mean_dw"], res["weighted_dw"]),
-                     "dh_rel_l2": rel(res["mean_dh"], res["weighted_dh"])},
-        "mean_vs_full": {"dw_rel_dev": rel(res["mean_dw"], G),
-                         "app_c_diagonal_prediction": float(torch.sqrt(var) / torch.linalg.vector_norm(G.double())),
-                         "loss_mean": res["mean_loss"], "loss_full": res["full_loss"]},
-    }

@@ -16,8 +16,8 @@ _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libpspo.so")
 
 PSPO_ACCUMULATE_DW = 1
-PSPO_RECOMPUTE_LOGITS = 2
-DEVERR_TARGET, DEVERR_BAD_XI, DEVERR_CAPACITY, DEVERR_SEQ_ID = 1, 2, 4, 8
+PSPO_KEEP_LOGITS = 4
+DEVERR_TARGET, DEVERR_BAD_XI, DEVERR_CAPACITY, DEVERR_SEQ_ID, DEVERR_NONFINITE = 1, 2, 4, 8, 16
 
 _P = ctypes.c_void_p
 _I32, _I64, _U32, _U64, _F32, _SZ = ctypes.c_int32, ctypes.c_int64, ctypes.c_uint32, ctypes.c_uint64, ctypes.c_float, ctypes.c_size_t
@@ -172,11 +172,29 @@ def loss_fwd_bwd(hidden, w_head, target, logp_old, weight, seq_id, advantage, N:
     """Loss and gradients for the first N rows of the packed per-token tensors.
 
     hidden: bf16 [>=N, d]; w_head: bf16 [V, d]; target int32, logp_old/weight float32,
-    seq_id int32 (all [>=N]); advantage float32 [R].  Returns loss (float64 [1]),
+    seq_id int32 (all [>=N]); advantage float32 [R].  d_hidden (float32 [>=N, d]) and
+    d_w_head (float32 [V, d]) may be given.  Returns loss (float64 [1]),
     d_hidden (float32 [N, d] view), d_w_head (float32 [V, d]), logp_new, stats.
+    Shapes are checked first (the kernels write d_hidden rows 0..N-1 and every row of
+    d_w_head, and read the first N rows of the per-token inputs), then devices and dtypes.
     """
-    _dev(w_head, torch.bfloat16, "w_head")
+    if w_head.dim() != 2:
+        raise ValueError("w_head must be [V, d]")
     V, d = w_head.shape
+    if N < 0:
+        raise ValueError("N must be >= 0")
+    if N > 0:
+        if hidden.dim() != 2 or hidden.shape[1] != d:
+            raise ValueError("hidden and w_head disagree on d")
+        for name, t in (("hidden", hidden), ("target", target), ("logp_old", logp_old),
+                        ("weight", weight), ("seq_id", seq_id)):
+            if t.shape[0] < N:
+                raise ValueError(f"{name} has fewer than N rows")
+    if d_w_head is not None and tuple(d_w_head.shape) != (V, d):
+        raise ValueError(f"d_w_head must be [V, d] = [{V}, {d}], got {list(d_w_head.shape)}")
+    if d_hidden is not None and (d_hidden.dim() != 2 or d_hidden.shape[1] != d or d_hidden.shape[0] < N):
+        raise ValueError(f"d_hidden must be [>= N, d] = [>= {N}, {d}], got {list(d_hidden.shape)}")
+    _dev(w_head, torch.bfloat16, "w_head")
     dev = w_head.device
     _dev(advantage, torch.float32, "advantage")
     if N > 0:
@@ -185,12 +203,6 @@ def loss_fwd_bwd(hidden, w_head, target, logp_old, weight, seq_id, advantage, N:
         _dev(logp_old, torch.float32, "logp_old")
         _dev(weight, torch.float32, "weight")
         _dev(seq_id, torch.int32, "seq_id")
-        if hidden.shape[1] != d:
-            raise ValueError("hidden and w_head disagree on d")
-        for name, t in (("hidden", hidden), ("target", target), ("logp_old", logp_old),
-                        ("weight", weight), ("seq_id", seq_id)):
-            if t.shape[0] < N:
-                raise ValueError(f"{name} has fewer than N rows")
     if d_w_head is None:
         d_w_head = torch.empty((V, d), dtype=torch.float32, device=dev)
     _dev(d_w_head, torch.float32, "d_w_head")

@@ -36,7 +36,7 @@ def test_exports_every_declared_symbol(lib):
 
 
 def test_version_and_status_strings(lib):
-    assert lib.pspo_abi_version() == 4
+    assert lib.pspo_abi_version() == 5
     assert lib.pspo_status_string(0) == b"PSPO_OK"
     assert lib.pspo_status_string(3) == b"PSPO_ERR_WORKSPACE"
     assert lib.pspo_status_string(99) == b"PSPO_ERR_UNKNOWN"
@@ -120,9 +120,12 @@ def test_loss_argument_errors(lib):
     assert _loss(lib, N=-1) == INVALID
     assert _loss(lib, d=0) == INVALID
     assert _loss(lib, V=0) == INVALID
-    assert _loss(lib, d=96) == UNSUPPORTED
+    assert _loss(lib, d=100) == UNSUPPORTED          # d % 8 != 0
+    _loss(lib, d=96)                                 # d % 8 == 0 passes the argument checks
+    assert b"multiple of" not in lib.pspo_last_error()
     assert _loss(lib, R=0) == INVALID
-    assert _loss(lib, flags=4) == INVALID            # unknown flag bit
+    assert _loss(lib, flags=2) == INVALID            # the retired bit
+    assert _loss(lib, flags=8) == INVALID            # unknown flag bit
     assert _loss(lib, el=1.0) == INVALID
     assert _loss(lib, eh=-0.1) == INVALID
     assert _loss(lib, el=float("nan")) == INVALID
@@ -138,13 +141,13 @@ def test_loss_argument_errors(lib):
     assert b"workspace too small" in lib.pspo_last_error()
 
 
-def test_workspace_bytes_recompute_flag(lib):
-    # without PSPO_RECOMPUTE_LOGITS the forward keeps the first vocabulary
-    # chunk's logits as fp16 offsets: Vc x round_up(N, 768) x 2 bytes more (Vc = 49152 at
+def test_workspace_bytes_keep_flag(lib):
+    # with PSPO_KEEP_LOGITS the forward keeps the first vocabulary chunk's
+    # logits as fp16 offsets: Vc x round_up(N, 768) x 2 bytes more (Vc = 49152 at
     # d = 3584, the whole padded vocabulary when that is smaller)
     for N, d, V, vc in ((1000, 3584, 152064, 49152), (300, 128, 2048, 2304), (5000, 4096, 151936, 6144)):
-        keep = lib.pspo_loss_workspace_bytes(N, d, V, 0)
-        lean = lib.pspo_loss_workspace_bytes(N, d, V, 2)
+        keep = lib.pspo_loss_workspace_bytes(N, d, V, 4)
+        lean = lib.pspo_loss_workspace_bytes(N, d, V, 0)
         npad = -(-N // 768) * 768
         assert keep - lean == vc * npad * 2, (N, d, V)
 
@@ -173,7 +176,9 @@ def test_score_proxy_argument_errors(lib):
     assert _proxy(lib, N=-1) == INVALID
     assert _proxy(lib, d=0) == INVALID
     assert _proxy(lib, V=0) == INVALID
-    assert _proxy(lib, d=96) == UNSUPPORTED
+    assert _proxy(lib, d=100) == UNSUPPORTED
+    _proxy(lib, d=96)
+    assert b"multiple of" not in lib.pspo_last_error()
     assert _proxy(lib, g=None) == INVALID
     assert _proxy(lib, h=None) == INVALID
     assert _proxy(lib, t=None) == INVALID
@@ -242,3 +247,32 @@ def test_mfma_loop_argument_errors(lib):
     assert lib.pspo_mfma_loop(4, 0, out, None) == INVALID
     assert lib.pspo_mfma_loop(4, 4, None, None) == INVALID
     assert lib.pspo_mfma_loop(4, 4, ctypes.c_void_p((1 << 20) + 2), None) == INVALID
+
+
+def test_binding_checks_gradient_shapes():
+    """The kernels write d_hidden rows 0..N-1 and every row of d_w_head: the binding refuses
+    buffers of another shape before anything reaches the library (shapes are checked ahead of
+    devices, so host tensors exercise it)."""
+    import torch
+    V, d, N = 40, 16, 5
+    w = torch.zeros(V, d, dtype=torch.bfloat16)
+    h = torch.zeros(N, d, dtype=torch.bfloat16)
+    i32 = torch.zeros(N, dtype=torch.int32)
+    f = torch.zeros(N, dtype=torch.float32)
+    adv = torch.zeros(2, dtype=torch.float32)
+
+    def call(**kw):
+        return pspo.loss_fwd_bwd(h, w, i32, f, f, i32, adv, N, 0.1, 0.1, 1.0, **kw)
+
+    with pytest.raises(ValueError, match="d_hidden"):
+        call(d_hidden=torch.zeros(N - 1, d))
+    with pytest.raises(ValueError, match="d_hidden"):
+        call(d_hidden=torch.zeros(N, d + 8))
+    with pytest.raises(ValueError, match="d_w_head"):
+        call(d_w_head=torch.zeros(V, d + 8))
+    with pytest.raises(ValueError, match="d_w_head"):
+        call(d_w_head=torch.zeros(V - 1, d))
+    with pytest.raises(ValueError, match="fewer than N rows"):
+        pspo.loss_fwd_bwd(h[:3], w, i32, f, f, i32, adv, N, 0.1, 0.1, 1.0)
+    with pytest.raises(ValueError, match="device tensor"):   # right shapes: the device check follows
+        call(d_hidden=torch.zeros(N, d), d_w_head=torch.zeros(V, d))

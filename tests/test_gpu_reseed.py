@@ -45,17 +45,23 @@ def _np(t):
     return t.detach().double().cpu().numpy()
 
 
+def _rel(a, b):
+    return float(torch.linalg.vector_norm((a - b).double()) / torch.linalg.vector_norm(b.double()))
+
+
 def _check_identity(dw, res, name):
-    s = pipeline.reseed_summary(dw, res)
-    print(f"[{name}] identity: loss rel {s['identity']['loss_rel']:.2e}, dW rel L2 {s['identity']['dw_rel_l2']:.2e}, "
-          f"dH rel L2 {s['identity']['dh_rel_l2']:.2e}; 64-draw mean vs full update: dW rel dev "
-          f"{s['mean_vs_full']['dw_rel_dev']:.3e}, App. C diagonal prediction "
-          f"{s['mean_vs_full']['app_c_diagonal_prediction']:.3e}", flush=True)
-    assert s["identity"]["loss_rel"] <= LOSS_RTOL
-    assert s["identity"]["dw_rel_l2"] <= GRAD_REL_L2
-    assert s["identity"]["dh_rel_l2"] <= GRAD_REL_L2
-    assert np.isfinite(s["mean_vs_full"]["dw_rel_dev"]) and np.isfinite(s["mean_vs_full"]["app_c_diagonal_prediction"])
-    return s
+    """The S-draw mean against the weighted full call (rounding only), and the mean's
+    distance from the plain full update (the estimator's noise; a report)."""
+    loss_rel = abs(res["mean_loss"] - res["weighted_loss"]) / abs(res["weighted_loss"])
+    dw_rel = _rel(res["mean_dw"], res["weighted_dw"])
+    dh_rel = _rel(res["mean_dh"], res["weighted_dh"])
+    dev = _rel(res["mean_dw"], res["full_dw"])
+    print(f"[{name}] identity: loss rel {loss_rel:.2e}, dW rel L2 {dw_rel:.2e}, dH rel L2 {dh_rel:.2e}; "
+          f"64-draw mean vs full update: dW rel dev {dev:.3e}", flush=True)
+    assert loss_rel <= LOSS_RTOL
+    assert dw_rel <= GRAD_REL_L2
+    assert dh_rel <= GRAD_REL_L2
+    assert np.isfinite(dev)
 
 
 def test_reseed_mean_equals_weighted_full_call_tiny():

@@ -178,3 +178,33 @@ def test_brute_force_unbiasedness():
             H[r] = hcut
             L_unweighted += pr * run(H, np.ones_like(xi))[0]
     assert abs(L_unweighted - full[0]) > 1e-3 * abs(full[0])
+
+
+@pytest.mark.parametrize("seed,el,eh", [(5, 0.1, 0.1), (6, 0.2, 0.28)])
+def test_loss_terms_and_grad_w_rows_match_autograd(seed, el, eh):
+    """The large-batch helpers: the loss from given log-probs, and selected dW rows from each
+    token's lse and delta, against float64 autograd of the plain formula (independent of
+    loss_fwd_bwd).  Rows: targets of one token, of several tokens, of none, first and last."""
+    h, W, target, lp_old, weight, seq_id, adv = _small_case(seed, N=41, V=29, sigma=0.25)
+    target[:6] = 3                      # a row that is the target of several tokens
+    lp_old = ppo_head.target_logprob(h, W, target) + 0.25 * np.random.default_rng(seed).standard_normal(len(target))
+    L, dh, dw, logp = _torch_reference(h, W, target, lp_old, weight, seq_id, adv, el, eh, 0.125)
+    t = ppo_head.loss_terms(logp, lp_old, weight, seq_id, adv, el, eh, 0.125)
+    assert t["loss"] == pytest.approx(L, rel=1e-12, abs=1e-14)
+    assert 0 < t["mu"].sum() < len(target)
+    # delta = dL/dl: autograd through the ratio and clip alone
+    tl = torch.tensor(logp, dtype=torch.float64, requires_grad=True)
+    rho = torch.exp(tl - torch.tensor(lp_old, dtype=torch.float64))
+    A = torch.tensor(adv, dtype=torch.float64)[torch.tensor(seq_id)]
+    (-0.125 * (torch.tensor(weight, dtype=torch.float64)
+               * torch.minimum(rho * A, torch.clamp(rho, 1 - el, 1 + eh) * A)).sum()).backward()
+    np.testing.assert_allclose(t["delta"], tl.grad.numpy(), rtol=1e-12, atol=1e-15)
+    lse = ppo_head.target_logits(h, W, target) - logp
+    np.testing.assert_allclose(lse, special.logsumexp(h @ W.T, axis=1), rtol=1e-13)
+    empty = next(v for v in range(W.shape[0]) if not np.any(target == v))   # no token targets it
+    rows = np.array([0, 3, int(target[10]), W.shape[0] - 1, empty])
+    got = ppo_head.grad_w_rows(h, W, target, lse, t["delta"], rows, chunk=7)
+    np.testing.assert_allclose(got, dw[rows], rtol=1e-10, atol=1e-13)
+    # and the full oracle agrees
+    full = ppo_head.loss_fwd_bwd(h, W, target, lp_old, weight, seq_id, adv, el, eh, 0.125)
+    np.testing.assert_allclose(got, full["d_w"][rows], rtol=1e-10, atol=1e-13)
