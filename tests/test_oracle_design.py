@@ -176,3 +176,58 @@ def test_design_tables_layout():
     xi = cd.design_tables(w, [0, 5, 8], 2.0)
     np.testing.assert_allclose(xi[:5], 0.4)
     np.testing.assert_allclose(xi[5:], 2.0 / 3)
+
+
+def _common_tail_case(seed, n, k, V=60, listed=36, rest_range=(0.05, 0.5)):
+    """Dense next-token distributions pi_r = pit_r + rest_r tau: pit_r on the k ids of row r's
+    list (ids < `listed`), tau one tail distribution on the ids >= `listed` (outside every
+    list), rest_r the row's mass outside its list."""
+    rng = np.random.default_rng(seed)
+    tau = rng.dirichlet(np.ones(V - listed))
+    ids = np.stack([rng.choice(listed, k, replace=False) for _ in range(n)]).astype(np.int32)
+    rest = rng.uniform(*rest_range, n)
+    top = rng.dirichlet(np.ones(k), n) * (1.0 - rest)[:, None]
+    dense = np.zeros((n, V))
+    dense[np.arange(n)[:, None], ids] = top
+    dense[:, listed:] = rest[:, None] * tau[None, :]
+    return dense, ids, np.log(top), rest
+
+
+@pytest.mark.parametrize("seed,n,k,succ", [(10, 6, 3, [1, 0, 0, 1, 1, 0]), (11, 8, 5, [1, 1, 1, 0, 1, 1, 0, 1]),
+                                           (12, 5, 2, [0, 0, 1, 0, 0]), (13, 7, 4, [0, 1, 0, 1, 0, 1, 0])])
+def test_topk_rest_coordinate_equals_dense_formula(seed, n, k, succ):
+    """App. E with top-k lists (k < V): when the mass outside each list lies on one tail
+    distribution shared by all completions and outside every list, the dense
+    1/2 - 1/2 || p pibar_G - (1-p) pibar_B ||_1 equals the top-k formula with one signed
+    "rest" coordinate exactly.  Rest masses 0.05..0.5 with successes holding more rest
+    mass in some cases and less in others, so both signs of the rest difference occur."""
+    dense, ids, logp, rest = _common_tail_case(seed, n, k)
+    succ = np.array(succ, dtype=np.float64)
+    out = cd.proxy_weights(np.ones(n), ids, logp, np.ones(n, dtype=np.int64), succ, 1, n)
+    ref = _dense_u(dense, succ > 0.5)
+    assert out["u"][0] == pytest.approx(ref, abs=1e-13)
+    assert 0.0 < ref < 0.5
+
+
+def test_topk_rest_coordinate_pins_sign_and_abs():
+    """Mutants of the oracle's rest term fail the dense-formula pin: dropping the
+    success/failure sign of each completion's rest mass, or the absolute value of the
+    summed rest (flipping every sign at once leaves |rest| unchanged and is the same
+    formula).  The mutants are the oracle's own source with one edit each."""
+    import inspect
+    import textwrap
+    src = textwrap.dedent(inspect.getsource(cd.proxy_weights))
+    mutants = {"no sign": ("rest += sign * max(0.0, 1.0 - mass)", "rest += max(0.0, 1.0 - mass)"),
+               "no abs": ("+ abs(rest)", "+ rest")}
+    cases = [(10, 6, 3, [1, 0, 0, 1, 1, 0]), (12, 5, 2, [0, 0, 1, 0, 0]), (13, 7, 4, [0, 1, 0, 1, 0, 1, 0])]
+    for name, (old, new) in mutants.items():
+        assert src.count(old) == 1, name
+        ns = {"np": np}
+        exec(src.replace(old, new), ns)
+        failed = False
+        for seed, n, k, succ in cases:
+            dense, ids, logp, _ = _common_tail_case(seed, n, k)
+            s = np.array(succ, dtype=np.float64)
+            u = ns["proxy_weights"](np.ones(n), ids, logp, np.ones(n, dtype=np.int64), s, 1, n)["u"][0]
+            failed |= abs(u - _dense_u(dense, s > 0.5)) > 1e-9
+        assert failed, f"mutant '{name}' passes the pin"
