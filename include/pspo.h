@@ -326,6 +326,23 @@ int pspo_design_cutoffs(const double* w, const int64_t* xi_off, int32_t P, int64
                         void* workspace, size_t workspace_bytes, int32_t* err_flag,
                         hipStream_t stream);
 
+/*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * survival tables as pspo_design_cutoffs, bitwise, with no workspace argument.
+ * The PAV block stack lives in a static device array of 8 MiB that the library
+ * holds on each GPU it runs on until the process ends, so total_T <= 2^19
+ * (524288 steps); a larger total_T returns PSPO_ERR_UNSUPPORTED before
+ * anything is enqueued.  The call allocates and frees nothing.  Every call on
+ * one GPU shares that GPU's array: calls that overlap on one GPU (concurrent
+ * streams or threads) race and must be ordered by the caller.  The array needs
+ * no clearing between calls (the solve writes each entry before reading it).
+ * Other arguments, conventions and errors as in pspo_design_cutoffs.
+ */
+int pspo_design_cutoffs_noalloc(const double* w, const int64_t* xi_off, int32_t P, int64_t total_T,
+                                double budget, int32_t variant, double lambda, double* xi,
+                                int32_t* err_flag, hipStream_t stream);
+
 /* ------------------------------------------------------------------------
  * Measurement entry point.  Not a step of the method and not used by any
  * call above: it exists so that a benchmark can report the sustained

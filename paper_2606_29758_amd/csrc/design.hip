@@ -24,6 +24,7 @@
 // Both kernels work in float64; their cost is negligible next to the proxy's
 // forward pass (a few operations per completion token and per step).
 #include <cmath>
+#include <mutex>
 #include <string>
 
 #include "common.h"
@@ -251,6 +252,67 @@ __global__ __launch_bounds__(64) void design_cutoffs_kernel(const double* __rest
   }
 }
 
+// Argument checks shared by the design entry points (host only).
+int check_design_args(const double* w, const int64_t* xi_off, int32_t P, int64_t total_T, double budget,
+                      int32_t variant, double lambda, const double* xi) {
+  PSPO_REQUIRE(P >= 1 && total_T >= 0, PSPO_ERR_INVALID_ARG, "need P >= 1 and total_T >= 0");
+  PSPO_REQUIRE(variant >= PSPO_DESIGN_OPTIMIZED && variant <= PSPO_DESIGN_TIME_PRIOR, PSPO_ERR_INVALID_ARG,
+               "unknown design variant");
+  PSPO_REQUIRE(std::isfinite(budget) && budget > 0.0, PSPO_ERR_INVALID_ARG, "budget must be finite and > 0");
+  PSPO_REQUIRE(std::isfinite(lambda) && lambda >= 0.0, PSPO_ERR_INVALID_ARG, "lambda must be finite and >= 0");
+  if (total_T == 0) return PSPO_OK;
+  PSPO_REQUIRE(w && xi_off && xi, PSPO_ERR_INVALID_ARG, "null pointer");
+  PSPO_REQUIRE(aligned(w, 8) && aligned(xi_off, 8) && aligned(xi, 8), PSPO_ERR_INVALID_ARG,
+               "misaligned pointer");
+  return PSPO_OK;
+}
+
+// The PAV block stack (start, length, value per step: pspo_design_workspace_bytes(total_T))
+// carved from `ws`, then the solve.  The kernel writes every stack entry before
+// reading it, so the memory needs no clearing.
+int launch_design(const double* w, const int64_t* xi_off, int32_t P, int64_t total_T, double budget, int32_t variant,
+                  double lambda, double* xi, char* ws, int32_t* err_flag, hipStream_t stream) {
+  int32_t* bstart = reinterpret_cast<int32_t*>(ws);
+  int32_t* blen = reinterpret_cast<int32_t*>(ws + round_up(total_T * 4, 256));
+  double* bval = reinterpret_cast<double*>(ws + 2 * round_up(total_T * 4, 256));
+  hipLaunchKernelGGL(design_cutoffs_kernel, dim3((unsigned)P), dim3(64), 0, stream, w, xi_off, budget, variant,
+                     lambda, xi, bstart, blen, bval, err_flag);
+  PSPO_HIP_CHECK(hipGetLastError());
+  return PSPO_OK;
+}
+
+}  // namespace
+
+// Scratch of the no-allocation entry point: a file-scope device array, one copy
+// per GPU, held until the process ends.  Host code never uses its name as an
+// address (on the host it is a stand-in symbol): the device address comes from
+// hipGetSymbolAddress, taken once per device with that device current.
+constexpr size_t kNoAllocScratchBytes = size_t(8) << 20;   // total_T <= 2^19 steps
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+char* g_scratch[kMaxDevices] = {};
+
+// The current device's address of `scratch` (looked up on the first call on
+// that device).
+int scratch_address(char** out) {
+  int dev = 0;
+  PSPO_HIP_CHECK(hipGetDevice(&dev));
+  PSPO_REQUIRE(dev >= 0 && dev < kMaxDevices, PSPO_ERR_UNSUPPORTED, "device id out of range");
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch[dev] == nullptr) {
+    void* p = nullptr;
+    PSPO_HIP_CHECK(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    PSPO_REQUIRE(p != nullptr && aligned(p, 256), PSPO_ERR_HIP, "scratch has no usable device address");
+    g_scratch[dev] = static_cast<char*>(p);
+  }
+  *out = g_scratch[dev];
+  return PSPO_OK;
+}
+
 }  // namespace
 }  // namespace pspo
 
@@ -291,28 +353,31 @@ int pspo_design_cutoffs(const double* w, const int64_t* xi_off, int32_t P, int64
                         int32_t* err_flag, hipStream_t stream) {
   using namespace pspo;
   clear_last_error();
-  PSPO_REQUIRE(P >= 1 && total_T >= 0, PSPO_ERR_INVALID_ARG, "need P >= 1 and total_T >= 0");
-  PSPO_REQUIRE(variant >= PSPO_DESIGN_OPTIMIZED && variant <= PSPO_DESIGN_TIME_PRIOR, PSPO_ERR_INVALID_ARG,
-               "unknown design variant");
-  PSPO_REQUIRE(std::isfinite(budget) && budget > 0.0, PSPO_ERR_INVALID_ARG, "budget must be finite and > 0");
-  PSPO_REQUIRE(std::isfinite(lambda) && lambda >= 0.0, PSPO_ERR_INVALID_ARG, "lambda must be finite and >= 0");
+  if (int rc = check_design_args(w, xi_off, P, total_T, budget, variant, lambda, xi)) return rc;
   if (total_T == 0) return PSPO_OK;
-  PSPO_REQUIRE(w && xi_off && xi, PSPO_ERR_INVALID_ARG, "null pointer");
-  PSPO_REQUIRE(aligned(w, 8) && aligned(xi_off, 8) && aligned(xi, 8), PSPO_ERR_INVALID_ARG,
-               "misaligned pointer");
   PSPO_REQUIRE(workspace && aligned(workspace, 256), PSPO_ERR_INVALID_ARG,
                "workspace must be non-NULL and 256-byte aligned");
   PSPO_REQUIRE(workspace_bytes >= pspo_design_workspace_bytes(total_T), PSPO_ERR_WORKSPACE,
                "workspace too small: need " + std::to_string(pspo_design_workspace_bytes(total_T)) + " bytes");
   if (int rc = require_gfx950()) return rc;
-  char* ws = static_cast<char*>(workspace);
-  int32_t* bstart = reinterpret_cast<int32_t*>(ws);
-  int32_t* blen = reinterpret_cast<int32_t*>(ws + round_up(total_T * 4, 256));
-  double* bval = reinterpret_cast<double*>(ws + 2 * round_up(total_T * 4, 256));
-  hipLaunchKernelGGL(design_cutoffs_kernel, dim3((unsigned)P), dim3(64), 0, stream, w, xi_off, budget, variant,
-                     lambda, xi, bstart, blen, bval, err_flag);
-  PSPO_HIP_CHECK(hipGetLastError());
-  return PSPO_OK;
+  return launch_design(w, xi_off, P, total_T, budget, variant, lambda, xi, static_cast<char*>(workspace), err_flag,
+                       stream);
+}
+
+int pspo_design_cutoffs_noalloc(const double* w, const int64_t* xi_off, int32_t P, int64_t total_T, double budget,
+                                int32_t variant, double lambda, double* xi, int32_t* err_flag, hipStream_t stream) {
+  using namespace pspo;
+  clear_last_error();
+  if (int rc = check_design_args(w, xi_off, P, total_T, budget, variant, lambda, xi)) return rc;
+  if (total_T == 0) return PSPO_OK;
+  PSPO_REQUIRE(pspo_design_workspace_bytes(total_T) <= kNoAllocScratchBytes, PSPO_ERR_UNSUPPORTED,
+               "total_T = " + std::to_string(total_T) + " needs " +
+                   std::to_string(pspo_design_workspace_bytes(total_T)) + " bytes of scratch; the no-allocation "
+                   "entry point has " + std::to_string(kNoAllocScratchBytes) + " (total_T <= 2^19)");
+  if (int rc = require_gfx950()) return rc;
+  char* ws = nullptr;
+  if (int rc = scratch_address(&ws)) return rc;
+  return launch_design(w, xi_off, P, total_T, budget, variant, lambda, xi, ws, err_flag, stream);
 }
 
 }  // extern "C"

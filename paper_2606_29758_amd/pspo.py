@@ -40,6 +40,8 @@ _SIGNATURES = {
     "pspo_design_cutoffs": (ctypes.c_int, [_P, _P, _I32, _I64, ctypes.c_double, _I32, ctypes.c_double,
                                            _P, _P, _SZ, _P, _P]),
     "pspo_score_proxy": (ctypes.c_int, [_P, _P, _P, _I32, _I32, _I32, _P, _P, _P, _P, _P, _SZ, _P]),
+    "pspo_design_cutoffs_noalloc": (ctypes.c_int, [_P, _P, _I32, _I64, ctypes.c_double, _I32, ctypes.c_double,
+                                                   _P, _P, _P]),
     "pspo_mfma_loop": (ctypes.c_int, [_I32, _I32, _P, _P]),
 }
 
@@ -304,6 +306,23 @@ def design_cutoffs(w, xi_off, P: int, total_T: int, budget: float, variant: int 
     _check(load().pspo_design_cutoffs(_ptr(w), _ptr(xi_off), P, total_T, float(budget), int(variant), float(lam),
                                       _ptr(xi), _ptr(ws), ws.numel(), _ptr(err_flag), _stream()))
     return xi[:total_T]
+
+
+def design_cutoffs_noalloc(w, xi_off, P: int, total_T: int, budget: float, out: torch.Tensor,
+                           variant: int = PSPO_DESIGN_OPTIMIZED, lam: float = 0.0,
+                           err_flag: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """design_cutoffs without a workspace (the library's static scratch; total_T <= 2^19):
+    writes `out` (float64 [>= total_T], caller-allocated) and allocates nothing."""
+    _dev(w, torch.float64, "w")
+    _dev(xi_off, torch.int64, "xi_off")
+    _dev(out, torch.float64, "out")
+    if out.numel() < total_T:
+        raise ValueError("out needs total_T entries")
+    if err_flag is not None:
+        _dev(err_flag, torch.int32, "err_flag")
+    _check(load().pspo_design_cutoffs_noalloc(_ptr(w), _ptr(xi_off), P, total_T, float(budget), int(variant),
+                                              float(lam), _ptr(out), _ptr(err_flag), _stream()))
+    return out[:total_T]
 
 
 def mfma_loop(iters: int, blocks: int, out: Optional[torch.Tensor] = None) -> torch.Tensor:

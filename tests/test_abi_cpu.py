@@ -29,7 +29,7 @@ def _declared():
 
 def test_exports_every_declared_symbol(lib):
     names = _declared()
-    assert len(names) == 14
+    assert len(names) == 15
     for name in names:
         assert hasattr(lib, name), name
     assert sorted(pspo.exported_symbols()) == names
@@ -276,3 +276,19 @@ def test_binding_checks_gradient_shapes():
         pspo.loss_fwd_bwd(h[:3], w, i32, f, f, i32, adv, N, 0.1, 0.1, 1.0)
     with pytest.raises(ValueError, match="device tensor"):   # right shapes: the device check follows
         call(d_hidden=torch.zeros(N, d), d_w_head=torch.zeros(V, d))
+
+
+def test_design_noalloc_argument_errors(lib):
+    def call(**kw):
+        a = dict(w=FAKE, xo=FAKE, P=2, T=100, B=8.0, v=0, lam=0.0, xi=FAKE)
+        a.update(kw)
+        return lib.pspo_design_cutoffs_noalloc(a["w"], a["xo"], a["P"], a["T"], a["B"], a["v"], a["lam"], a["xi"],
+                                               None, None)
+    assert call(T=0, w=None, xi=None) == OK
+    assert call(P=0) == INVALID
+    assert call(v=4) == INVALID
+    assert call(B=-1.0) == INVALID
+    assert call(xi=None) == INVALID
+    assert call(T=2 ** 19 + 1) == UNSUPPORTED          # beyond the static scratch (8 MiB)
+    assert b"2^19" in lib.pspo_last_error()
+    assert lib.pspo_design_workspace_bytes(2 ** 19) <= 8 << 20 < lib.pspo_design_workspace_bytes(2 ** 19 + 1)
