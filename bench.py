@@ -416,12 +416,21 @@ def main():
     dense_equiv = 6.0 * N * cfg.V * cfg.d / (loss_avg * 1e-3) / 1e12
     # HBM bytes per call from the committed counter runs, only while the kernels
     # are still the ones those counters were taken on
-    traffic = None
+    traffic, counters = None, None
     if os.path.exists(TRAFFIC_FILE):
         with open(TRAFFIC_FILE) as f:
             t = json.load(f)
         if t.get("N") == N and t.get("workload") == args.workload and t.get("source_hash") == source_hash():
             traffic = t.get("bytes_per_call")
+            # rocprofv3 counters of the same kernels and batch (committed under profiles/):
+            # matrix-core busy fraction and clock of the products, and the memory-side
+            # (beyond L2) read and write volume per call as rates at this run's call time
+            counters = {"source": os.path.relpath(TRAFFIC_FILE, ROOT) + " (rocprofv3 --pmc runs of the same "
+                                                                        "kernels on this batch, not re-measured here)",
+                        "mfma_busy_pct": t.get("mfma_busy_pct"),
+                        "clock_ghz": t.get("clock_ghz"),
+                        "memory_read_GBps": t["fetch_bytes_per_call"] / (loss_avg * 1e-3) / 1e9,
+                        "memory_write_GBps": t["write_bytes_per_call"] / (loss_avg * 1e-3) / 1e9}
 
     result = {
         "metric": "prefix tokens/sec for fused LM-head PPO loss fwd+bwd; % of bf16 MFMA peak",
@@ -469,6 +478,8 @@ def main():
             "traffic": traffic,
         },
     }
+    if counters is not None:
+        result["counters"] = counters
     if keep is not None:
         result["keep_logits_control"] = dict(
             keep, pct_bf16_peak=100.0 * flops / (keep["loss_call_ms"] * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,

@@ -6,7 +6,13 @@
 //
 // Operands are K-blocked: element (r, k) of an operand with R rows per K block
 // sits at ((k / 32) * R + r) * 32 + k % 32, so the 32-deep K step of a panel of
-// consecutive rows is one contiguous block of 64-byte rows.  The caller pads
+// consecutive rows is one contiguous block of 64-byte rows.  The A operand may
+// instead be row-blocked: G rows per block (a multiple of the 384-row tile, so
+// that a tile's rows lie in one block), each block its own K-blocked array of G
+// rows, blocks `blk_stride_a` bytes apart, i.e. element (r, k) at
+// (r / G) * blk_stride_a / 2 + ((k / 32) * G + r % G) * 32 + k % 32 (the
+// layout a product writes when its output tiles are to sit in compact blocks,
+// read back as the A operand of another).  The caller pads
 // every operand: rows [0, tiles_m * 384) of A and [0, tiles_n * 256) of B must
 // be readable (their content only reaches output rows / columns the epilogue
 // masks), K % 32 == 0, and K-padding entries must be zero in both operands.
@@ -93,6 +99,10 @@ struct GemmShape {
   // of the order) instead of first: for an epilogue that does extra work on
   // those tiles only.
   int spread_m = 0;
+  // Row-blocked A (0: plain K-blocked with rows_a rows per K block): rows per
+  // block (a multiple of kTileM) and bytes between blocks.
+  int blk_a = 0;
+  int64_t blk_stride_a = 0;
 };
 
 // Accumulator (i, j, r) of lane `lane` in wave (wm, wn) holds
@@ -369,9 +379,12 @@ void gemm_nt_kernel(GemmShape g, Epi epi) {
   // logical chunk (l % 4) ^ swizzle(row) of that row's 64-byte K slice.  Wave w
   // loads A rows w*96 + q*16 (q < 6) and B rows w*64 + q*16 (q < 4).
   const uint32_t lane_off = (uint32_t)((lane >> 2) * kLdsRow + (((lane & 3) ^ chunk_swizzle(lane >> 2)) << 4));
-  const int64_t kstep_a = g.rows_a * kLdsRow, kstep_b = g.rows_b * kLdsRow;   // bytes per K step
-  const unsigned char* gA = reinterpret_cast<const unsigned char*>(g.A) +
-                            ((int64_t)tm * kTileM + wave * (kTileM / 4)) * kLdsRow + (int64_t)kb * kstep_a;
+  // bytes per K step; the wave's A rows start at gA (the tile lies inside one
+  // block of a row-blocked A)
+  const int64_t kstep_a = (g.blk_a > 0 ? (int64_t)g.blk_a : g.rows_a) * kLdsRow, kstep_b = g.rows_b * kLdsRow;
+  const int64_t ra = (int64_t)tm * kTileM + wave * (kTileM / 4);
+  const unsigned char* gA = reinterpret_cast<const unsigned char*>(g.A) + (int64_t)kb * kstep_a +
+                            (g.blk_a > 0 ? (ra / g.blk_a) * g.blk_stride_a + (ra % g.blk_a) * kLdsRow : ra * kLdsRow);
   const unsigned char* gB = reinterpret_cast<const unsigned char*>(g.B) +
                             ((int64_t)tn * kTileN + wave * (kTileN / 4)) * kLdsRow + (int64_t)kb * kstep_b;
 
@@ -466,8 +479,11 @@ void gemm_nt_kernel(GemmShape g, Epi epi) {
   // blocks into registers (A blocks 6..11 are read in groups 0..5).  With
   // nk == 0 (a device-side K bound of 0) the loads and reads still happen, at
   // K offset 0, but no MFMA consumes them and the accumulators stay zero.
+#pragma unroll
   for (int st = 0; st < kStages - 1; ++st)
+#pragma unroll
     for (int q = 0; q < kLoadsA + kLoadsB; ++q) issue_load(st, st, q);
+#pragma unroll
   for (int q = 0; q < kLoadsA; ++q) issue_load(kStages - 1, kStages - 1, q);
   stage_barrier<2 * (kLoadsA + kLoadsB) + kLoadsA>();
 #pragma unroll

@@ -54,17 +54,20 @@ constexpr float kNegInf = -INFINITY;
 // Epilogues
 // ---------------------------------------------------------------------------
 
-// One entry of the logit gradient delta (1[v = o] - exp(z - lse)) (the
-// objective of Sec. 3.1 differentiated through the log-softmax of App. D) away
-// from the target, -delta exp(z - lse), and 0 at the target (that entry is
-// added in float32 by the target-entry kernels), with lsb = lse log2(e):
-// p = exp2(min(z log2(e) - lsb, 0)) (one fma; the min keeps p <= 1 and finite
-// for padding columns, whose delta is 0).  The recomputing product and the
-// kept-logit conversion both use it, so they produce the same bits.
-__device__ __forceinline__ float logit_grad(float z, float lsb, float delta, bool is_target) {
-  const float p = __builtin_amdgcn_exp2f(fminf(fmaf(z, kLog2e, -lsb), 0.f));
-  return is_target ? 0.f : -delta * p;
+// An off-target entry of the logit gradient delta (1[v = o] - exp(z - lse))
+// (the objective of Sec. 3.1 differentiated through the log-softmax of App. D)
+// is -delta exp(z - lse).  Its magnitude is computed as exp2(z log2(e) + c)
+// with the per-column constant c = log2|delta| - lse log2(e): one fma and one
+// exp per entry (c = -inf for a padding column, whose delta is 0, gives 0);
+// its sign, that of -delta, is applied to packed bf16 pairs by XOR.  The
+// target entries are then overwritten with 0 (zero_targets_kernel): they are
+// added in float32 by the target-entry kernels.  The recomputing product and
+// the kept-logit conversion both use these, so they produce the same bits.
+__device__ __forceinline__ float grad_col_const(float lse, float delta) {
+  return delta != 0.f ? fmaf(-lse, kLog2e, log2f(fabsf(delta))) : -INFINITY;
 }
+__device__ __forceinline__ uint32_t grad_sign_bits(float delta) { return delta > 0.f ? 0x80008000u : 0u; }
+__device__ __forceinline__ float grad_mag(float z, float c) { return __builtin_amdgcn_exp2f(fmaf(z, kLog2e, c)); }
 
 // Two floats as packed bf16 (round to nearest even): one v_cvt_pk_bf16_f32.
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
@@ -262,7 +265,7 @@ __device__ __forceinline__ u32x2 quad_transpose(u32x2 p, int k) {
   return o;
 }
 
-// Backward logit gradient (without its target entries) for one vocabulary chunk:
+// Backward logit gradient (its target entries zeroed afterwards) for one vocabulary chunk:
 // rows = vocabulary rows v0 + vl (A = W[v0:]), columns = the compacted tokens
 // that carry gradient (column t < *n_dev).  Writes bf16 Delta in both K-blocked
 // layouts (vocabulary rows for dW, token rows for dH); zero outside t < *n_dev,
@@ -281,12 +284,13 @@ __device__ __forceinline__ u32x2 quad_transpose(u32x2 p, int k) {
 template <bool kFull>
 struct EpiDelta {
   int V, N, v0, tm0;
-  uint16_t* dT;          // K-blocked [Npad/32][rT][32]: rows = vocabulary entries of the chunk, K = tokens
-  int64_t rT;
-  uint16_t* dN;          // K-blocked [Vc/32][rN][32]: rows = tokens, K = vocabulary entries of the chunk
-  int64_t rN;
-  const int32_t* ctgt;   // target, lse and delta of column t (columns t < *n_dev), in column order
-  const float* clse;
+  // Both layouts row-blocked, so that each tile's values sit in a compact
+  // region (the vocabulary-major one a contiguous 192 KB block):
+  uint16_t* dT;          // [Vc/384][tkb][384][32]: rows = vocabulary entries (block = vocabulary tile), K = tokens
+  int64_t tkb;           //   token K blocks per vocabulary block (Npad / 32)
+  uint16_t* dN;          // [Npad/768][nkb][768][32]: rows = tokens (block = 3 token tiles), K = vocabulary entries
+  int64_t nkb;           //   vocabulary K blocks per token block (Vc / 32)
+  const float* clse;     // lse and delta of column t (columns t < *n_dev), in column order
   const float* cdelta;
   const int32_t* n_dev;
 
@@ -294,29 +298,29 @@ struct EpiDelta {
     const int n = min(N, __builtin_amdgcn_readfirstlane(*n_dev));
     const int tm = kFull ? tm_launch : tm0 + tm_launch;
     const int vl0 = tm * kTileM + acc_row(wm, 0, 0, lane);   // chunk rows of this lane: vl0 + i*16 + r
-    const int vbase = v0 + vl0;
+    [[maybe_unused]] const int vbase = v0 + vl0;   // (rows past V of a partial last tile are masked)
     // per-column token data of the lane's 8 columns, fetched together (one
     // round trip: the arrays are in column order)
-    float dls[kBlocksN], lss[kBlocksN];
-    int tgs[kBlocksN];
+    float cc[kBlocksN];
+    uint32_t sg[kBlocksN];
 #pragma unroll
     for (int j = 0; j < kBlocksN; ++j) {
       const int t = tn * kTileN + acc_col(wn, j, lane);
-      const bool tv = t < n;
-      dls[j] = tv ? cdelta[t] : 0.f;
-      lss[j] = tv ? clse[t] * kLog2e : 0.f;   // lse log2(e)
-      tgs[j] = tv ? ctgt[t] : -1;
+      const float dl = t < n ? cdelta[t] : 0.f;
+      cc[j] = grad_col_const(t < n ? clse[t] : 0.f, dl);
+      sg[j] = grad_sign_bits(dl);
     }
     // Store addresses: a per-tile base (uniform) plus a 32-bit byte offset per
-    // lane and block group (a tile spans 12 K blocks of the token-major layout
-    // and 8 of the vocabulary-major one, far below 4 GB).
+    // lane and block group.  The tile's 12 K blocks of the token-major layout
+    // are 16 KB pieces 48 KB apart in token block tn / 3, its 8 K blocks of the
+    // vocabulary-major layout consecutive 24 KB pieces of vocabulary block tm.
     const int k = lane & 3, q = (lane >> 2) & 3, g = lane >> 4;
     const bool qeven = (q & 1) == 0;
     unsigned char* nbase = reinterpret_cast<unsigned char*>(
-        dN + ((int64_t)(tm * (kTileM / kTileK)) * rN + tn * kTileN) * kTileK);
+        dN + (((int64_t)(tn / 3) * nkb + tm * (kTileM / kTileK)) * kTileLcm + (tn % 3) * kTileN) * kTileK);
     unsigned char* tbase = reinterpret_cast<unsigned char*>(
-        dT + ((int64_t)(tn * (kTileN / kTileK)) * rT + tm * kTileM) * kTileK);
-    const uint32_t kstepN = (uint32_t)rN * (kTileK * 2), kstepT = (uint32_t)rT * (kTileK * 2);
+        dT + ((int64_t)tm * tkb + tn * (kTileN / kTileK)) * (kTileM * kTileK));
+    const uint32_t kstepN = kTileLcm * (kTileK * 2), kstepT = kTileM * (kTileK * 2);
     // token-major: after the row swap the lane holds K entries
     // 16 (g % 2) + 8 (g / 2) .. +7 of its token wn*128 + j*16 + lane%16
     const uint32_t noff = (uint32_t)(wm * (kWaveM / kTileK)) * kstepN +
@@ -343,12 +347,11 @@ struct EpiDelta {
             float x[kAccPerBlock];
 #pragma unroll
             for (int r = 0; r < kAccPerBlock; ++r) {
-              const int v = vbase + i * 16 + r;
-              x[r] = logit_grad(acc_get(acc, i, j, r), lss[j], dls[j], v == tgs[j]);
-              if constexpr (!kFull) x[r] = (v < V) ? x[r] : 0.f;
+              x[r] = grad_mag(acc_get(acc, i, j, r), cc[j]);
+              if constexpr (!kFull) x[r] = (vbase + i * 16 + r < V) ? x[r] : 0.f;
             }
-            blk[ii][jj].x = pack_bf16x2(x[0], x[1]);
-            blk[ii][jj].y = pack_bf16x2(x[2], x[3]);
+            blk[ii][jj].x = pack_bf16x2(x[0], x[1]) ^ sg[j];
+            blk[ii][jj].y = pack_bf16x2(x[2], x[3]) ^ sg[j];
           }
         // vocabulary-major stores, one per row block
 #pragma unroll
@@ -398,7 +401,7 @@ struct EpiDelta {
 // the logit is M + offset with M the tile's per-column maximum in part_m)
 // instead of a recomputing product: the values and layouts the logit-gradient
 // epilogue writes for that chunk.  Backward column a < n = min(N, *n_dev) has
-// the target, lse and delta ctgt[a], clse[a], cdelta[a] and its logits sit in
+// the lse and delta clse[a], cdelta[a] and its logits sit in
 // forward column afwd[a]; columns n <= a < round_up(n, 32) are written as the
 // zero gradient of a padding column (the dW product reads whole 32-token K
 // steps); rows v >= V are zero.
@@ -412,11 +415,10 @@ __global__ __launch_bounds__(256) void logit_grad_kept_kernel(const uint16_t* __
                                                               int kept_cols, int Vc, int V, int N,
                                                               const int32_t* __restrict__ n_dev,
                                                               const int32_t* __restrict__ afwd,
-                                                              const int32_t* __restrict__ ctgt,
                                                               const float* __restrict__ clse,
                                                               const float* __restrict__ cdelta,
-                                                              uint16_t* __restrict__ dN, int64_t rN,
-                                                              uint16_t* __restrict__ dT, int64_t rT) {
+                                                              uint16_t* __restrict__ dN, int64_t nkb,
+                                                              uint16_t* __restrict__ dT, int64_t tkb) {
   __shared__ uint16_t tile[32][128 + 8];   // [token][entry]; padded rows: the column reads hit distinct banks
   const int n = min(N, *n_dev);
   const int a0 = blockIdx.y * 32, v0 = blockIdx.x * 128;   // Vc is a multiple of 128
@@ -433,9 +435,8 @@ __global__ __launch_bounds__(256) void logit_grad_kept_kernel(const uint16_t* __
     const u32x4 h0 = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src));
     const u32x4 h1 = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src + 8));
     const float M = part_m[vt * ldp + f];
-    const float dl = cdelta[a];
-    const float ls = clse[a] * kLog2e;   // lse log2(e), as the recomputing epilogue takes it
-    const int tg = ctgt[a];
+    const float c = grad_col_const(clse[a], cdelta[a]);   // as the recomputing epilogue takes it
+    const uint32_t sgn = grad_sign_bits(cdelta[a]);
 #pragma unroll
     for (int e2 = 0; e2 < 8; ++e2) {
       const uint32_t hb = e2 < 4 ? h0[e2] : h1[e2 - 4];
@@ -443,32 +444,52 @@ __global__ __launch_bounds__(256) void logit_grad_kept_kernel(const uint16_t* __
 #pragma unroll
       for (int u = 0; u < 2; ++u) {
         const int e = 2 * e2 + u;
-        x[u] = logit_grad(M + f16_bits_to_f32(hb >> (16 * u)), ls, dl, v + e == tg);
+        x[u] = grad_mag(M + f16_bits_to_f32(hb >> (16 * u)), c);
         if (v + e >= V) x[u] = 0.f;
       }
-      w[e2] = pack_bf16x2(x[0], x[1]);
+      w[e2] = pack_bf16x2(x[0], x[1]) ^ sgn;
     }
   }
   *reinterpret_cast<u32x4*>(&tile[al][vl]) = u32x4{w[0], w[1], w[2], w[3]};
   *reinterpret_cast<u32x4*>(&tile[al][vl + 8]) = u32x4{w[4], w[5], w[6], w[7]};
   __syncthreads();
   // token-major: token a0 + tid / 8, entries v0 + (tid % 8) * 16 .. +15
+  // (the row-blocked layout of the recomputing epilogue: blocks of 768 tokens)
   {
-    const int tl = tid >> 3, ol = (tid & 7) * 16, ov = v0 + ol;
-    uint16_t* pn = dN + ((int64_t)(ov >> 5) * rN + a0 + tl) * kTileK + (ov & 31);
+    const int tl = tid >> 3, ol = (tid & 7) * 16, ov = v0 + ol, at = a0 + tl;
+    uint16_t* pn = dN + (((int64_t)(at / kTileLcm) * nkb + (ov >> 5)) * kTileLcm + at % kTileLcm) * kTileK + (ov & 31);
     *reinterpret_cast<u32x4*>(pn) = *reinterpret_cast<const u32x4*>(&tile[tl][ol]);
     *reinterpret_cast<u32x4*>(pn + 8) = *reinterpret_cast<const u32x4*>(&tile[tl][ol + 8]);
   }
   // vocabulary-major: entry v0 + tid / 2 of tokens a0 + (tid % 2) * 16 .. +15
+  // (blocks of 384 vocabulary entries)
   {
-    const int ol = tid >> 1, ap = (tid & 1) * 16;
+    const int ol = tid >> 1, ap = (tid & 1) * 16, vv = v0 + ol;
     uint32_t q[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e)
       q[e] = (uint32_t)tile[ap + 2 * e][ol] | ((uint32_t)tile[ap + 2 * e + 1][ol] << 16);
-    uint16_t* pt = dT + ((int64_t)(a0 >> 5) * rT + v0 + ol) * kTileK + ap;
+    uint16_t* pt = dT + (((int64_t)(vv / kTileM) * tkb + (a0 >> 5)) * kTileM + vv % kTileM) * kTileK + ap;
     *reinterpret_cast<u32x4*>(pt) = u32x4{q[0], q[1], q[2], q[3]};
     *reinterpret_cast<u32x4*>(pt + 8) = u32x4{q[4], q[5], q[6], q[7]};
+  }
+}
+
+// The target entries of one chunk's logit-gradient layouts (the columns whose
+// target lies in vocabulary rows [v0, v0 + vc)) set to 0: those entries are
+// applied in float32 by the target-entry kernels.  Backward column a <
+// min(N, *n_dev); the row-blocked layouts of EpiDelta (token blocks of 768,
+// vocabulary blocks of 384).
+__global__ __launch_bounds__(256) void zero_targets_kernel(int N, const int32_t* __restrict__ n_dev,
+                                                           const int32_t* __restrict__ ctgt, int v0, int vc,
+                                                           uint16_t* __restrict__ dN, int64_t nkb,
+                                                           uint16_t* __restrict__ dT, int64_t tkb) {
+  const int n = min(N, *n_dev);
+  for (int a = blockIdx.x * 256 + threadIdx.x; a < n; a += gridDim.x * 256) {
+    const int vl = ctgt[a] - v0;
+    if (vl < 0 || vl >= vc) continue;
+    dN[(((int64_t)(a / kTileLcm) * nkb + (vl >> 5)) * kTileLcm + a % kTileLcm) * kTileK + (vl & 31)] = 0;
+    dT[(((int64_t)(vl / kTileM) * tkb + (a >> 5)) * kTileM + vl % kTileM) * kTileK + (a & 31)] = 0;
   }
 }
 
@@ -963,11 +984,11 @@ __global__ __launch_bounds__(256) void onehot_dh_kernel(int N, int d, const int3
   }
 }
 
-// The dW side groups the backward columns by target id.  Stable bucketing in
-// four launches, every result independent of scheduling:
+// The dW side groups the backward columns by target id.  Stable bucketing,
+// every result independent of scheduling:
 //   count:  cnt[v] = #{a : ctgt[a] = v}                    (integer atomics)
 //   scan:   start[v] = sum_{u < v} cnt[u]; cursor = start;   the non-empty ids
-//           in increasing order in rows[0 .. *nrows)
+//           in increasing order in rows[0 .. *nrows)        (three launches)
 //   fill:   each column takes a slot of its bucket           (arbitrary order)
 //   rank:   column a goes to start[v] + #{b in bucket v : b < a} of `sorted`,
 //           i.e. the bucket in increasing column order.
@@ -981,45 +1002,100 @@ __global__ __launch_bounds__(256) void onehot_count_kernel(int N, const int32_t*
   for (int a = blockIdx.x * 256 + threadIdx.x; a < n; a += gridDim.x * 256) atomicAdd(&cnt[ctgt[a]], 1);
 }
 
-constexpr int kScanThreads = 1024;
+// The scan in three launches over blocks of kScanSpan ids (256 threads x 16
+// consecutive ids each): per-block totals of cnt and of non-empty ids; their
+// exclusive scan (one work-group, 256 blocks at a time); then each block's
+// outputs from its offsets and a work-group scan of its threads' totals.
+constexpr int kScanPer = 16, kScanSpan = 256 * kScanPer;
 
-// One work-group: thread k scans ids [k s, (k + 1) s), s = ceil(V / 1024), in
-// two passes (its own totals, then the outputs after a work-group scan of them).
-__global__ __launch_bounds__(kScanThreads) void onehot_scan_kernel(int V, const int32_t* __restrict__ cnt,
-                                                                   int32_t* __restrict__ start,
-                                                                   int32_t* __restrict__ cursor,
-                                                                   int32_t* __restrict__ rows,
-                                                                   int32_t* __restrict__ nrows) {
-  __shared__ int sh_c[kScanThreads], sh_r[kScanThreads];
-  const int tid = threadIdx.x;
-  const int span = (V + kScanThreads - 1) / kScanThreads;
-  const int v0 = min(V, tid * span), v1 = min(V, v0 + span);
+// Exclusive scan of one value per thread over a 256-thread work-group; also
+// returns the work-group total.
+__device__ int block_exclusive_scan(int v, int* sh, int& total) {
+  sh[threadIdx.x] = v;
+  __syncthreads();
+  for (int off = 1; off < 256; off <<= 1) {
+    const int a = threadIdx.x >= off ? sh[threadIdx.x - off] : 0;
+    __syncthreads();
+    sh[threadIdx.x] += a;
+    __syncthreads();
+  }
+  total = sh[255];
+  const int r = sh[threadIdx.x] - v;
+  __syncthreads();
+  return r;
+}
+
+__global__ __launch_bounds__(256) void onehot_scan_totals_kernel(int V, const int32_t* __restrict__ cnt,
+                                                                 int32_t* __restrict__ tot) {
+  __shared__ int sh[256];
+  const int v0 = blockIdx.x * kScanSpan + threadIdx.x * kScanPer;
   int c = 0, r = 0;
-  for (int v = v0; v < v1; ++v) {
-    const int k = cnt[v];
+#pragma unroll
+  for (int e = 0; e < kScanPer; ++e) {
+    const int k = v0 + e < V ? cnt[v0 + e] : 0;
     c += k;
     r += k > 0 ? 1 : 0;
   }
-  sh_c[tid] = c;
-  sh_r[tid] = r;
-  __syncthreads();
-  for (int off = 1; off < kScanThreads; off <<= 1) {   // inclusive scans
-    const int ac = tid >= off ? sh_c[tid - off] : 0, ar = tid >= off ? sh_r[tid - off] : 0;
-    __syncthreads();
-    sh_c[tid] += ac;
-    sh_r[tid] += ar;
-    __syncthreads();
+  int tc, tr;
+  block_exclusive_scan(c, sh, tc);
+  block_exclusive_scan(r, sh, tr);
+  if (threadIdx.x == 0) {
+    tot[2 * blockIdx.x] = tc;
+    tot[2 * blockIdx.x + 1] = tr;
   }
-  c = sh_c[tid] - c;
-  r = sh_r[tid] - r;
-  for (int v = v0; v < v1; ++v) {
-    const int k = cnt[v];
-    start[v] = c;
-    cursor[v] = c;
-    if (k > 0) rows[r++] = v;
-    c += k;
+}
+
+// One work-group: tot (a pair per block) -> exclusive offsets in place; the
+// number of non-empty ids to *nrows.
+__global__ __launch_bounds__(256) void onehot_scan_offsets_kernel(int nblk, int32_t* __restrict__ tot,
+                                                                  int32_t* __restrict__ nrows) {
+  __shared__ int sh[256];
+  int base_c = 0, base_r = 0;
+  for (int b0 = 0; b0 < nblk; b0 += 256) {
+    const int b = b0 + threadIdx.x;
+    const int c = b < nblk ? tot[2 * b] : 0, r = b < nblk ? tot[2 * b + 1] : 0;
+    int tc, tr;
+    const int ec = block_exclusive_scan(c, sh, tc);
+    const int er = block_exclusive_scan(r, sh, tr);
+    if (b < nblk) {
+      tot[2 * b] = base_c + ec;
+      tot[2 * b + 1] = base_r + er;
+    }
+    base_c += tc;
+    base_r += tr;
   }
-  if (tid == kScanThreads - 1) *nrows = sh_r[kScanThreads - 1];
+  if (threadIdx.x == 0) *nrows = base_r;
+}
+
+// start[v] = sum_{u < v} cnt[u]; cursor = start; the non-empty ids in
+// increasing order in rows.
+__global__ __launch_bounds__(256) void onehot_scan_write_kernel(int V, const int32_t* __restrict__ cnt,
+                                                                const int32_t* __restrict__ off,
+                                                                int32_t* __restrict__ start,
+                                                                int32_t* __restrict__ cursor,
+                                                                int32_t* __restrict__ rows) {
+  __shared__ int sh[256];
+  const int v0 = blockIdx.x * kScanSpan + threadIdx.x * kScanPer;
+  int k[kScanPer];
+  int c = 0, r = 0;
+#pragma unroll
+  for (int e = 0; e < kScanPer; ++e) {
+    k[e] = v0 + e < V ? cnt[v0 + e] : 0;
+    c += k[e];
+    r += k[e] > 0 ? 1 : 0;
+  }
+  int tc, tr;
+  c = off[2 * blockIdx.x] + block_exclusive_scan(c, sh, tc);
+  r = off[2 * blockIdx.x + 1] + block_exclusive_scan(r, sh, tr);
+#pragma unroll
+  for (int e = 0; e < kScanPer; ++e) {
+    if (v0 + e < V) {
+      start[v0 + e] = c;
+      cursor[v0 + e] = c;
+      if (k[e] > 0) rows[r++] = v0 + e;
+      c += k[e];
+    }
+  }
 }
 
 __global__ __launch_bounds__(256) void onehot_fill_kernel(int N, const int32_t* __restrict__ n_dev,
@@ -1111,7 +1187,7 @@ struct Plan {
   int64_t Dk;   // K of the products over the hidden features: d rounded up to 32 (zero padding)
   int64_t off_pm, off_pl, off_zt, off_lse, off_delta, off_fidx, off_fpos, off_nfwd, off_idx, off_nact, off_afwd,
       off_ctgt, off_clse, off_cdelta, off_cg1, off_ftgt, off_cnt, off_blk, off_wk, off_hk, off_ht, off_wt, off_dn, off_dt,
-      off_slab, off_zk, off_oh_cnt, off_oh_start, off_oh_cursor, off_oh_rows, off_oh_nrows, off_oh_tmp,
+      off_slab, off_zk, off_oh_cnt, off_oh_start, off_oh_cursor, off_oh_rows, off_oh_nrows, off_oh_tot, off_oh_tmp,
       off_oh_sorted, total;
   bool keep;   // the forward keeps the first chunk's logits (fp16 offsets from the tile maxima)
 };
@@ -1167,8 +1243,8 @@ Plan make_plan(int64_t N, int64_t d, int64_t V, bool keep) {
   p.off_hk = take(d64 * p.Npad * 2);                                  // gathered hidden rows [d64/32][Npad][32]
   p.off_ht = take(p.dpad * p.Npad * 2);                               // H[bwd]^T [Npad/32][dpad][32]
   p.off_wt = take(p.dpad * ((p.Vpad + p.Vc - 1) / p.Vc) * p.Vc * 2);  // per chunk: W^T [Vc/32][dpad][32]
-  p.off_dn = take(p.Npad * p.Vc * 2);                                 // K-blocked [Vc/32][Npad][32]
-  p.off_dt = take(p.Vc * p.Npad * 2);                                 // K-blocked [Npad/32][Vc][32]
+  p.off_dn = take(p.Npad * p.Vc * 2);                                 // [Npad/768][Vc/32][768][32] (token blocks)
+  p.off_dt = take(p.Vc * p.Npad * 2);                                 // [Vc/384][Npad/32][384][32] (vocabulary blocks)
   p.off_slab = take((int64_t)kNumXcd * kTailSlots * kTileM * kTileN * 4);   // K parts of tail tiles
   p.keep = keep;
   p.off_zk = take(keep ? p.Vc * p.Npad * 2 : 0);                      // kept fp16 logit offsets, one block per forward tile
@@ -1177,6 +1253,7 @@ Plan make_plan(int64_t N, int64_t d, int64_t V, bool keep) {
   p.off_oh_cursor = take(V * 4);
   p.off_oh_rows = take(V * 4);                                        //   non-empty ids and their count,
   p.off_oh_nrows = take(4);
+  p.off_oh_tot = take((V + kScanSpan - 1) / kScanSpan * 8);           //   per-block totals of the scan
   p.off_oh_tmp = take(p.Npad * 4);                                    //   buckets unordered, then in column order
   p.off_oh_sorted = take(p.Npad * 4);
   p.total = o;
@@ -1300,6 +1377,7 @@ int pspo_loss_fwd_bwd(const uint16_t* hidden, const uint16_t* w_head, const int3
   int32_t* oh_cursor = reinterpret_cast<int32_t*>(ws + pl.off_oh_cursor);
   int32_t* oh_rows = reinterpret_cast<int32_t*>(ws + pl.off_oh_rows);
   int32_t* oh_nrows = reinterpret_cast<int32_t*>(ws + pl.off_oh_nrows);
+  int32_t* oh_tot = reinterpret_cast<int32_t*>(ws + pl.off_oh_tot);
   int32_t* oh_tmp = reinterpret_cast<int32_t*>(ws + pl.off_oh_tmp);
   int32_t* oh_sorted = reinterpret_cast<int32_t*>(ws + pl.off_oh_sorted);
   const int Dk = (int)pl.Dk;
@@ -1375,8 +1453,8 @@ int pspo_loss_fwd_bwd(const uint16_t* hidden, const uint16_t* w_head, const int3
     const int ctiles = (int)(vc / kTileM);
     if (v0 == 0 && zk != nullptr) {
       hipLaunchKernelGGL(logit_grad_kept_kernel, dim3((unsigned)(pl.Vc / 128), (unsigned)(pl.Npad / 32)), dim3(256), 0,
-                         stream, zk, part_m, pl.Npad, tiles_tok_n, (int)pl.Vc, V, N, n_act, act_fwd, act_tgt, act_lse,
-                         act_delta, dN, pl.Npad, dT, pl.Vc);
+                         stream, zk, part_m, pl.Npad, tiles_tok_n, (int)pl.Vc, V, N, n_act, act_fwd, act_lse,
+                         act_delta, dN, pl.Vc / kTileK, dT, pl.Npad / kTileK);
       PSPO_HIP_CHECK(hipGetLastError());
     } else {
       // the chunk's vocabulary tiles whose rows are all token ids, then a
@@ -1385,25 +1463,30 @@ int pspo_loss_fwd_bwd(const uint16_t* hidden, const uint16_t* w_head, const int3
       const int tfull = (int)(rows / kTileM);
       if (tfull > 0) {
         GemmShape g{wk + v0 * kTileK, pl.Vpad, tfull * kTileM, hk, pl.Npad, N, Dk, tfull, tiles_tok_n, n_act, kDynN};
-        EpiDelta<true> e{V, N, (int)v0, 0, dT, pl.Vc, dN, pl.Npad, act_tgt, act_lse, act_delta, n_act};
+        EpiDelta<true> e{V, N, (int)v0, 0, dT, pl.Npad / kTileK, dN, pl.Vc / kTileK, act_lse, act_delta, n_act};
         if (int rc = launch_gemm(g, e, stream)) return rc;
       }
       if (tfull < ctiles) {
         const int64_t vp = v0 + (int64_t)tfull * kTileM;   // first row of the partial tile
         GemmShape g{wk + vp * kTileK, pl.Vpad, (int)(V - vp), hk, pl.Npad, N, Dk, 1, tiles_tok_n, n_act, kDynN};
-        EpiDelta<false> e{V, N, (int)v0, tfull, dT, pl.Vc, dN, pl.Npad, act_tgt, act_lse, act_delta, n_act};
+        EpiDelta<false> e{V, N, (int)v0, tfull, dT, pl.Npad / kTileK, dN, pl.Vc / kTileK, act_lse, act_delta,
+                          n_act};
         if (int rc = launch_gemm(g, e, stream)) return rc;
       }
     }
+    hipLaunchKernelGGL(zero_targets_kernel, dim3((unsigned)std::min<int64_t>((pl.Npad + 255) / 256, 1024)), dim3(256),
+                       0, stream, N, n_act, act_tgt, (int)v0, (int)vc, dN, pl.Vc / kTileK, dT, pl.Npad / kTileK);
+    PSPO_HIP_CHECK(hipGetLastError());
     {
-      GemmShape g{dT, pl.Vc, (int)vc, hT, pl.dpad, d, (int)pl.Npad, ctiles, tiles_d, n_act, kDynK};
+      GemmShape g{dT, pl.Vc, (int)vc, hT, pl.dpad, d, (int)pl.Npad, ctiles, tiles_d, n_act, kDynK, 0,
+                  kTileM, pl.Npad * kTileM * 2};
       EpiDW e{V, d, (int)v0, d_w_head, accumulate};
       if (int rc = launch_gemm_split_tail(g, e, TailDW{V, d, (int)v0, d_w_head, accumulate}, slab, stream))
         return rc;
     }
     {
       GemmShape g{dN, pl.Npad, (int)pl.Npad, wT + (v0 / pl.Vc) * pl.dpad * pl.Vc, pl.dpad, d, (int)vc, tiles_tok_m,
-                  tiles_d, n_act, kDynM};
+                  tiles_d, n_act, kDynM, 0, kTileLcm, pl.Vc * kTileLcm * 2};
       EpiDH e{N, d, d_hidden, v0 == 0, act_idx, n_act};
       if (int rc = launch_gemm_split_tail(g, e, TailDH{N, d, d_hidden, v0 == 0, act_idx, n_act}, slab, stream))
         return rc;
@@ -1419,8 +1502,13 @@ int pspo_loss_fwd_bwd(const uint16_t* hidden, const uint16_t* w_head, const int3
     PSPO_HIP_CHECK(hipGetLastError());
     hipLaunchKernelGGL(onehot_count_kernel, dim3(gcols), dim3(256), 0, stream, N, n_act, act_tgt, oh_cnt);
     PSPO_HIP_CHECK(hipGetLastError());
-    hipLaunchKernelGGL(onehot_scan_kernel, dim3(1), dim3(kScanThreads), 0, stream, V, oh_cnt, oh_start, oh_cursor,
-                       oh_rows, oh_nrows);
+    const unsigned nscan = (unsigned)((V + kScanSpan - 1) / kScanSpan);
+    hipLaunchKernelGGL(onehot_scan_totals_kernel, dim3(nscan), dim3(256), 0, stream, V, oh_cnt, oh_tot);
+    PSPO_HIP_CHECK(hipGetLastError());
+    hipLaunchKernelGGL(onehot_scan_offsets_kernel, dim3(1), dim3(256), 0, stream, (int)nscan, oh_tot, oh_nrows);
+    PSPO_HIP_CHECK(hipGetLastError());
+    hipLaunchKernelGGL(onehot_scan_write_kernel, dim3(nscan), dim3(256), 0, stream, V, oh_cnt, oh_tot, oh_start,
+                       oh_cursor, oh_rows);
     PSPO_HIP_CHECK(hipGetLastError());
     hipLaunchKernelGGL(onehot_fill_kernel, dim3(gcols), dim3(256), 0, stream, N, n_act, act_tgt, oh_cursor, oh_tmp);
     PSPO_HIP_CHECK(hipGetLastError());
