@@ -49,9 +49,11 @@
 // One dimension can be bounded by a count that lives in device memory (a
 // product over a data-dependent subset of tokens needs no host round trip).
 // Work-group -> tile mapping is XCD-aware: work-groups are dispatched
-// round-robin over the 8 XCDs, so consecutive tile ids go to the same XCD, in
-// a grouped order (4 A-tiles x 8 B-tiles resident per XCD round) for reuse
-// inside each XCD's private L2.
+// round-robin over the 8 XCDs, so work-groups b, b + 8, b + 16, ... share an
+// XCD; each XCD runs its share of a grouped order (4 A-tiles x 8 B-tiles
+// resident per XCD round) for reuse inside its private L2, and the groups are
+// dealt to the XCDs so that all eight read the same B panels at the same time
+// (shared through the memory-side cache).
 #pragma once
 
 #include "common.h"
@@ -94,10 +96,9 @@ struct GemmShape {
   // Tiles outside the bound exit at once; a shorter K shortens the loop.
   const int32_t* dyn = nullptr;
   int dyn_dim = kDynNone;
-  // Row tiles 0 .. spread_m-1 are placed evenly among the others in launch
-  // order (and so spread over the XCDs, each of which takes a contiguous run
-  // of the order) instead of first: for an epilogue that does extra work on
-  // those tiles only.
+  // Row tiles 0 .. spread_m-1 are placed evenly among the others in the
+  // grouped order (and so spread over the XCDs and their rounds) instead of
+  // first: for an epilogue that does extra work on those tiles only.
   int spread_m = 0;
   // Row-blocked A (0: plain K-blocked with rows_a rows per K block): rows per
   // block (a multiple of kTileM) and bytes between blocks.
@@ -199,19 +200,41 @@ __device__ __forceinline__ void bounded_dims(const GemmShape& g, int& M, int& N,
   }
 }
 
-// The tiles of a product bounded to M x N (tiles_m/n: the launch's extents);
-// each XCD runs the contiguous run of per_xcd positions of the grouped order
-// that starts at its index times per_xcd.
+// The tiles of a product bounded to M x N (tiles_m/n: the launch's extents),
+// and which positions of the grouped order each XCD runs: the whole groups
+// (kGroupM row tiles x all column tiles) that divide evenly among the XCDs are
+// dealt round-robin, group g to XCD g % 8, so that at any time every XCD works
+// on the same column tiles (the memory-side cache then serves the column
+// panels to all eight from one fetch); the positions left over are split into
+// contiguous runs of per_rest.  Each XCD runs at most per_xcd positions.
 struct TileGrid {
   int tiles_m, tiles_n, total, per_xcd;
+  int width;       // positions per group
+  int per_dealt;   // positions of the dealt groups per XCD
+  int rest0;       // first position after the dealt groups
+  int per_rest;    // positions of the remainder per XCD (the last run may be shorter)
 };
 __host__ __device__ inline TileGrid tile_grid(int tiles_m, int tiles_n, int M, int N) {
   TileGrid tg;
   tg.tiles_m = min(tiles_m, (M + kTileM - 1) / kTileM);
   tg.tiles_n = min(tiles_n, (N + kTileN - 1) / kTileN);
   tg.total = tg.tiles_m * tg.tiles_n;
-  tg.per_xcd = (tg.total + kNumXcd - 1) / kNumXcd;
+  tg.width = kGroupM * tg.tiles_n;
+  const int dealt = tg.tiles_m / kGroupM / kNumXcd * kNumXcd;
+  tg.per_dealt = dealt / kNumXcd * tg.width;
+  tg.rest0 = dealt * tg.width;
+  tg.per_rest = (tg.total - tg.rest0 + kNumXcd - 1) / kNumXcd;
+  tg.per_xcd = tg.per_dealt + tg.per_rest;   // = ceil(total / 8)
   return tg;
+}
+// Number of positions XCD x runs.
+__host__ __device__ inline int xcd_count(const TileGrid& tg, int x) {
+  return tg.per_dealt + min(max(tg.total - tg.rest0 - x * tg.per_rest, 0), tg.per_rest);
+}
+// Grouped-order position of XCD x's k-th tile (k < xcd_count(tg, x)).
+__host__ __device__ inline int xcd_position(const TileGrid& tg, int x, int k) {
+  if (k < tg.per_dealt) return ((k / tg.width) * kNumXcd + x) * tg.width + k % tg.width;
+  return tg.rest0 + x * tg.per_rest + (k - tg.per_dealt);
 }
 // Tile (tm, tn) at position t of the grouped order (kGroupM row tiles x all
 // column tiles per group).
@@ -225,8 +248,8 @@ __host__ __device__ inline void tile_at(const TileGrid& tg, int t, int spread_m,
   if (spread_m > 0) tm = spread_row_tile(tm, min(spread_m, tg.tiles_m), tg.tiles_m);
 }
 
-// How a launch covers the tiles.  A run of per_xcd positions on an XCD's 32
-// CUs that is no multiple of 32 ends in a partial round of whole tiles; a
+// How a launch covers the tiles.  An XCD's share of up to per_xcd positions on
+// its 32 CUs that is no multiple of 32 ends in a partial round of whole tiles; a
 // product with long tiles can instead run its whole rounds in one launch and
 // the rest, split along K, in a second one whose parts fill the CUs.
 enum : int {
@@ -240,12 +263,10 @@ constexpr int kTailSlots = 64;   // work-groups per XCD of a tail launch (two ro
 __host__ __device__ inline bool map_tile_at(int bid, int tiles_m, int tiles_n, int M, int N, int& tm, int& tn,
                                             int spread_m, bool rounds_only) {
   const TileGrid tg = tile_grid(tiles_m, tiles_n, M, N);
-  const int k = bid / kNumXcd;
-  if (k >= tg.per_xcd) return false;
+  const int x = bid % kNumXcd, k = bid / kNumXcd;
+  if (k >= xcd_count(tg, x)) return false;
   if (rounds_only && k >= tg.per_xcd / 32 * 32) return false;
-  const int t = (bid % kNumXcd) * tg.per_xcd + k;
-  if (t >= tg.total) return false;
-  tile_at(tg, t, spread_m, tm, tn);
+  tile_at(tg, xcd_position(tg, x, k), spread_m, tm, tn);
   return true;
 }
 __device__ __forceinline__ bool map_tile(int tiles_m, int tiles_n, int M, int N, int& tm, int& tn,
@@ -284,12 +305,12 @@ __host__ __device__ inline bool map_tail(const TileGrid& tg, int bid, int nk, in
                                          int* u_out = nullptr, int* parts_out = nullptr) {
   const int x = bid % kNumXcd, k = bid / kNumXcd;
   const int full = tg.per_xcd / 32 * 32;
-  const int r = min(tg.per_xcd, tg.total - x * tg.per_xcd) - full;
+  const int r = xcd_count(tg, x) - full;
   if (r <= 0 || k >= kTailSlots) return false;
   const int parts = tail_parts(r, nk);
   const int u = k / parts, part = k % parts;
   if (u >= r) return false;
-  tile_at(tg, x * tg.per_xcd + full + u, 0, tm, tn);
+  tile_at(tg, xcd_position(tg, x, full + u), 0, tm, tn);
   kb = part * nk / parts;
   ke = (part + 1) * nk / parts;
   if (u_out) *u_out = u;

@@ -858,11 +858,11 @@ __global__ __launch_bounds__(256) void tail_reduce_kernel(GemmShape g, const flo
   const TileGrid tg = tile_grid(g.tiles_m, g.tiles_n, M, N);
   const int x = blockIdx.y % kNumXcd, u = blockIdx.y / kNumXcd;
   const int full = tg.per_xcd / 32 * 32;
-  const int r = min(tg.per_xcd, tg.total - x * tg.per_xcd) - full;
+  const int r = xcd_count(tg, x) - full;
   if (u >= r) return;
   const int parts = tail_parts(r, K / kTileK);
   int tm, tn;
-  tile_at(tg, x * tg.per_xcd + full + u, 0, tm, tn);
+  tile_at(tg, xcd_position(tg, x, full + u), 0, tm, tn);
   const int rb = blockIdx.x, tid = threadIdx.x;
   // the slab layout [24 blocks of 16 rows][256 columns][16]: column tid of row
   // block rb is 16 consecutive floats

@@ -4,7 +4,8 @@ The functions that place tiles on work-groups (the spread row order, whole and
 whole-rounds launches, the K-split tail) are host-and-device code in gemm.h;
 tile_map_check.cpp compiles them for the host and checks that every tile is
 covered exactly once, that each tail tile's K parts partition its K steps, and
-that the spread order is a bijection keeping its first tiles in order.
+that the spread order is a bijection keeping its first tiles in order, and
+that the groups dealt to the XCDs keep all eight on the same column tiles.
 """
 import os
 import shutil

@@ -1,5 +1,6 @@
 // Host build of the product kernel's tile placement (gemm.h): checks the
-// spread row order, whole and whole-rounds launches plus K-split tails.
+// spread row order, whole and whole-rounds launches plus K-split tails, and
+// that the dealt groups keep the XCDs on the same column tiles.
 // Prints "ok" and exits 0, or names the first failing case and exits 1.
 #include <algorithm>
 #include <cstdio>
@@ -66,9 +67,24 @@ static int check_launches(int tiles_m, int tiles_n, int M, int N, int nk) {
     }
     if (pos != nk) return fail("K end", kv.first.first, kv.first.second, pos);
   }
+  int sum = 0;
   for (int x = 0; x < kNumXcd; ++x) {
-    const int r = std::min(tg.per_xcd, tg.total - x * tg.per_xcd) - tg.per_xcd / 32 * 32;
+    const int c = xcd_count(tg, x);
+    sum += c;
+    if (c > tg.per_xcd) return fail("positions per XCD", tiles_m, tiles_n, c);
+    const int r = c - tg.per_xcd / 32 * 32;
     if (r > 31) return fail("tail tiles per XCD", tiles_m, tiles_n, r);
+  }
+  if (sum != tg.total) return fail("positions of all XCDs", tiles_m, tiles_n, sum);
+  // the dealt groups: at every slot k all eight XCDs run the same column tile
+  for (int k = 0; k < tg.per_dealt; ++k) {
+    int tm0, tn0;
+    tile_at(tg, xcd_position(tg, 0, k), 0, tm0, tn0);
+    for (int x = 1; x < kNumXcd; ++x) {
+      int tm, tn;
+      tile_at(tg, xcd_position(tg, x, k), 0, tm, tn);
+      if (tn != tn0 || tm == tm0) return fail("dealt groups aligned", tiles_m, tiles_n, k);
+    }
   }
   return 0;
 }
