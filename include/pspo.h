@@ -24,7 +24,12 @@
  *    which argument).  Errors only the device can see (a target id outside
  *    [0, V), an invalid xi table, a capacity overflow) are OR-ed into the
  *    optional device word `err_flag` (PSPO_DEVERR_* bits); the call does not
- *    synchronise to report them.
+ *    synchronise to report them.  A kernel launch that fails returns
+ *    PSPO_ERR_HIP naming the kernel.
+ *  - Debug mode: with the environment variable PSPO_DEBUG set (to anything
+ *    but "" or "0"; read at every launch) every call synchronises its stream
+ *    after each kernel and returns PSPO_ERR_HIP naming the kernel whose
+ *    execution failed.  Results are the same bits as without it.
  *  - bf16 tensors are passed as their raw 16-bit patterns (uint16_t).
  *  - Rollouts are prompt-major: completion k of prompt p is r = p*K + k.
  */
@@ -186,7 +191,11 @@ size_t pspo_loss_workspace_bytes(int32_t N, int32_t d, int32_t V, uint32_t flags
  *  target     device, int32 [N]; logp_old, weight: device float32 [N];
  *  seq_id     device, int32 [N] in [0, R);  advantage: device float32 [R].
  *  N >= 0, R >= 1 if N > 0, V >= 1, d > 0 with d % 8 == 0.  All device
- *  pointers 16-byte aligned.
+ *  pointers 16-byte aligned.  Size limits (PSPO_ERR_UNSUPPORTED beyond them):
+ *  N rounded up to 768, V rounded up to 384, and d each at most 2097120
+ *  (65535 x 32: the operand copies put 32-row blocks on the grid's y axis);
+ *  device memory binds first (about 240 KB of workspace and buffers per
+ *  token at d = 3584, V = 152064).
  *  eps_low, eps_high in [0, 1); loss_scale finite (e.g. 1/(P*K)).
  *  flags      PSPO_ACCUMULATE_DW | PSPO_KEEP_LOGITS or 0.
  *  loss       device, float64 [1] out.
@@ -236,6 +245,8 @@ size_t pspo_score_proxy_workspace_bytes(int32_t N, int32_t d, int32_t V);
  *  hidden     device, bf16 bits [N, d] row-major; w_head: device, bf16 bits [V, d].
  *  target     device, int32 [N]: the generated token of each row.
  *  N >= 0, V >= 1, d > 0 with d % 8 == 0; device pointers 16-byte aligned.
+ *  N rounded up to 256, V rounded up to 384, and d each at most 2097120
+ *  (PSPO_ERR_UNSUPPORTED beyond).
  *  gamma      device, float32 [N] out.
  *  logp       device, float32 [N] out, or NULL: log p_i(o_i) (the old-policy
  *             log-probs the update later consumes).

@@ -1,6 +1,9 @@
-// Status strings, thread-local error detail, device check and host-side
-// validation of survival tables.
+// Status strings, thread-local error detail, device check, the check after
+// every launch (with the PSPO_DEBUG mode) and host-side validation of
+// survival tables.
 #include <cmath>
+#include <cstdlib>
+#include <cstring>
 #include <mutex>
 #include <string>
 
@@ -28,6 +31,22 @@ int require_gfx950() {
   });
   if (err != hipSuccess) return fail(PSPO_ERR_HIP, std::string("hipGetDeviceProperties: ") + hipGetErrorString(err));
   if (!is_gfx950[dev]) return fail(PSPO_ERR_UNSUPPORTED, "libpspo kernels are built for gfx950 (MI355X) only");
+  return PSPO_OK;
+}
+
+bool debug_mode() {
+  const char* v = std::getenv("PSPO_DEBUG");
+  return v != nullptr && v[0] != '\0' && std::strcmp(v, "0") != 0;
+}
+
+int after_launch(const char* kernel, hipStream_t stream) {
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(PSPO_ERR_HIP, std::string(kernel) + " (launch): " + hipGetErrorString(e));
+  if (debug_mode()) {
+    e = hipStreamSynchronize(stream);
+    if (e == hipSuccess) e = hipGetLastError();
+    if (e != hipSuccess) return fail(PSPO_ERR_HIP, std::string(kernel) + " (PSPO_DEBUG): " + hipGetErrorString(e));
+  }
   return PSPO_OK;
 }
 

@@ -36,9 +36,26 @@ inline int fail(int code, const std::string& msg) {
 // The kernels are written for CDNA4 (gfx950) only; this checks the current device.
 int require_gfx950();
 
+// After every kernel launch: a launch error returns PSPO_ERR_HIP naming the
+// kernel.  In the debug mode (the environment variable PSPO_DEBUG set to
+// anything but "" or "0", read at every launch) the stream is also
+// synchronised and an execution error is returned the same way, so a failing
+// kernel is named where it happens; every call then runs synchronously.
+bool debug_mode();
+int after_launch(const char* kernel, hipStream_t stream);
+#define PSPO_LAUNCHED(kernel, stream)                                   \
+  do {                                                                  \
+    if (int rc_ = ::pspo::after_launch((kernel), (stream))) return rc_; \
+  } while (0)
+
 inline bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
 inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
+
+// The K-blocked copies (layout.h) put an operand's 32-row blocks on the grid's
+// y axis, which holds at most 65535 work-groups: token and vocabulary counts
+// are supported up to this many rows after padding to whole tiles.
+constexpr int64_t kMaxPaddedRows = 65535LL * 32;
 
 // ---- device vector types ---------------------------------------------------
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));

@@ -277,7 +277,7 @@ int launch_design(const double* w, const int64_t* xi_off, int32_t P, int64_t tot
   double* bval = reinterpret_cast<double*>(ws + 2 * round_up(total_T * 4, 256));
   hipLaunchKernelGGL(design_cutoffs_kernel, dim3((unsigned)P), dim3(64), 0, stream, w, xi_off, budget, variant,
                      lambda, xi, bstart, blen, bval, err_flag);
-  PSPO_HIP_CHECK(hipGetLastError());
+  PSPO_LAUNCHED("design_cutoffs_kernel", stream);
   return PSPO_OK;
 }
 
@@ -338,7 +338,7 @@ int pspo_design_weights(const float* gamma, const int32_t* topk_ids, const float
   PSPO_REQUIRE(blocks <= INT32_MAX, PSPO_ERR_UNSUPPORTED, "problem too large");
   hipLaunchKernelGGL(design_weights_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, gamma, topk_ids, topk_logp,
                      topk, lengths, full_off, rewards, xi_off, P, K, total_T, w, gamma_bar, u, err_flag);
-  PSPO_HIP_CHECK(hipGetLastError());
+  PSPO_LAUNCHED("design_weights_kernel", stream);
   return PSPO_OK;
 }
 

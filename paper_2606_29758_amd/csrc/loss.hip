@@ -703,10 +703,10 @@ int launch_compact(int N, const Keep& keep, int32_t* cnt, int32_t* idx, int32_t*
                    int32_t* mapped, int32_t* count, double* stats, hipStream_t stream) {
   const unsigned nblk = (unsigned)((N + kCompactSpan - 1) / kCompactSpan);
   hipLaunchKernelGGL(compact_count_kernel<Keep>, dim3(nblk), dim3(kCompactThreads), 0, stream, N, keep, cnt);
-  PSPO_HIP_CHECK(hipGetLastError());
+  PSPO_LAUNCHED("compact_count_kernel", stream);
   hipLaunchKernelGGL(compact_scatter_kernel<Keep>, dim3(nblk), dim3(kCompactThreads), 0, stream, N, keep, cnt, idx,
                      pos, map, mapped, count, stats);
-  PSPO_HIP_CHECK(hipGetLastError());
+  PSPO_LAUNCHED("compact_scatter_kernel", stream);
   return PSPO_OK;
 }
 
@@ -1264,7 +1264,7 @@ template <class Epi>
 int launch_gemm(const GemmShape& g, const Epi& epi, hipStream_t stream) {
   hipLaunchKernelGGL(gemm_nt_kernel<Epi>, dim3(gemm_grid(g.tiles_m, g.tiles_n)), dim3(kGemmThreads), 0, stream, g,
                      epi);
-  PSPO_HIP_CHECK(hipGetLastError());
+  PSPO_LAUNCHED(__PRETTY_FUNCTION__, stream);
   return PSPO_OK;
 }
 
@@ -1275,13 +1275,13 @@ template <class Epi, class Out>
 int launch_gemm_split_tail(const GemmShape& g, const Epi& epi, const Out& out, float* slab, hipStream_t stream) {
   hipLaunchKernelGGL((gemm_nt_kernel<Epi, kLaunchRounds>), dim3(gemm_grid(g.tiles_m, g.tiles_n)), dim3(kGemmThreads),
                      0, stream, g, epi);
-  PSPO_HIP_CHECK(hipGetLastError());
+  PSPO_LAUNCHED("gemm_nt_kernel (whole rounds)", stream);
   hipLaunchKernelGGL((gemm_nt_kernel<EpiSlab, kLaunchTail>), dim3(kNumXcd * kTailSlots), dim3(kGemmThreads), 0,
                      stream, g, EpiSlab{slab});
-  PSPO_HIP_CHECK(hipGetLastError());
+  PSPO_LAUNCHED("gemm_nt_kernel (K-split tail)", stream);
   hipLaunchKernelGGL(tail_reduce_kernel<Out>, dim3(kTileM / 16, kNumXcd * 32), dim3(256), 0, stream, g,
                      (const float*)slab, out);
-  PSPO_HIP_CHECK(hipGetLastError());
+  PSPO_LAUNCHED("tail_reduce_kernel", stream);
   return PSPO_OK;
 }
 
@@ -1328,20 +1328,23 @@ int pspo_loss_fwd_bwd(const uint16_t* hidden, const uint16_t* w_head, const int3
   }
   if (stats) PSPO_REQUIRE(aligned(stats, 8), PSPO_ERR_INVALID_ARG, "misaligned stats");
   const Plan pl = make_plan(N, d, V, (flags & PSPO_KEEP_LOGITS) != 0);
+  PSPO_REQUIRE(pl.Npad <= kMaxPaddedRows && pl.Vpad <= kMaxPaddedRows, PSPO_ERR_UNSUPPORTED,
+               "N and V must each be at most " + std::to_string(kMaxPaddedRows) + " rows after padding");
+  PSPO_REQUIRE(d <= kMaxPaddedRows, PSPO_ERR_UNSUPPORTED,
+               "d must be at most " + std::to_string(kMaxPaddedRows));
   PSPO_REQUIRE(N == 0 || workspace_bytes >= (size_t)pl.total, PSPO_ERR_WORKSPACE,
                "workspace too small: need " + std::to_string(pl.total) + " bytes");
-  PSPO_REQUIRE(pl.Npad <= INT32_MAX && pl.Vpad <= INT32_MAX, PSPO_ERR_UNSUPPORTED, "problem too large");
   if (int rc = require_gfx950()) return rc;
 
   const bool accumulate = (flags & PSPO_ACCUMULATE_DW) != 0;
   if (N == 0) {
     if (!accumulate) {
       hipLaunchKernelGGL(fill_f32_kernel, dim3(1024), dim3(256), 0, stream, d_w_head, (int64_t)V * d, 0.f);
-      PSPO_HIP_CHECK(hipGetLastError());
+      PSPO_LAUNCHED("fill_f32_kernel", stream);
     }
     hipLaunchKernelGGL(reduce_loss_kernel, dim3(1), dim3(kFinThreads), 0, stream, 0, nullptr, loss_scale, loss,
                        stats);
-    PSPO_HIP_CHECK(hipGetLastError());
+    PSPO_LAUNCHED("reduce_loss_kernel", stream);
     return PSPO_OK;
   }
 
@@ -1397,10 +1400,10 @@ int pspo_loss_fwd_bwd(const uint16_t* hidden, const uint16_t* w_head, const int3
   // chunk, W[chunk]^T (dH product), in one pass over W
   hipLaunchKernelGGL(kblock_rows_kernel, dim3(ctiles64, (unsigned)(pl.Vpad / 32)), dim3(256), 0, stream, w_head,
                      (int64_t)d, d, V, nullptr, nullptr, wk, pl.Vpad, wT, pl.dpad, pl.Vc);
-  PSPO_HIP_CHECK(hipGetLastError());
+  PSPO_LAUNCHED("kblock_rows_kernel", stream);
   hipLaunchKernelGGL(kblock_rows_kernel, dim3(ctiles64, (unsigned)(pl.Npad / 32)), dim3(256), 0, stream, hidden,
                      (int64_t)d, d, N, fwd_idx, n_fwd, hk, pl.Npad, nullptr, (int64_t)0, (int64_t)kTileK);
-  PSPO_HIP_CHECK(hipGetLastError());
+  PSPO_LAUNCHED("kblock_rows_kernel", stream);
   // 2. forward logits -> per-tile softmax partials (target logits apart): the
   //    vocabulary tiles whose rows are all token ids, then a partial last one
   {
@@ -1422,30 +1425,30 @@ int pspo_loss_fwd_bwd(const uint16_t* hidden, const uint16_t* w_head, const int3
   // the target logit of each forward column (the column's token row and target)
   hipLaunchKernelGGL(row_dots_kernel, dim3((unsigned)(pl.Npad / 4)), dim3(256), 0, stream, hidden, w_head, d, V, N,
                      fwd_idx, fwd_tgt, n_fwd, zt, nullptr);
-  PSPO_HIP_CHECK(hipGetLastError());
+  PSPO_LAUNCHED("row_dots_kernel", stream);
   // 3. lse, PPO terms, delta, loss
   hipLaunchKernelGGL(finalize_kernel, dim3((unsigned)pl.nfin), dim3(kFinThreads), 0, stream, N, V, R, tiles_voc,
                      pl.Npad, part_m, part_l, zt, fwd_pos, target, logp_old, weight, seq_id, advantage, eps_low,
                      eps_high, loss_scale, lse, delta, logp_new, blk, err_flag);
-  PSPO_HIP_CHECK(hipGetLastError());
+  PSPO_LAUNCHED("finalize_kernel", stream);
   hipLaunchKernelGGL(reduce_loss_kernel, dim3(1), dim3(kFinThreads), 0, stream, (int)pl.nfin, blk, loss_scale,
                      loss, stats);
-  PSPO_HIP_CHECK(hipGetLastError());
+  PSPO_LAUNCHED("reduce_loss_kernel", stream);
   // 4. the backward runs over the tokens with delta != 0 only (every other
   //    token has a zero logit-gradient row: zero d_hidden row, no dW term)
   if (int rc = launch_compact(N, KeepActive{delta}, cnt, act_idx, nullptr, nullptr, nullptr, n_act, stats, stream))
     return rc;
   hipLaunchKernelGGL(gather_backward_kernel, dim3((unsigned)((pl.Npad + 255) / 256)), dim3(256), 0, stream, N, n_act,
                      act_idx, fwd_pos, target, lse, delta, zt, act_fwd, act_tgt, act_lse, act_delta, act_g1);
-  PSPO_HIP_CHECK(hipGetLastError());
+  PSPO_LAUNCHED("gather_backward_kernel", stream);
   hipLaunchKernelGGL(zero_inactive_rows_kernel, dim3((unsigned)N), dim3(256), 0, stream, d, delta, d_hidden);
-  PSPO_HIP_CHECK(hipGetLastError());
+  PSPO_LAUNCHED("zero_inactive_rows_kernel", stream);
   // 5. operands of the gradient products: the backward tokens' hidden rows
   //    (K-blocked, in the forward's buffer) and their transpose H[bwd]^T
   //    [dpad x Npad], in one pass
   hipLaunchKernelGGL(kblock_rows_kernel, dim3(ctiles64, (unsigned)(pl.Npad / 32)), dim3(256), 0, stream, hidden,
                      (int64_t)d, d, N, act_idx, n_act, hk, pl.Npad, hT, pl.dpad, pl.Npad);
-  PSPO_HIP_CHECK(hipGetLastError());
+  PSPO_LAUNCHED("kblock_rows_kernel", stream);
   // 6. backward, one vocabulary chunk at a time; every product is bounded by
   //    the active-token count in device memory
   for (int64_t v0 = 0; v0 < pl.Vpad; v0 += pl.Vc) {
@@ -1455,7 +1458,7 @@ int pspo_loss_fwd_bwd(const uint16_t* hidden, const uint16_t* w_head, const int3
       hipLaunchKernelGGL(logit_grad_kept_kernel, dim3((unsigned)(pl.Vc / 128), (unsigned)(pl.Npad / 32)), dim3(256), 0,
                          stream, zk, part_m, pl.Npad, tiles_tok_n, (int)pl.Vc, V, N, n_act, act_fwd, act_lse,
                          act_delta, dN, pl.Vc / kTileK, dT, pl.Npad / kTileK);
-      PSPO_HIP_CHECK(hipGetLastError());
+      PSPO_LAUNCHED("logit_grad_kept_kernel", stream);
     } else {
       // the chunk's vocabulary tiles whose rows are all token ids, then a
       // partial last one (the last chunk's, when 384 does not divide V)
@@ -1476,7 +1479,7 @@ int pspo_loss_fwd_bwd(const uint16_t* hidden, const uint16_t* w_head, const int3
     }
     hipLaunchKernelGGL(zero_targets_kernel, dim3((unsigned)std::min<int64_t>((pl.Npad + 255) / 256, 1024)), dim3(256),
                        0, stream, N, n_act, act_tgt, (int)v0, (int)vc, dN, pl.Vc / kTileK, dT, pl.Npad / kTileK);
-    PSPO_HIP_CHECK(hipGetLastError());
+    PSPO_LAUNCHED("zero_targets_kernel", stream);
     {
       GemmShape g{dT, pl.Vc, (int)vc, hT, pl.dpad, d, (int)pl.Npad, ctiles, tiles_d, n_act, kDynK, 0,
                   kTileM, pl.Npad * kTileM * 2};
@@ -1499,29 +1502,29 @@ int pspo_loss_fwd_bwd(const uint16_t* hidden, const uint16_t* w_head, const int3
     const unsigned gcols = (unsigned)std::min<int64_t>((pl.Npad + 255) / 256, 1024);
     hipLaunchKernelGGL(fill_i32_kernel, dim3((unsigned)std::min<int64_t>((V + 255) / 256, 1024)), dim3(256), 0,
                        stream, oh_cnt, (int64_t)V, 0);
-    PSPO_HIP_CHECK(hipGetLastError());
+    PSPO_LAUNCHED("fill_i32_kernel", stream);
     hipLaunchKernelGGL(onehot_count_kernel, dim3(gcols), dim3(256), 0, stream, N, n_act, act_tgt, oh_cnt);
-    PSPO_HIP_CHECK(hipGetLastError());
+    PSPO_LAUNCHED("onehot_count_kernel", stream);
     const unsigned nscan = (unsigned)((V + kScanSpan - 1) / kScanSpan);
     hipLaunchKernelGGL(onehot_scan_totals_kernel, dim3(nscan), dim3(256), 0, stream, V, oh_cnt, oh_tot);
-    PSPO_HIP_CHECK(hipGetLastError());
+    PSPO_LAUNCHED("onehot_scan_totals_kernel", stream);
     hipLaunchKernelGGL(onehot_scan_offsets_kernel, dim3(1), dim3(256), 0, stream, (int)nscan, oh_tot, oh_nrows);
-    PSPO_HIP_CHECK(hipGetLastError());
+    PSPO_LAUNCHED("onehot_scan_offsets_kernel", stream);
     hipLaunchKernelGGL(onehot_scan_write_kernel, dim3(nscan), dim3(256), 0, stream, V, oh_cnt, oh_tot, oh_start,
                        oh_cursor, oh_rows);
-    PSPO_HIP_CHECK(hipGetLastError());
+    PSPO_LAUNCHED("onehot_scan_write_kernel", stream);
     hipLaunchKernelGGL(onehot_fill_kernel, dim3(gcols), dim3(256), 0, stream, N, n_act, act_tgt, oh_cursor, oh_tmp);
-    PSPO_HIP_CHECK(hipGetLastError());
+    PSPO_LAUNCHED("onehot_fill_kernel", stream);
     hipLaunchKernelGGL(onehot_rank_kernel, dim3(gcols), dim3(256), 0, stream, N, n_act, act_tgt, oh_start, oh_cnt,
                        oh_tmp, oh_sorted);
-    PSPO_HIP_CHECK(hipGetLastError());
+    PSPO_LAUNCHED("onehot_rank_kernel", stream);
     const int rows_bound = std::min(N, V);
     hipLaunchKernelGGL(onehot_dw_kernel, dim3((unsigned)((rows_bound + 3) / 4)), dim3(256), 0, stream, rows_bound, d,
                        oh_nrows, oh_rows, oh_start, oh_cnt, oh_sorted, act_idx, act_g1, hidden, d_w_head);
-    PSPO_HIP_CHECK(hipGetLastError());
+    PSPO_LAUNCHED("onehot_dw_kernel", stream);
     hipLaunchKernelGGL(onehot_dh_kernel, dim3((unsigned)((N + 3) / 4)), dim3(256), 0, stream, N, d, n_act, act_idx,
                        act_tgt, act_g1, w_head, d_hidden);
-    PSPO_HIP_CHECK(hipGetLastError());
+    PSPO_LAUNCHED("onehot_dh_kernel", stream);
   }
   return PSPO_OK;
 }

@@ -56,6 +56,6 @@ extern "C" int pspo_mfma_loop(int32_t iters, int32_t blocks, float* out, hipStre
   PSPO_REQUIRE(out != nullptr && aligned(out, 4), PSPO_ERR_INVALID_ARG, "out must be a non-NULL float pointer");
   if (int rc = require_gfx950()) return rc;
   hipLaunchKernelGGL(mfma_loop_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, iters, out);
-  PSPO_HIP_CHECK(hipGetLastError());
+  PSPO_LAUNCHED("mfma_loop_kernel", stream);
   return PSPO_OK;
 }

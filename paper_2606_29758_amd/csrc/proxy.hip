@@ -261,9 +261,11 @@ int pspo_score_proxy(const uint16_t* hidden, const uint16_t* w_head, const int32
   PSPO_REQUIRE(workspace != nullptr && aligned(workspace, 256), PSPO_ERR_INVALID_ARG,
                "workspace must be non-NULL and 256-byte aligned");
   const ProxyPlan pl = make_proxy_plan(N, d, V);
+  PSPO_REQUIRE(pl.Npad <= kMaxPaddedRows && pl.Vpad <= kMaxPaddedRows && d <= kMaxPaddedRows,
+               PSPO_ERR_UNSUPPORTED,
+               "N, V and d must each be at most " + std::to_string(kMaxPaddedRows) + " rows after padding");
   PSPO_REQUIRE(workspace_bytes >= (size_t)pl.total, PSPO_ERR_WORKSPACE,
                "workspace too small: need " + std::to_string(pl.total) + " bytes");
-  PSPO_REQUIRE(pl.Npad <= INT32_MAX && pl.Vpad <= INT32_MAX, PSPO_ERR_UNSUPPORTED, "problem too large");
   if (int rc = require_gfx950()) return rc;
 
   char* ws = static_cast<char*>(workspace);
@@ -281,10 +283,10 @@ int pspo_score_proxy(const uint16_t* hidden, const uint16_t* w_head, const int32
   const int Dk = (int)round_up(d, kTileK);   // K of the product: d with zero padding to whole K steps
   hipLaunchKernelGGL(kblock_rows_kernel, dim3(ctiles64, (unsigned)(pl.Vpad / 32)), dim3(256), 0, stream, w_head,
                      (int64_t)d, d, V, nullptr, nullptr, wk, pl.Vpad, nullptr, (int64_t)0, (int64_t)kTileK);
-  PSPO_HIP_CHECK(hipGetLastError());
+  PSPO_LAUNCHED("kblock_rows_kernel", stream);
   hipLaunchKernelGGL(kblock_rows_kernel, dim3(ctiles64, (unsigned)(pl.Npad / 32)), dim3(256), 0, stream, hidden,
                      (int64_t)d, d, N, nullptr, nullptr, hk, pl.Npad, nullptr, (int64_t)0, (int64_t)kTileK);
-  PSPO_HIP_CHECK(hipGetLastError());
+  PSPO_LAUNCHED("kblock_rows_kernel", stream);
   {
     // the vocabulary tiles whose rows are all token ids, then a partial last one
     const int tiles_full = V / kTileM;
@@ -293,7 +295,7 @@ int pspo_score_proxy(const uint16_t* hidden, const uint16_t* w_head, const int32
       EpiProxy<true> e{V, N, pl.Npad, 0, target, part_m, part_s1, part_s2};
       hipLaunchKernelGGL(gemm_nt_kernel<EpiProxy<true>>, dim3(gemm_grid(tiles_full, tiles_tok)), dim3(kGemmThreads),
                          0, stream, g, e);
-      PSPO_HIP_CHECK(hipGetLastError());
+      PSPO_LAUNCHED("gemm_nt_kernel (score proxy)", stream);
     }
     if (tiles_full < tiles_voc) {
       GemmShape g{wk + (int64_t)tiles_full * kTileM * kTileK, pl.Vpad, V - tiles_full * kTileM, hk, pl.Npad, N, Dk, 1,
@@ -301,16 +303,16 @@ int pspo_score_proxy(const uint16_t* hidden, const uint16_t* w_head, const int32
       EpiProxy<false> e{V, N, pl.Npad, tiles_full, target, part_m, part_s1, part_s2};
       hipLaunchKernelGGL(gemm_nt_kernel<EpiProxy<false>>, dim3(gemm_grid(1, tiles_tok)), dim3(kGemmThreads), 0,
                          stream, g, e);
-      PSPO_HIP_CHECK(hipGetLastError());
+      PSPO_LAUNCHED("gemm_nt_kernel (score proxy)", stream);
     }
   }
   // the target logit and ||h||^2 of every token, one pass over its hidden row
   hipLaunchKernelGGL(row_dots_kernel, dim3((unsigned)((N + 3) / 4)), dim3(256), 0, stream, hidden, w_head, d, V, N,
                      nullptr, target, nullptr, zt, hn);
-  PSPO_HIP_CHECK(hipGetLastError());
+  PSPO_LAUNCHED("row_dots_kernel", stream);
   hipLaunchKernelGGL(proxy_finalize_kernel, dim3((unsigned)((N + 255) / 256)), dim3(256), 0, stream, N, V,
                      tiles_voc, pl.Npad, part_m, part_s1, part_s2, zt, hn, target, gamma, logp, p_sq, err_flag);
-  PSPO_HIP_CHECK(hipGetLastError());
+  PSPO_LAUNCHED("proxy_finalize_kernel", stream);
   return PSPO_OK;
 }
 

@@ -205,12 +205,12 @@ int pspo_sample_cutoffs(const double* xi, const int64_t* xi_off, const int32_t* 
   if (int rc = require_gfx950()) return rc;
   if (err_flag) {
     hipLaunchKernelGGL(validate_xi_kernel, dim3(4, P), dim3(256), 0, stream, xi, xi_off, err_flag);
-    PSPO_HIP_CHECK(hipGetLastError());
+    PSPO_LAUNCHED("validate_xi_kernel", stream);
   }
   hipLaunchKernelGGL(sample_cutoffs_kernel, dim3((R + 255) / 256), dim3(256), 0, stream, xi, xi_off, lengths,
                      R, K, (uint32_t)seed, (uint32_t)(seed >> 32), (uint32_t)offset, (uint32_t)(offset >> 32),
                      cutoffs);
-  PSPO_HIP_CHECK(hipGetLastError());
+  PSPO_LAUNCHED("sample_cutoffs_kernel", stream);
   return PSPO_OK;
 }
 
@@ -244,15 +244,15 @@ int pspo_pack_prefixes(const int32_t* cutoffs, const int32_t* lengths, const dou
   if (int rc = require_gfx950()) return rc;
   hipLaunchKernelGGL(pack_scan_kernel, dim3(1), dim3(kScanThreads), 0, stream, cutoffs, lengths, xi_off, R, K,
                      capacity, cu_seqlens, full_off, n_tokens, err_flag);
-  PSPO_HIP_CHECK(hipGetLastError());
+  PSPO_LAUNCHED("pack_scan_kernel", stream);
   if (R == 0 || capacity == 0) return PSPO_OK;
   hipLaunchKernelGGL(pack_fill_kernel, dim3(16, R), dim3(256), 0, stream, cu_seqlens, full_off, xi, xi_off, K,
                      capacity, target_full, logp_old_full, src_row, seq_id, weight, target, logp_old);
-  PSPO_HIP_CHECK(hipGetLastError());
+  PSPO_LAUNCHED("pack_fill_kernel", stream);
   if (hidden_full) {
     hipLaunchKernelGGL(pack_hidden_kernel, dim3(64, R), dim3(256), 0, stream, cu_seqlens, full_off, capacity,
                        reinterpret_cast<const u32x4*>(hidden_full), reinterpret_cast<u32x4*>(hidden), d / 8);
-    PSPO_HIP_CHECK(hipGetLastError());
+    PSPO_LAUNCHED("pack_hidden_kernel", stream);
   }
   return PSPO_OK;
 }

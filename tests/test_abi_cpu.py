@@ -121,6 +121,13 @@ def test_loss_argument_errors(lib):
     assert _loss(lib, d=0) == INVALID
     assert _loss(lib, V=0) == INVALID
     assert _loss(lib, d=100) == UNSUPPORTED          # d % 8 != 0
+    # sizes beyond the copy kernels' grid (65535 blocks of 32 rows on its y axis)
+    assert _loss(lib, N=2730 * 768 + 1, wsb=0) == UNSUPPORTED        # pads to 2097408 > 2097120 rows
+    assert b"at most 2097120" in lib.pspo_last_error()
+    assert _loss(lib, V=5461 * 384 + 1) == UNSUPPORTED                # pads to 2097408 rows
+    assert _loss(lib, d=65535 * 32 + 8) == UNSUPPORTED
+    assert _loss(lib, N=2730 * 768, wsb=0) == WORKSPACE               # 2096640 tokens: within the limit
+    assert _loss(lib, V=5461 * 384, wsb=0) == WORKSPACE               # 2097024 rows: within the limit
     _loss(lib, d=96)                                 # d % 8 == 0 passes the argument checks
     assert b"multiple of" not in lib.pspo_last_error()
     assert _loss(lib, R=0) == INVALID
@@ -177,6 +184,9 @@ def test_score_proxy_argument_errors(lib):
     assert _proxy(lib, d=0) == INVALID
     assert _proxy(lib, V=0) == INVALID
     assert _proxy(lib, d=100) == UNSUPPORTED
+    assert _proxy(lib, N=65535 * 32 + 1) == UNSUPPORTED              # pads to 2097152 rows
+    assert _proxy(lib, V=5461 * 384 + 1) == UNSUPPORTED
+    assert _proxy(lib, N=8191 * 256, wsb=0) == WORKSPACE              # 2096896 rows: within the limit
     _proxy(lib, d=96)
     assert b"multiple of" not in lib.pspo_last_error()
     assert _proxy(lib, g=None) == INVALID
