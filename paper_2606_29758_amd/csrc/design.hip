@@ -21,8 +21,9 @@
 // (H uniform on 1..T) and Time prior (xi_t = exp(-lambda (t-1))).  Every xi is
 // floored at 2^-32, the resolution of the sampler's thresholds.
 //
-// Both kernels work in float64; their cost is negligible next to the proxy's
-// forward pass (a few operations per completion token and per step).
+// Both kernels work in float64; their cost is small next to the proxy's
+// forward pass (a few operations per completion token and per step; the
+// design's sequential solve reads LDS-resident weights and block stack).
 #include <cmath>
 #include <mutex>
 #include <string>
@@ -127,106 +128,72 @@ __global__ __launch_bounds__(256) void design_weights_kernel(
   }
 }
 
-// One block of 64 threads per prompt; lane 0 runs the sequential solve.
-__global__ __launch_bounds__(64) void design_cutoffs_kernel(const double* __restrict__ w,
-                                                            const int64_t* __restrict__ xi_off, double budget,
-                                                            int variant, double lambda, double* __restrict__ xi,
-                                                            int32_t* __restrict__ bstart, int32_t* __restrict__ blen,
-                                                            double* __restrict__ bval, int32_t* __restrict__ err_flag) {
-  const int p = blockIdx.x;
-  const int64_t a = xi_off[p];
-  const int T = (int)(xi_off[p + 1] - a);
-  const double* wp = w + a;
-  double* xp = xi + a;
-  if (variant == PSPO_DESIGN_UNIFORM) {
-    for (int t = threadIdx.x; t < T; t += blockDim.x) xp[t] = (double)(T - t) / (double)T;
-    return;
-  }
-  if (variant == PSPO_DESIGN_TIME_PRIOR) {
-    for (int t = threadIdx.x; t < T; t += blockDim.x) xp[t] = fmax(exp(-lambda * (double)t), kXiFloor);
-    return;
-  }
-  if (threadIdx.x != 0) return;
-  bool bad = false;
-  double root_sum = 0.0;
-  for (int t = 0; t < T; ++t) {
-    const double v = wp[t];
-    if (!(v >= 0.0) || isinf(v)) bad = true;
-    else root_sum += sqrt(v);
-  }
-  if (bad) {
-    if (err_flag) atomicOr(err_flag, PSPO_DEVERR_BAD_XI);
-    for (int t = 0; t < T; ++t) xp[t] = NAN;
-    return;
-  }
-  if (budget >= (double)T) {
-    for (int t = 0; t < T; ++t) xp[t] = 1.0;
-    return;
-  }
-  if (root_sum == 0.0) {   // every weight zero: any feasible table is optimal
-    for (int t = 0; t < T; ++t) xp[t] = budget / (double)T;
-    return;
-  }
-  if (variant == PSPO_DESIGN_HEURISTIC) {
-    double run = 1.0;
-    for (int t = 0; t < T; ++t) {
-      run = fmin(run, fmin(1.0, budget * sqrt(wp[t]) / root_sum));
-      xp[t] = fmax(run, kXiFloor);
-    }
-    return;
-  }
-  // Pooling Adjacent Violators: a stack of blocks (start, length, summed
-  // weight); a new element pools with the block below it while that block's
-  // score sqrt(W / L) is below its own.  The top block and its score stay in
-  // registers (the memory stack holds the blocks under it), so an element
-  // that does not pool costs no memory round trip; every comparison and sum
-  // is the same expression as with the whole stack in memory.
-  int32_t* st = bstart + a;
-  int32_t* ln = blen + a;
-  double* wv = bval + a;
-  int M = 0;                       // blocks under the top
-  int ts = 0, tl = 1;              // the top block
-  double tw = wp[0];
-  double tsc = sqrt(tw / (double)tl);
-  for (int t = 1; t < T; ++t) {
-    int s0 = t, L = 1;
-    double W = wp[t];
-    double sc = sqrt(W / (double)L);
-    bool top = true;
-    while (top && tsc < sc) {      // pool the top into the new block
-      s0 = ts;
-      L += tl;
-      W = tw + W;
-      sc = sqrt(W / (double)L);
-      if (M > 0) {
-        --M;
-        ts = st[M];
-        tl = ln[M];
-        tw = wv[M];
-        tsc = sqrt(tw / (double)tl);
-      } else {
-        top = false;
+// The budgeted monotone solve of one prompt (App. F) on the storage given: wr
+// the weights, wv / ln the block stack (summed weight and length of each
+// block), rest the suffix sums (it may alias wr: the weights are not read
+// after the pooling).  Force-inlined at each call with pointers of one memory
+// kind, so that LDS-resident data is read and written by LDS instructions
+// rather than generic ones.  Called by all 64 lanes of the block's one wave:
+// lane 0 pools, the lanes compute the block scores, lane 0 does the rest.
+__device__ __forceinline__ void pav_solve(const double* wr, double* wv, int32_t* ln, double* rest, int T,
+                                          double budget, double* xp) {
+  const int lane = threadIdx.x;
+  int M = 0;                       // blocks under the top, then all blocks
+  if (lane == 0) {
+    // Pooling Adjacent Violators: a stack of blocks (start, length, summed
+    // weight); a new element pools with the block below it while that block's
+    // score sqrt(W / L) is below its own.  Scores of positive lengths are in the
+    // order of the mean weights, and tw / tl < W / L exactly when tw L < W tl, so
+    // each step compares two products: no division or root per step (a product
+    // rounds to 2^-53 relative, so the decision can differ from the exact one
+    // only for blocks whose means agree to that; pooling or not such a pair
+    // moves the table by the same relative amount).  The top block stays in
+    // registers (the stack holds the blocks under it), so an element that does
+    // not pool costs no stack access.
+    // A block's start is not stored: the block under the top ends where the top
+    // starts.
+    int ts = 0, tl = 1;              // the top block
+    double tw = wr[0];
+    double w_next = T > 1 ? wr[1] : 0.0;   // each step's weight is read one step ahead
+    for (int t = 1; t < T; ++t) {
+      int s0 = t, L = 1;
+      double W = w_next;
+      if (t + 1 < T) w_next = wr[t + 1];
+      bool top = true;
+      while (top && tw * (double)L < W * (double)tl) {   // pool the top into the new block
+        s0 = ts;
+        L += tl;
+        W = tw + W;
+        if (M > 0) {
+          --M;
+          tl = ln[M];
+          tw = wv[M];
+          ts = s0 - tl;
+        } else {
+          top = false;
+        }
       }
+      if (top) {                     // the old top goes under the new block
+        ln[M] = tl;
+        wv[M] = tw;
+        ++M;
+      }
+      ts = s0;
+      tl = L;
+      tw = W;
     }
-    if (top) {                     // the old top goes under the new block
-      st[M] = ts;
-      ln[M] = tl;
-      wv[M] = tw;
-      ++M;
-    }
-    ts = s0;
-    tl = L;
-    tw = W;
-    tsc = sc;
+    ln[M] = tl;
+    wv[M] = tw;
+    ++M;
   }
-  st[M] = ts;
-  ln[M] = tl;
-  wv[M] = tw;
-  ++M;
-  // scores, then suffix sums of L_m s_m (accumulated from the last block)
-  for (int m = 0; m < M; ++m) wv[m] = sqrt(wv[m] / (double)ln[m]);
+  M = __shfl(M, 0);
+  __syncthreads();   // lane 0's stack is visible to every lane
+  // the block scores sqrt(W_m / L_m), spread over the lanes
+  for (int m = lane; m < M; m += 64) wv[m] = sqrt(wv[m] / (double)ln[m]);
+  __syncthreads();
+  if (lane != 0) return;
+  // suffix sums of L_m s_m (accumulated from the last block)
   // first unsaturated block: kappa(m) = (B - sum_{j<m} L_j) / sum_{j>=m} L_j s_j, kappa(m) s_m <= 1
-  double* rest = xp;   // scratch: the output table holds the suffix sums until it is written
   double acc = 0.0;
   for (int m = M - 1; m >= 0; --m) {
     acc += (double)ln[m] * wv[m];
@@ -243,13 +210,89 @@ __global__ __launch_bounds__(64) void design_cutoffs_kernel(const double* __rest
     if (kappa * wv[m] <= 1.0) break;
     saturated += ln[m];
   }
-  for (int m = 0; m < M; ++m) {
+  for (int m = 0, start = 0; m < M; start += ln[m], ++m) {
     double v;
-    if (kappa < 0.0) v = (st[m] < saturated) ? 1.0 : (budget - (double)saturated) / (double)(T - saturated);
+    if (kappa < 0.0) v = (start < saturated) ? 1.0 : (budget - (double)saturated) / (double)(T - saturated);
     else v = fmin(1.0, kappa * wv[m]);
     v = fmax(v, kXiFloor);
-    for (int t = st[m]; t < st[m] + ln[m]; ++t) xp[t] = v;
+    for (int t = start; t < start + ln[m]; ++t) xp[t] = v;
   }
+}
+
+// LDS of one design block: the prompt's weights (8 bytes per step) and, when
+// they fit as well, the PAV block stack (12 bytes per step: summed weight and
+// length).
+constexpr int kDesignLdsBytes = 160 * 1024;
+
+// One block of 64 threads (one wave) per prompt: the lanes stage the prompt's
+// weights in LDS, check them and sum their square roots; lane 0 then runs the
+// sequential solve on LDS-resident data (the weights when T <= 20480, the
+// block stack too when T <= 8192; otherwise from the workspace).
+__global__ __launch_bounds__(64) void design_cutoffs_kernel(const double* __restrict__ w,
+                                                            const int64_t* __restrict__ xi_off, double budget,
+                                                            int variant, double lambda, double* __restrict__ xi,
+                                                            int32_t* __restrict__ blen,
+                                                            double* __restrict__ bval, int32_t* __restrict__ err_flag) {
+  __shared__ __attribute__((aligned(16))) unsigned char lds[kDesignLdsBytes];
+  const int p = blockIdx.x;
+  const int64_t a = xi_off[p];
+  const int T = (int)(xi_off[p + 1] - a);
+  const double* wp = w + a;
+  double* xp = xi + a;
+  if (variant == PSPO_DESIGN_UNIFORM) {
+    for (int t = threadIdx.x; t < T; t += blockDim.x) xp[t] = (double)(T - t) / (double)T;
+    return;
+  }
+  if (variant == PSPO_DESIGN_TIME_PRIOR) {
+    for (int t = threadIdx.x; t < T; t += blockDim.x) xp[t] = fmax(exp(-lambda * (double)t), kXiFloor);
+    return;
+  }
+  const bool w_in_lds = (int64_t)T * 8 <= kDesignLdsBytes;
+  const bool stack_in_lds = (int64_t)T * 20 <= kDesignLdsBytes;
+  double* wl = reinterpret_cast<double*>(lds);
+  bool bad_lane = false;
+  double part = 0.0;   // this lane's steps t = lane, lane + 64, ... in order
+  for (int t = threadIdx.x; t < T; t += 64) {
+    const double v = wp[t];
+    if (w_in_lds) wl[t] = v;
+    if (!(v >= 0.0) || isinf(v)) bad_lane = true;
+    else part += sqrt(v);
+  }
+  const bool bad = __ballot(bad_lane) != 0;
+  const double root_sum = wave_sum(part);   // the lanes' partial sums in a fixed butterfly order
+  __syncthreads();
+  const double* wr = w_in_lds ? wl : wp;
+  const bool single = bad || budget >= (double)T || root_sum == 0.0 || variant == PSPO_DESIGN_HEURISTIC;
+  if (single && threadIdx.x != 0) return;
+  if (bad) {
+    if (err_flag) atomicOr(err_flag, PSPO_DEVERR_BAD_XI);
+    for (int t = 0; t < T; ++t) xp[t] = NAN;
+    return;
+  }
+  if (budget >= (double)T) {
+    for (int t = 0; t < T; ++t) xp[t] = 1.0;
+    return;
+  }
+  if (root_sum == 0.0) {   // every weight zero: any feasible table is optimal
+    for (int t = 0; t < T; ++t) xp[t] = budget / (double)T;
+    return;
+  }
+  if (variant == PSPO_DESIGN_HEURISTIC) {
+    double run = 1.0;
+    for (int t = 0; t < T; ++t) {
+      run = fmin(run, fmin(1.0, budget * sqrt(wr[t]) / root_sum));
+      xp[t] = fmax(run, kXiFloor);
+    }
+    return;
+  }
+  // the solve, on LDS-resident weights and stack where they fit
+  if (stack_in_lds)
+    pav_solve(wl, reinterpret_cast<double*>(lds + (int64_t)T * 8), reinterpret_cast<int32_t*>(lds + (int64_t)T * 16),
+              wl, T, budget, xp);
+  else if (w_in_lds)
+    pav_solve(wl, bval + a, blen + a, wl, T, budget, xp);
+  else
+    pav_solve(wp, bval + a, blen + a, xp, T, budget, xp);
 }
 
 // Argument checks shared by the design entry points (host only).
@@ -267,16 +310,17 @@ int check_design_args(const double* w, const int64_t* xi_off, int32_t P, int64_t
   return PSPO_OK;
 }
 
-// The PAV block stack (start, length, value per step: pspo_design_workspace_bytes(total_T))
-// carved from `ws`, then the solve.  The kernel writes every stack entry before
-// reading it, so the memory needs no clearing.
+// The PAV block stack of the prompts whose stack does not fit in LDS (length
+// and summed weight per block, at most one block per step) carved from `ws`
+// (pspo_design_workspace_bytes(total_T), whose first 4 bytes per step are
+// spare), then the solve.  The kernel writes every stack entry before reading
+// it, so the memory needs no clearing.
 int launch_design(const double* w, const int64_t* xi_off, int32_t P, int64_t total_T, double budget, int32_t variant,
                   double lambda, double* xi, char* ws, int32_t* err_flag, hipStream_t stream) {
-  int32_t* bstart = reinterpret_cast<int32_t*>(ws);
   int32_t* blen = reinterpret_cast<int32_t*>(ws + round_up(total_T * 4, 256));
   double* bval = reinterpret_cast<double*>(ws + 2 * round_up(total_T * 4, 256));
   hipLaunchKernelGGL(design_cutoffs_kernel, dim3((unsigned)P), dim3(64), 0, stream, w, xi_off, budget, variant,
-                     lambda, xi, bstart, blen, bval, err_flag);
+                     lambda, xi, blen, bval, err_flag);
   PSPO_LAUNCHED("design_cutoffs_kernel", stream);
   return PSPO_OK;
 }
