@@ -1,4 +1,5 @@
-"""GPU: token counts on and around the tile edges, against the float64 oracle.
+"""GPU: token counts on and around the tile edges, against the float64 oracle
+(loss call and score proxy).
 
 The products tile the tokens by 256 (forward, logit gradient), 384 (dH) and
 pad them to 768; the forward and backward token sets are compacted on the
@@ -62,3 +63,19 @@ def test_token_count_edges(N, V, d):
     assert int(out["stats"][4].item()) == N
     assert rel_l2(out["d_hidden"].cpu().numpy(), ref["d_hidden"]) <= GRAD_REL_L2
     assert rel_l2(out["d_w_head"].cpu().numpy(), ref["d_w"]) <= GRAD_REL_L2
+
+
+@pytest.mark.parametrize("V,d", [(1152, 128), (1000, 200)])
+@pytest.mark.parametrize("N", EDGES)
+def test_score_proxy_token_count_edges(N, V, d):
+    from oracle import score_proxy as osp
+    rng = np.random.default_rng(104729 * N + V + d)
+    h = synth.round_to_bf16_bits(rng.normal(0.0, 1.0, (N, d)).astype(np.float32))
+    W = synth.round_to_bf16_bits(rng.normal(0.0, 0.05, (V, d)).astype(np.float32))
+    tgt = rng.integers(0, V, N).astype(np.int32)
+    ref = osp.score_proxy(h, W, tgt)
+    out = pspo.score_proxy(_bits_tensor(h), _bits_tensor(W), torch.from_numpy(tgt).to("cuda"), N, want_p_sq=True)
+    torch.cuda.synchronize()
+    np.testing.assert_allclose(out["gamma"].cpu().numpy().astype(np.float64), ref["gamma"], rtol=1e-4, atol=0)
+    np.testing.assert_allclose(out["p_sq"].cpu().numpy().astype(np.float64), ref["p_sq"], rtol=1e-4, atol=0)
+    assert np.max(np.abs(out["logp"].cpu().numpy().astype(np.float64) - ref["logp"])) <= LOGP_ATOL
