@@ -182,8 +182,10 @@ size_t pspo_loss_workspace_bytes(int32_t N, int32_t d, int32_t V, uint32_t flags
  * and the one-hot part delta_i e_{o_i} in float32 (d_hidden[i] += delta_i W[o_i];
  * d_w_head[v] += sum_{i : o_i = v} delta_i h_i, each row's terms summed in token
  * order), so the largest entry of each row of G is never rounded to bf16.
- * The chunk is Vc = 384 * 256 / gcd(ceil(d / 256), 256) vocabulary rows (the
- * whole padded vocabulary if that is smaller); 49152 at d = 3584.  Every
+ * The chunk width is about Vb = 384 * 256 / gcd(ceil(d / 256), 256) rows: the
+ * vocabulary (padded to 384) is split evenly into floor(V / Vb) chunks, or one
+ * more when the remainder exceeds Vb / 4 (one chunk if V < Vb), each a
+ * multiple of 384 rows; three chunks of 50688 rows at d = 3584, V = 152064.  Every
  * result is deterministic (no floating-point atomics).
  *
  *  hidden     device, bf16 bits [N, d] row-major (packed prefix tokens).

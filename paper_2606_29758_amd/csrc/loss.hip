@@ -1199,10 +1199,16 @@ Plan make_plan(int64_t N, int64_t d, int64_t V, bool keep) {
   p.dpad = round_up(d, kTileN);
   p.Dk = round_up(d, kTileK);
   const int64_t d64 = round_up(d, 64);   // columns the K-blocked copies write (64 per copy tile)
-  // Vocabulary rows per backward chunk: a multiple of 384-row tiles such that
-  // the dW product of a chunk ((Vc / 384) x ceil(d / 256) tiles of very long
-  // K) fills whole rounds of the 256 CUs (d = 3584: 14 column tiles, 128 row
-  // tiles, exactly 7 rounds); the whole vocabulary if smaller.
+  // Vocabulary rows per backward chunk.  The base width is a multiple of
+  // 384-row tiles for which the dW product of a chunk ((Vc / 384) x
+  // ceil(d / 256) tiles of very long K) fills whole rounds of the 256 CUs
+  // (d = 3584: 14 column tiles, 128 row tiles, exactly 7 rounds).  The
+  // vocabulary is split evenly into as many chunks as it holds base widths,
+  // plus one more only if the remainder exceeds a quarter of a base width: a
+  // short last chunk would run its dH product at a short K, where the per-tile
+  // read-modify-write and prologue costs dominate (V = 152064: three chunks of
+  // 50688 rows instead of three of 49152 and one of 4608, -0.4% per call); the
+  // K-split tails absorb the partial rounds.
   {
     int64_t a = p.dpad / kTileN, b = 256;
     while (b) {
@@ -1211,7 +1217,9 @@ Plan make_plan(int64_t N, int64_t d, int64_t V, bool keep) {
       b = r;
     }
     const int64_t rows = 256 / a * kTileM;
-    p.Vc = p.Vpad < rows ? p.Vpad : rows;
+    const int64_t whole = p.Vpad / rows, rem = p.Vpad % rows;
+    const int64_t nch = whole == 0 ? 1 : (rem * 4 <= rows ? whole : whole + 1);
+    p.Vc = round_up((p.Vpad + nch - 1) / nch, kTileM);
   }
   p.ntv = p.Vpad / kTileM;
   p.nfin = (N + kFinThreads - 1) / kFinThreads;

@@ -150,9 +150,12 @@ def test_loss_argument_errors(lib):
 
 def test_workspace_bytes_keep_flag(lib):
     # with PSPO_KEEP_LOGITS the forward keeps the first vocabulary chunk's
-    # logits as fp16 offsets: Vc x round_up(N, 768) x 2 bytes more (Vc = 49152 at
-    # d = 3584, the whole padded vocabulary when that is smaller)
-    for N, d, V, vc in ((1000, 3584, 152064, 49152), (300, 128, 2048, 2304), (5000, 4096, 151936, 6144)):
+    # logits as fp16 offsets: Vc x round_up(N, 768) x 2 bytes more (Vc = 50688 at
+    # d = 3584, V = 152064: the padded vocabulary split evenly into three chunks
+    # of about the round-filling width 49152; the whole padded vocabulary when
+    # that is smaller; d = 4096: width 6144, 25 chunks since the remainder of
+    # 4608 rows exceeds a quarter of it)
+    for N, d, V, vc in ((1000, 3584, 152064, 50688), (300, 128, 2048, 2304), (5000, 4096, 151936, 6144)):
         keep = lib.pspo_loss_workspace_bytes(N, d, V, 4)
         lean = lib.pspo_loss_workspace_bytes(N, d, V, 0)
         npad = -(-N // 768) * 768

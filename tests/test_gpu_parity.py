@@ -35,7 +35,7 @@ MINI = {
     # of 6 K steps, and one of three chunks whose last ends in a partial tile (7B width)
     "odd_small": synth.custom("odd_small", "tiny", d=192, V=1000, P=2, K=3, length_law=("uniform", 20, 90),
                               data_seed=41),
-    "odd_chunks": synth.custom("odd_chunks", "qwen7b", V=100003, P=2, K=3, length_law=("uniform", 60, 160),
+    "odd_chunks": synth.custom("odd_chunks", "qwen7b", V=130003, P=2, K=3, length_law=("uniform", 60, 160),
                                data_seed=49),
     # the 7B width and vocabulary with short completions (the oracle's logp_old of a rescaled head
     # is recomputed per test)

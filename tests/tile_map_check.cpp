@@ -95,7 +95,8 @@ int main() {
       {210, 14, 80367, 3584, 1536}, {128, 14, 49152, 3584, 2512}, {12, 14, 4608, 3584, 2512},
       {210, 14, 80367, 3584, 144},  {1, 1, 300, 128, 72},        {6, 1, 2304, 128, 10},
       {3, 1, 1000, 192, 0},         {298, 14, 114432, 3584, 1536}, {2, 2, 500, 300, 3},
-      {447, 14, 5000, 3584, 1},     {396, 372, 152064, 95214, 112}, {5, 6, 1920, 1536, 7}};
+      {447, 14, 5000, 3584, 1},     {396, 372, 152064, 95214, 112}, {5, 6, 1920, 1536, 7},
+      {132, 14, 50688, 3584, 2512}, {210, 14, 80367, 3584, 1584},  {132, 314, 50688, 80367, 112}};
   for (auto& c : cases)
     if (check_launches(c[0], c[1], c[2], c[3], c[4])) return 1;
   std::printf("ok\n");
