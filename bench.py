@@ -459,6 +459,16 @@ def main():
             "parallelism": "single GPU",
         },
         "loss_call_ms": loss_avg,
+        # the last timed step's own numbers (the loss call's stats output)
+        "step_stats": {
+            "loss": float(out["loss"].item()),
+            "clipped_fraction": float(st[1]) / max(n_fwd, 1),   # of the tokens with A != 0
+            "zero_advantage_tokens": int(st[2]),
+            "max_weight": float(st[3]),
+            "prefix_tokens_per_prompt": N / cfg.P,
+            "mean_prefix_length": N / cfg.R,
+            "mean_completion_length": int(wl.total_tokens) / cfg.R,
+        },
         "sample_pack_ms": pack_avg,
         "memory": {"peak_device_bytes": int(peak_bytes),
                    "loss_workspace_bytes": ws_bytes,
