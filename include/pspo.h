@@ -30,6 +30,8 @@
  *    but "" or "0"; read at every launch) every call synchronises its stream
  *    after each kernel and returns PSPO_ERR_HIP naming the kernel whose
  *    execution failed.  Results are the same bits as without it.
+ *  - Tracing: each call opens a roctx range named after it while it enqueues
+ *    its work (rocprofv3 --marker-trace shows it next to its kernels).
  *  - bf16 tensors are passed as their raw 16-bit patterns (uint16_t).
  *  - Rollouts are prompt-major: completion k of prompt p is r = p*K + k.
  */

@@ -2,6 +2,7 @@
 #pragma once
 
 #include <hip/hip_runtime.h>
+#include <rocprofiler-sdk-roctx/roctx.h>
 
 #include <cstdint>
 #include <cstdio>
@@ -43,6 +44,16 @@ int require_gfx950();
 // kernel is named where it happens; every call then runs synchronously.
 bool debug_mode();
 int after_launch(const char* kernel, hipStream_t stream);
+
+// A roctx range named after the entry point, open while the call enqueues its
+// work (rocprofv3 --marker-trace shows it next to the kernels it launched; it
+// costs next to nothing with no tool attached).
+struct TraceRange {
+  explicit TraceRange(const char* name) { roctxRangePush(name); }
+  ~TraceRange() { roctxRangePop(); }
+  TraceRange(const TraceRange&) = delete;
+  TraceRange& operator=(const TraceRange&) = delete;
+};
 #define PSPO_LAUNCHED(kernel, stream)                                   \
   do {                                                                  \
     if (int rc_ = ::pspo::after_launch((kernel), (stream))) return rc_; \

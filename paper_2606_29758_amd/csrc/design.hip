@@ -368,6 +368,7 @@ int pspo_design_weights(const float* gamma, const int32_t* topk_ids, const float
                         int32_t* err_flag, hipStream_t stream) {
   using namespace pspo;
   clear_last_error();
+  TraceRange trace_range("pspo_design_weights");
   PSPO_REQUIRE(P >= 1 && K >= 1 && total_T >= 0, PSPO_ERR_INVALID_ARG, "need P >= 1, K >= 1, total_T >= 0");
   PSPO_REQUIRE(K <= 64, PSPO_ERR_UNSUPPORTED, "K must be <= 64");
   PSPO_REQUIRE(topk >= 1 && (int64_t)K * topk <= kDesignMaxEntries, PSPO_ERR_UNSUPPORTED,
@@ -397,6 +398,7 @@ int pspo_design_cutoffs(const double* w, const int64_t* xi_off, int32_t P, int64
                         int32_t* err_flag, hipStream_t stream) {
   using namespace pspo;
   clear_last_error();
+  TraceRange trace_range("pspo_design_cutoffs");
   if (int rc = check_design_args(w, xi_off, P, total_T, budget, variant, lambda, xi)) return rc;
   if (total_T == 0) return PSPO_OK;
   PSPO_REQUIRE(workspace && aligned(workspace, 256), PSPO_ERR_INVALID_ARG,
@@ -412,6 +414,7 @@ int pspo_design_cutoffs_noalloc(const double* w, const int64_t* xi_off, int32_t 
                                 int32_t variant, double lambda, double* xi, int32_t* err_flag, hipStream_t stream) {
   using namespace pspo;
   clear_last_error();
+  TraceRange trace_range("pspo_design_cutoffs_noalloc");
   if (int rc = check_design_args(w, xi_off, P, total_T, budget, variant, lambda, xi)) return rc;
   if (total_T == 0) return PSPO_OK;
   PSPO_REQUIRE(pspo_design_workspace_bytes(total_T) <= kNoAllocScratchBytes, PSPO_ERR_UNSUPPORTED,

@@ -1310,6 +1310,7 @@ int pspo_loss_fwd_bwd(const uint16_t* hidden, const uint16_t* w_head, const int3
                       int32_t* err_flag, void* workspace, size_t workspace_bytes, hipStream_t stream) {
   using namespace pspo;
   clear_last_error();
+  TraceRange trace_range("pspo_loss_fwd_bwd");
   PSPO_REQUIRE(N >= 0 && R >= 0, PSPO_ERR_INVALID_ARG, "N and R must be >= 0");
   PSPO_REQUIRE(d > 0 && V > 0, PSPO_ERR_INVALID_ARG, "d and V must be > 0");
   PSPO_REQUIRE(d % 8 == 0, PSPO_ERR_UNSUPPORTED, "d must be a multiple of 8");

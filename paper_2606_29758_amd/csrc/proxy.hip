@@ -249,6 +249,7 @@ int pspo_score_proxy(const uint16_t* hidden, const uint16_t* w_head, const int32
                      size_t workspace_bytes, hipStream_t stream) {
   using namespace pspo;
   clear_last_error();
+  TraceRange trace_range("pspo_score_proxy");
   PSPO_REQUIRE(N >= 0, PSPO_ERR_INVALID_ARG, "N must be >= 0");
   PSPO_REQUIRE(d > 0 && V > 0, PSPO_ERR_INVALID_ARG, "d and V must be > 0");
   PSPO_REQUIRE(d % 8 == 0, PSPO_ERR_UNSUPPORTED, "d must be a multiple of 8");

@@ -195,6 +195,7 @@ int pspo_sample_cutoffs(const double* xi, const int64_t* xi_off, const int32_t* 
                         hipStream_t stream) {
   using namespace pspo;
   clear_last_error();
+  TraceRange trace_range("pspo_sample_cutoffs");
   PSPO_REQUIRE(P >= 0 && K >= 0, PSPO_ERR_INVALID_ARG, "P and K must be >= 0");
   PSPO_REQUIRE((int64_t)P * K <= INT32_MAX, PSPO_ERR_INVALID_ARG, "P*K overflows int32");
   const int32_t R = P * K;
@@ -222,6 +223,7 @@ int pspo_pack_prefixes(const int32_t* cutoffs, const int32_t* lengths, const dou
                        hipStream_t stream) {
   using namespace pspo;
   clear_last_error();
+  TraceRange trace_range("pspo_pack_prefixes");
   PSPO_REQUIRE(P >= 0 && K >= 0 && capacity >= 0, PSPO_ERR_INVALID_ARG, "P, K and capacity must be >= 0");
   PSPO_REQUIRE((int64_t)P * K <= 65535, PSPO_ERR_UNSUPPORTED, "packing supports at most 65535 completions");
   const int32_t R = P * K;

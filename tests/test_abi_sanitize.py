@@ -24,7 +24,7 @@ def test_host_code_under_asan_ubsan(tmp_path):
     san = ["-O1", "-g", "-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
            "-Xarch_host", "-fno-sanitize-recover=all", "-Xarch_host", "-fno-omit-frame-pointer"]
     srcs = [os.path.join(pbuild.CSRC, s) for s in pbuild.SOURCES] + [os.path.join(HERE, "abi_sanitize.cpp")]
-    cmd = [pbuild.hipcc(), *flags, *san, "-I", pbuild.INCLUDE, "-I", pbuild.CSRC, *srcs, "-o", exe]
+    cmd = [pbuild.hipcc(), *flags, *san, "-I", pbuild.INCLUDE, "-I", pbuild.CSRC, *srcs, "-o", exe, *pbuild.LINK_FLAGS]
     res = subprocess.run(cmd, capture_output=True, text=True)
     assert res.returncode == 0, res.stderr[-3000:]
     env = dict(os.environ, ASAN_OPTIONS="detect_leaks=0:abort_on_error=1",
