@@ -375,7 +375,8 @@ def test_target_entries_exact(name, seed):
     """The target entry of each logit-gradient row, delta (1 - p(o)), is applied in float32
     (d_hidden += g W[o], d_w_head[o] += g h); only the other entries, -delta p, pass through
     bf16.  With a flat softmax the target entry carries almost all of a row's norm, so the
-    gradients sit far inside the benchmark spec's tolerance: the bound here is a hundredth of it
+    gradients sit far inside the gradient tolerance of the parity tests (GRAD_REL_L2): the
+    bound here is a hundredth of it
     (a path that rounded the target entries to bf16 lands at ~1.5e-3)."""
     wl, lp = _workload(name)
     out = pipeline.Step(pipeline.upload(wl, lp))(seed=seed)
