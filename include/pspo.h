@@ -18,6 +18,9 @@
  *  - The caller allocates and owns every buffer; the library never allocates
  *    or frees memory and keeps no mutable global state, so calls on distinct
  *    streams are independent.  Outputs must not alias inputs.
+ *  - No call synchronises (outside debug mode) or records a memset, so every
+ *    call can be captured into a HIP graph and replayed; a replay repeats the
+ *    call with the arguments it was captured with (sizes included).
  *  - Every call is asynchronous on `stream` (0 = the null stream) and returns
  *    a pspo_status.  Errors detectable from the arguments alone are returned
  *    before anything is enqueued (the thread-local pspo_last_error() says
