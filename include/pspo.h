@@ -17,10 +17,14 @@
  *    device; "host" pointers are host memory.  Sizes and scalars are by value.
  *  - The caller allocates and owns every buffer; the library never allocates
  *    or frees memory and keeps no mutable global state, so calls on distinct
- *    streams are independent.  Outputs must not alias inputs.
+ *    streams are independent (pspo_design_cutoffs_noalloc's static array is
+ *    the one exception; see there).  Outputs must not alias inputs.
  *  - No call synchronises (outside debug mode) or records a memset, so every
  *    call can be captured into a HIP graph and replayed; a replay repeats the
- *    call with the arguments it was captured with (sizes included).
+ *    call with the arguments it was captured with (sizes included).  The
+ *    first call on a device checks the device's architecture, and the first
+ *    pspo_design_cutoffs_noalloc call looks up its array's address: make
+ *    those first calls outside a capture.
  *  - Every call is asynchronous on `stream` (0 = the null stream) and returns
  *    a pspo_status.  Errors detectable from the arguments alone are returned
  *    before anything is enqueued (the thread-local pspo_last_error() says
