@@ -12,13 +12,19 @@ V = 152064; 8 prompts x 8 rollouts; lengths lognormal around 2048, clipped
 to [128, 8192]; per-prompt discrete Beta(a, b) cutoff laws, a, b ~ U[1, 4];
 old log-probs = new + N(0, 0.1^2)).
 
-Prints one JSON line.  `roofline` covers the loss call (the forward, logit-
-gradient, dW and dH matrix-core kernels it launches), timed with HIP events
-on the stream it runs on: achieved = (2 n_fwd + 4 n_bwd) V d algorithmic
-flops / mean call duration, where n_fwd counts the tokens of completions with a
-nonzero advantage (the only ones whose loss term can be nonzero) and n_bwd the
-tokens whose logit gradient is not identically zero (the others add nothing to
-dH or dW); the kernels skip the rest.
+Prints one JSON line.  `roofline` is that of the dominant kernel, the forward
+logit product (one launch per call, about a quarter of a step): achieved = its
+algorithmic flops per launch, 2 n_fwd V d, / its mean duration, timed live
+over the timed steps with HIP events that the library records on the call's
+own stream around each of its matrix-core products (pspo_timing_start; the
+rocprofv3 kernel trace of the same command gives the same average).  n_fwd
+counts the tokens of completions with a nonzero advantage (the only ones whose
+loss term can be nonzero).  `products` gives the same for each product of the
+call (the logit-gradient recompute, dW and dH per vocabulary chunk, with their
+K-split tails), and `loss_call` the whole call: (2 n_fwd + 4 n_bwd) V d needed
+flops / mean call duration, n_bwd counting the tokens whose logit gradient is
+not identically zero (the others add nothing to dH or dW; the kernels skip
+them); `pct_bf16_peak` is that whole-call figure.
 `dense_equivalent_tflops` is 6 N V d / duration, the rate a path that ran the
 gradient products over every token would need for the same throughput.
 `full_trajectory_control` times the untruncated update on the same batch, and
@@ -248,6 +254,7 @@ def bench_proxy(args):
     torch.cuda.synchronize()
     s, e = ev(), ev()
     proxy_ms = []
+    pspo.timing_start(4 * args.steps)   # events on the call's stream around its matrix-core product
     s.record(stream)
     for _ in range(args.steps):
         m = (ev(), ev())
@@ -255,11 +262,15 @@ def bench_proxy(args):
         proxy_ms.append(m)
     e.record(stream)
     torch.cuda.synchronize()
+    timing = pspo.timing_stop()
+    assert timing["proxy"]["count"] == args.steps, timing["proxy"]
+    prod_ms = timing["proxy"]["ms"] / timing["proxy"]["count"]
     ms = s.elapsed_time(e) / args.steps
     pms = float(np.mean([a.elapsed_time(b) for a, b in proxy_ms]))
     assert int(err.item()) == 0, "device error flag raised"
     flops = 2.0 * N * cfg.V * cfg.d
     achieved = flops / (pms * 1e-3) / 1e12
+    prod_achieved = flops / (prod_ms * 1e-3) / 1e12
     result = {
         "metric": "completion tokens/sec for computing xi (score proxy on the matrix cores + cutoff design); "
                   "% of bf16 MFMA peak",
@@ -269,9 +280,16 @@ def bench_proxy(args):
         "config": {"workload": f"{args.workload}: every completion token, d={cfg.d}, V={cfg.V}, top-16 lists, "
                                f"budget {budget:g}", "tokens": N, "steps_designed": total_T},
         "score_proxy_ms": pms, "design_ms": ms - pms,
-        "roofline": {"bound": "mfma", "kernel": "pspo_score_proxy (forward bf16 MFMA kernel + two-sum epilogue)",
-                     "flops": "2 N V d per call", "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
-                     "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None},
+        "roofline": {"bound": "mfma",
+                     "kernel": "gemm_nt_kernel<EpiProxy> (the score-proxy logit product: bf16 MFMA, two-sum "
+                               "epilogue), timed live with HIP events the library records around it",
+                     "flops": "2 N V d per launch", "launch_ms": prod_ms, "achieved": prod_achieved,
+                     "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": prod_achieved / PEAK_BF16_TFLOPS,
+                     "traffic": None},
+        "score_proxy_call": {"what": "the whole pspo_score_proxy call (operand copies, the product, row norms, "
+                                     "finalize): 2 N V d flops / its mean duration",
+                             "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                             "frac": achieved / PEAK_BF16_TFLOPS},
     }
     if not args.no_cpu_baseline:
         from threadpoolctl import threadpool_info
@@ -329,6 +347,7 @@ def main():
     loss_ms = []
     starts, ends, pack_marks = [], [], []
     t_start, t_end = ev(), ev()
+    pspo.timing_start(64 * args.steps)   # events on the call's stream around each product
     torch.cuda.synchronize()
     t_start.record(stream)
     N = 0
@@ -348,6 +367,7 @@ def main():
         ends.append(e)
     t_end.record(stream)
     torch.cuda.synchronize()
+    timing = pspo.timing_stop()
     ms_step = t_start.elapsed_time(t_end) / args.steps
     loss_ms = [s.elapsed_time(e) for s, e in zip(starts, ends)]
     loss_avg = float(np.mean(loss_ms))
@@ -414,14 +434,31 @@ def main():
     flops = (2.0 * n_fwd + 4.0 * n_bwd) * cfg.V * cfg.d
     achieved = flops / (loss_avg * 1e-3) / 1e12
     dense_equiv = 6.0 * N * cfg.V * cfg.d / (loss_avg * 1e-3) / 1e12
+    # each matrix-core product of the call, timed live (events on the call's stream)
+    prod_flops = {"forward": 2.0 * n_fwd * cfg.V * cfg.d, "logit_grad": 2.0 * n_bwd * cfg.V * cfg.d,
+                  "dw": 2.0 * n_bwd * cfg.V * cfg.d, "dh": 2.0 * n_bwd * cfg.V * cfg.d}
+    products = {}
+    for k, f in prod_flops.items():
+        t = timing[k]
+        assert t["count"] > 0 and t["count"] % args.steps == 0, (k, t)
+        per_call = t["ms"] / args.steps
+        tf = f / (per_call * 1e-3) / 1e12
+        products[k] = {"ms_per_call": per_call, "records_per_call": t["count"] // args.steps,
+                       "flops_per_call": f, "achieved": tf, "frac": tf / PEAK_BF16_TFLOPS}
+    products["what"] = ("ms per call from HIP events around each product (all its launches; the logit-"
+                        "gradient, dW and dH products once per vocabulary chunk, dW and dH with their K-split "
+                        "tails); flops: the forward over n_fwd tokens, the other three over n_bwd tokens "
+                        "(the logit-gradient product recomputes the logits the forward did not keep)")
+    fwd_launch_ms = timing["forward"]["ms"] / timing["forward"]["count"]
     # HBM bytes per call from the committed counter runs, only while the kernels
     # are still the ones those counters were taken on
-    traffic, counters = None, None
+    traffic, fwd_traffic, counters = None, None, None
     if os.path.exists(TRAFFIC_FILE):
         with open(TRAFFIC_FILE) as f:
             t = json.load(f)
         if t.get("N") == N and t.get("workload") == args.workload and t.get("source_hash") == source_hash():
             traffic = t.get("bytes_per_call")
+            fwd_traffic = t["per_kernel_fetch_bytes"]["EpiForward"] + t["per_kernel_write_bytes"]["EpiForward"]
             # rocprofv3 counters of the same kernels and batch (committed under profiles/):
             # matrix-core busy fraction and clock of the products, and the memory-side
             # (beyond L2) read and write volume per call as rates at this run's call time
@@ -477,15 +514,23 @@ def main():
         "dense_equivalent_tflops": dense_equiv,
         "roofline": {
             "bound": "mfma",
-            "kernel": "pspo_loss_fwd_bwd (forward, logit-gradient recompute, dW and dH bf16 MFMA kernels; "
-                      "no logit stored)",
-            "flops": "(2 n_fwd + 4 n_bwd) V d per call: forward over the tokens of completions with "
-                     "A != 0, dH and dW over the tokens with a nonzero logit gradient",
-            "achieved": achieved,
+            "kernel": "gemm_nt_kernel<EpiForward> (the forward logit product of pspo_loss_fwd_bwd: bf16 MFMA, "
+                      "per-token softmax partials in the epilogue, no logit stored)",
+            "flops": "2 n_fwd V d per launch (the tokens of completions with A != 0)",
+            "launch_ms": fwd_launch_ms,
+            "achieved": prod_flops["forward"] / (fwd_launch_ms * 1e-3) / 1e12,
             "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s",
-            "frac": achieved / PEAK_BF16_TFLOPS,
-            "traffic": traffic,
+            "frac": prod_flops["forward"] / (fwd_launch_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
+            "traffic": fwd_traffic,
+        },
+        "products": products,
+        "loss_call": {
+            "what": "the whole pspo_loss_fwd_bwd call: (2 n_fwd + 4 n_bwd) V d needed flops per call (forward "
+                    "over the tokens of completions with A != 0, dH and dW over the tokens with a nonzero "
+                    "logit gradient) / mean call duration; traffic: memory-side bytes of all its kernels",
+            "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+            "frac": achieved / PEAK_BF16_TFLOPS, "traffic": traffic,
         },
     }
     if counters is not None:

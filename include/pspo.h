@@ -88,7 +88,7 @@ const char* pspo_status_string(int status);
 /* Detail of the last error returned on the calling thread ("" if none). */
 const char* pspo_last_error(void);
 
-/* Version of this ABI (incremented on any incompatible change). */
+/* Version of this ABI (incremented on any change of its calls). */
 int pspo_abi_version(void);
 
 /*
@@ -366,10 +366,49 @@ int pspo_design_cutoffs_noalloc(const double* w, const int64_t* xi_off, int32_t 
                                 int32_t* err_flag, hipStream_t stream);
 
 /* ------------------------------------------------------------------------
- * Measurement entry point.  Not a step of the method and not used by any
- * call above: it exists so that a benchmark can report the sustained
- * matrix-core rate next to the products' achieved rate.
+ * Measurement entry points.  Not steps of the method: they exist so that a
+ * benchmark can time each matrix-core product of a call with HIP events on
+ * the call's own stream, and report the sustained matrix-core rate next to
+ * the products' achieved rate.
  * ------------------------------------------------------------------------ */
+
+/* Product kinds of the per-product timing (index of pspo_timing_stop's arrays). */
+enum {
+  PSPO_TIME_FORWARD = 0,      /* pspo_loss_fwd_bwd: the forward logit product (all its launches)     */
+  PSPO_TIME_LOGIT_GRAD = 1,   /* pspo_loss_fwd_bwd: one vocabulary chunk's logit-gradient product
+                                 (or, with PSPO_KEEP_LOGITS, the kept chunk's conversion)            */
+  PSPO_TIME_DW = 2,           /* pspo_loss_fwd_bwd: one chunk's dW product with its K-split tail      */
+  PSPO_TIME_DH = 3,           /* pspo_loss_fwd_bwd: one chunk's dH product with its K-split tail      */
+  PSPO_TIME_PROXY = 4,        /* pspo_score_proxy: the score-proxy logit product (all its launches)  */
+  PSPO_TIMED_KINDS = 5
+};
+
+/*
+ * Starts per-product timing on the calling thread: until pspo_timing_stop,
+ * each pspo_loss_fwd_bwd and pspo_score_proxy call made on this thread records
+ * a pair of HIP events on its stream around each of its matrix-core products
+ * (one record per product and chunk, as listed above), for the first
+ * `max_records` records; later products are not timed.  The events are
+ * created here (2 * max_records hipEventCreate), so start outside any graph
+ * capture.  The recording adds two event records per product and no
+ * synchronisation.
+ *  max_records  1 .. 2^20.
+ * Errors: PSPO_ERR_INVALID_ARG if timing is already started on this thread
+ * or max_records is out of range; PSPO_ERR_HIP if an event cannot be created.
+ */
+int pspo_timing_start(int32_t max_records);
+
+/*
+ * Stops the timing started on this thread: waits for every recorded event and
+ * returns, per product kind, the summed elapsed milliseconds and the number
+ * of records, then destroys the events.
+ *  ms     host, float64 [PSPO_TIMED_KINDS], written.
+ *  count  host, int32 [PSPO_TIMED_KINDS], written.
+ * Errors: PSPO_ERR_INVALID_ARG if timing is not started on this thread or a
+ * pointer is NULL; PSPO_ERR_HIP if an event wait fails (the events are
+ * destroyed and timing stops either way).
+ */
+int pspo_timing_stop(double* ms, int32_t* count);
 
 /*
  * `blocks` work-groups of 256 threads each run `iters` rounds of 16

@@ -59,6 +59,21 @@ struct TraceRange {
     if (int rc_ = ::pspo::after_launch((kernel), (stream))) return rc_; \
   } while (0)
 
+// Per-product timing (the measurement mode of pspo_timing_start): begin()
+// records the start event of a product of `kind` on the call's stream and
+// end() its end event; both do nothing while timing is off on this thread or
+// its records are used up.  They return PSPO_OK or PSPO_ERR_HIP.
+class ProductTimer {
+ public:
+  explicit ProductTimer(hipStream_t stream) : stream_(stream) {}
+  int begin(int kind);
+  int end();
+
+ private:
+  hipStream_t stream_;
+  int rec_ = -1;
+};
+
 inline bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
 inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }

@@ -1416,6 +1416,8 @@ int pspo_loss_fwd_bwd(const uint16_t* hidden, const uint16_t* w_head, const int3
   // 2. forward logits -> per-tile softmax partials (target logits apart): the
   //    vocabulary tiles whose rows are all token ids, then a partial last one
   {
+    ProductTimer timer(stream);
+    if (int rc = timer.begin(PSPO_TIME_FORWARD)) return rc;
     const int tiles_full = V / kTileM, kept_tiles = zk != nullptr ? (int)(pl.Vc / kTileM) : 0;
     if (tiles_full > 0) {
       // the kept tiles' stores spread over the XCDs
@@ -1430,6 +1432,7 @@ int pspo_loss_fwd_bwd(const uint16_t* hidden, const uint16_t* w_head, const int3
       EpiForward<false> e{V, N, pl.Npad, tiles_full, part_m, part_l, n_fwd, zk, kept_tiles, tiles_tok_n};
       if (int rc = launch_gemm(g, e, stream)) return rc;
     }
+    if (int rc = timer.end()) return rc;
   }
   // the target logit of each forward column (the column's token row and target)
   hipLaunchKernelGGL(row_dots_kernel, dim3((unsigned)(pl.Npad / 4)), dim3(256), 0, stream, hidden, w_head, d, V, N,
@@ -1463,6 +1466,8 @@ int pspo_loss_fwd_bwd(const uint16_t* hidden, const uint16_t* w_head, const int3
   for (int64_t v0 = 0; v0 < pl.Vpad; v0 += pl.Vc) {
     const int64_t vc = (pl.Vpad - v0) < pl.Vc ? (pl.Vpad - v0) : pl.Vc;
     const int ctiles = (int)(vc / kTileM);
+    ProductTimer t_grad(stream), t_dw(stream), t_dh(stream);
+    if (int rc = t_grad.begin(PSPO_TIME_LOGIT_GRAD)) return rc;
     if (v0 == 0 && zk != nullptr) {
       hipLaunchKernelGGL(logit_grad_kept_kernel, dim3((unsigned)(pl.Vc / 128), (unsigned)(pl.Npad / 32)), dim3(256), 0,
                          stream, zk, part_m, pl.Npad, tiles_tok_n, (int)pl.Vc, V, N, n_act, act_fwd, act_lse,
@@ -1486,6 +1491,7 @@ int pspo_loss_fwd_bwd(const uint16_t* hidden, const uint16_t* w_head, const int3
         if (int rc = launch_gemm(g, e, stream)) return rc;
       }
     }
+    if (int rc = t_grad.end()) return rc;
     hipLaunchKernelGGL(zero_targets_kernel, dim3((unsigned)std::min<int64_t>((pl.Npad + 255) / 256, 1024)), dim3(256),
                        0, stream, N, n_act, act_tgt, (int)v0, (int)vc, dN, pl.Vc / kTileK, dT, pl.Npad / kTileK);
     PSPO_LAUNCHED("zero_targets_kernel", stream);
@@ -1493,15 +1499,19 @@ int pspo_loss_fwd_bwd(const uint16_t* hidden, const uint16_t* w_head, const int3
       GemmShape g{dT, pl.Vc, (int)vc, hT, pl.dpad, d, (int)pl.Npad, ctiles, tiles_d, n_act, kDynK, 0,
                   kTileM, pl.Npad * kTileM * 2};
       EpiDW e{V, d, (int)v0, d_w_head, accumulate};
+      if (int rc = t_dw.begin(PSPO_TIME_DW)) return rc;
       if (int rc = launch_gemm_split_tail(g, e, TailDW{V, d, (int)v0, d_w_head, accumulate}, slab, stream))
         return rc;
+      if (int rc = t_dw.end()) return rc;
     }
     {
       GemmShape g{dN, pl.Npad, (int)pl.Npad, wT + (v0 / pl.Vc) * pl.dpad * pl.Vc, pl.dpad, d, (int)vc, tiles_tok_m,
                   tiles_d, n_act, kDynM, 0, kTileLcm, pl.Vc * kTileLcm * 2};
       EpiDH e{N, d, d_hidden, v0 == 0, act_idx, n_act};
+      if (int rc = t_dh.begin(PSPO_TIME_DH)) return rc;
       if (int rc = launch_gemm_split_tail(g, e, TailDH{N, d, d_hidden, v0 == 0, act_idx, n_act}, slab, stream))
         return rc;
+      if (int rc = t_dh.end()) return rc;
     }
   }
   // 7. the target entries of the logit gradient, in float32: the backward

@@ -290,6 +290,8 @@ int pspo_score_proxy(const uint16_t* hidden, const uint16_t* w_head, const int32
   PSPO_LAUNCHED("kblock_rows_kernel", stream);
   {
     // the vocabulary tiles whose rows are all token ids, then a partial last one
+    ProductTimer timer(stream);
+    if (int rc = timer.begin(PSPO_TIME_PROXY)) return rc;
     const int tiles_full = V / kTileM;
     if (tiles_full > 0) {
       GemmShape g{wk, pl.Vpad, tiles_full * kTileM, hk, pl.Npad, N, Dk, tiles_full, tiles_tok};
@@ -306,6 +308,7 @@ int pspo_score_proxy(const uint16_t* hidden, const uint16_t* w_head, const int32
                          stream, g, e);
       PSPO_LAUNCHED("gemm_nt_kernel (score proxy)", stream);
     }
+    if (int rc = timer.end()) return rc;
   }
   // the target logit and ||h||^2 of every token, one pass over its hidden row
   hipLaunchKernelGGL(row_dots_kernel, dim3((unsigned)((N + 3) / 4)), dim3(256), 0, stream, hidden, w_head, d, V, N,

@@ -43,6 +43,8 @@ _SIGNATURES = {
     "pspo_design_cutoffs_noalloc": (ctypes.c_int, [_P, _P, _I32, _I64, ctypes.c_double, _I32, ctypes.c_double,
                                                    _P, _P, _P]),
     "pspo_mfma_loop": (ctypes.c_int, [_I32, _I32, _P, _P]),
+    "pspo_timing_start": (ctypes.c_int, [_I32]),
+    "pspo_timing_stop": (ctypes.c_int, [_P, _P]),
 }
 
 _lib = None
@@ -335,3 +337,20 @@ def mfma_loop(iters: int, blocks: int, out: Optional[torch.Tensor] = None) -> to
         raise ValueError("out needs blocks * 256 floats")
     _check(load().pspo_mfma_loop(int(iters), int(blocks), _ptr(out), _stream()))
     return out
+
+
+TIMED_KINDS = ("forward", "logit_grad", "dw", "dh", "proxy")   # PSPO_TIME_* order
+
+
+def timing_start(max_records: int) -> None:
+    """Per-product timing of the loss and score-proxy calls made on this thread (HIP events
+    on each call's stream around each matrix-core product), until timing_stop()."""
+    _check(load().pspo_timing_start(int(max_records)))
+
+
+def timing_stop() -> dict:
+    """Waits for the recorded events; per product kind (TIMED_KINDS): summed ms and record count."""
+    ms = (ctypes.c_double * len(TIMED_KINDS))()
+    cnt = (ctypes.c_int32 * len(TIMED_KINDS))()
+    _check(load().pspo_timing_stop(ctypes.cast(ms, _P), ctypes.cast(cnt, _P)))
+    return {k: {"ms": float(ms[i]), "count": int(cnt[i])} for i, k in enumerate(TIMED_KINDS)}

@@ -29,17 +29,32 @@ def _declared():
 
 def test_exports_every_declared_symbol(lib):
     names = _declared()
-    assert len(names) == 15
+    assert len(names) == 17
     for name in names:
         assert hasattr(lib, name), name
     assert sorted(pspo.exported_symbols()) == names
 
 
 def test_version_and_status_strings(lib):
-    assert lib.pspo_abi_version() == 5
+    assert lib.pspo_abi_version() == 6
     assert lib.pspo_status_string(0) == b"PSPO_OK"
     assert lib.pspo_status_string(3) == b"PSPO_ERR_WORKSPACE"
     assert lib.pspo_status_string(99) == b"PSPO_ERR_UNKNOWN"
+
+
+def test_timing_argument_errors(lib):
+    """The measurement mode's host paths: nothing to stop before a start, a start needs
+    1 <= max_records <= 2^20 (the event creation itself needs a device)."""
+    ms = (ctypes.c_double * 5)()
+    cnt = (ctypes.c_int32 * 5)()
+    assert lib.pspo_timing_stop(ms, cnt) == INVALID
+    assert b"not started" in lib.pspo_last_error()
+    assert lib.pspo_timing_start(0) == INVALID
+    assert lib.pspo_timing_start(-3) == INVALID
+    assert lib.pspo_timing_start((1 << 20) + 1) == INVALID
+    assert lib.pspo_timing_stop(ms, cnt) == INVALID   # still not started
+    with pytest.raises(pspo.PspoError, match="INVALID_ARG"):
+        pspo.timing_stop()
 
 
 def _vx(xi, off):
