@@ -320,3 +320,34 @@ def test_design_noalloc_argument_errors(lib):
     assert call(T=2 ** 19 + 1) == UNSUPPORTED          # beyond the static scratch (8 MiB)
     assert b"2^19" in lib.pspo_last_error()
     assert lib.pspo_design_workspace_bytes(2 ** 19) <= 8 << 20 < lib.pspo_design_workspace_bytes(2 ** 19 + 1)
+
+
+def test_validate_xi_host_agrees_with_the_oracle(lib):
+    """The library's host check of survival tables accepts exactly the tables the
+    oracle's check accepts (Sec. 3.2: 1 >= xi_1 >= ... >= xi_T > 0), on random tables
+    built to sit on and around every boundary: exact 0 and 1, values just above 1 or
+    just below the previous one, NaN, +-inf, denormals, empty prompts."""
+    from hypothesis import given, settings, strategies as st
+    from oracle import cutoffs as ocut
+
+    edge = st.sampled_from([0.0, 1.0, np.nextafter(1.0, 2.0), 0.5, np.nextafter(0.5, 0.0),
+                            np.nextafter(0.5, 1.0), 5e-324, 2.0 ** -40, -0.0, float("nan"), float("inf"),
+                            -float("inf"), -1e-300])
+    val = st.one_of(edge, st.floats(min_value=0.0, max_value=1.0), st.floats(allow_nan=True))
+    prompt = st.lists(val, min_size=0, max_size=6)
+
+    @settings(max_examples=400, deadline=None, derandomize=True)
+    @given(st.lists(prompt, min_size=1, max_size=4), st.booleans())
+    def check(prompts, sort_desc):
+        if sort_desc:   # mostly-valid tables too: each prompt's values sorted non-increasing
+            prompts = [sorted(p, reverse=True) if not any(np.isnan(p)) else p for p in prompts]
+        xi = np.array([v for p in prompts for v in p], dtype=np.float64)
+        off = np.concatenate([[0], np.cumsum([len(p) for p in prompts])]).astype(np.int64)
+        try:
+            ocut.validate_xi(xi, off)
+            want = OK
+        except ValueError:
+            want = BAD_XI
+        assert _vx(xi, off) == want, (prompts, lib.pspo_last_error())
+
+    check()
