@@ -496,6 +496,8 @@ def main():
             "parallelism": "single GPU",
         },
         "loss_call_ms": loss_avg,
+        "loss_call_ms_spread": {"median": float(np.median(loss_ms)), "min": float(np.min(loss_ms)),
+                                "max": float(np.max(loss_ms))},
         # the last timed step's own numbers (the loss call's stats output)
         "step_stats": {
             "loss": float(out["loss"].item()),
