@@ -79,3 +79,53 @@ def test_score_proxy_token_count_edges(N, V, d):
     np.testing.assert_allclose(out["gamma"].cpu().numpy().astype(np.float64), ref["gamma"], rtol=1e-4, atol=0)
     np.testing.assert_allclose(out["p_sq"].cpu().numpy().astype(np.float64), ref["p_sq"], rtol=1e-4, atol=0)
     assert np.max(np.abs(out["logp"].cpu().numpy().astype(np.float64) - ref["logp"])) <= LOGP_ATOL
+
+
+# vocabularies around the 384-row tile (down to a single entry) and widths that are no
+# multiple of 32 or 64 (down to one 16-byte piece per row), for the loss call and the
+# score proxy; a single-entry vocabulary has p = 1 and every gradient exactly zero
+SHAPES = [(1, 128, 300), (2, 8, 769), (383, 24, 300), (384, 40, 257), (385, 264, 300), (767, 520, 200),
+          (769, 136, 385), (3001, 8, 1), (3001, 200, 1537)]
+
+
+@pytest.mark.parametrize("V,d,N", SHAPES)
+def test_vocabulary_and_width_edges(V, d, N):
+    from oracle import score_proxy as osp
+    print(f"[edges] V={V} d={d} N={N}", flush=True)
+    rng = np.random.default_rng(31 * V + 7 * d + N)
+    R = 5
+    h = synth.round_to_bf16_bits(rng.normal(0.0, 1.0, (N, d)).astype(np.float32))
+    W = synth.round_to_bf16_bits(rng.normal(0.0, 0.3 / np.sqrt(d) * 4, (V, d)).astype(np.float32))
+    tgt = rng.integers(0, V, N).astype(np.int32)
+    seq = np.sort(rng.integers(0, R, N)).astype(np.int32)
+    adv = rng.choice([-1.0, 0.0, 1.0], R).astype(np.float32)
+    weight = (1.0 + rng.random(N)).astype(np.float32)
+    lp_old = (ohead.target_logprob(h, W, tgt) + rng.normal(0.0, 0.2, N)).astype(np.float32)
+    el, eh, scale = 0.2, 0.28, 1.0 / R
+    ref = ohead.loss_fwd_bwd(h, W, tgt, lp_old, weight, seq, adv, f32(el), f32(eh), f32(scale))
+
+    t = lambda a, dt: torch.from_numpy(np.ascontiguousarray(a)).to(device="cuda", dtype=dt)
+    err = torch.zeros(1, dtype=torch.int32, device="cuda")
+    out = pspo.loss_fwd_bwd(_bits_tensor(h), _bits_tensor(W), t(tgt, torch.int32), t(lp_old, torch.float32),
+                            t(weight, torch.float32), t(seq, torch.int32), t(adv, torch.float32), N, el, eh, scale,
+                            err_flag=err)
+    prox = pspo.score_proxy(_bits_tensor(h), _bits_tensor(W), t(tgt, torch.int32), N, want_p_sq=True)
+    torch.cuda.synchronize()
+    assert int(err.item()) == 0
+    loss = float(out["loss"].item())
+    assert abs(loss - ref["loss"]) <= LOSS_RTOL * max(abs(ref["loss"]), 1e-3 * ref["abs_mass"]), (loss, ref["loss"])
+    np.testing.assert_allclose(out["logp_new"].cpu().numpy(), ref["logp_new"], rtol=0, atol=LOGP_ATOL)
+    st = out["stats"].cpu().numpy()
+    A = adv.astype(np.float64)[seq]
+    assert st[2] == np.count_nonzero(A == 0) and st[4] == np.count_nonzero(ref["delta"])
+    dh, dw = out["d_hidden"].cpu().numpy(), out["d_w_head"].cpu().numpy()
+    if V == 1:   # p = 1: every logit-gradient row is zero (up to the log-prob's rounding)
+        assert np.abs(dh).max() <= 1e-5 and np.abs(dw).max() <= 1e-5
+    else:
+        assert rel_l2(dh, ref["d_hidden"]) <= GRAD_REL_L2
+        assert rel_l2(dw, ref["d_w"]) <= GRAD_REL_L2
+    pref = osp.score_proxy(h, W, tgt)
+    assert np.max(np.abs(prox["logp"].cpu().numpy().astype(np.float64) - pref["logp"])) <= LOGP_ATOL
+    np.testing.assert_allclose(prox["p_sq"].cpu().numpy().astype(np.float64), pref["p_sq"], rtol=1e-4, atol=0)
+    np.testing.assert_allclose(prox["gamma"].cpu().numpy().astype(np.float64), pref["gamma"], rtol=1e-4,
+                               atol=1e-6 * float(np.max(pref["gamma"], initial=0.0)) if V > 1 else 1e-5)
