@@ -141,3 +141,26 @@ def test_computing_xi_end_to_end():
     assert np.array_equal(H.cpu().numpy(), H_ref)
     for p in range(cfg.P):
         assert xi_np[xi_off[p]:xi_off[p + 1]].sum() == pytest.approx(budget, rel=1e-9)
+
+
+@pytest.mark.parametrize("variant", [cd.OPTIMIZED, cd.HEURISTIC])
+def test_design_cutoffs_lds_and_global_paths(variant):
+    """Prompt horizons on both sides of the solve's two LDS limits (its weights and block
+    stack in the 160 KB of LDS up to T = 8192, the weights alone up to T = 20480, both in
+    device memory beyond), in one call, against the oracle; the no-allocation entry point
+    gives the same bits."""
+    T = np.array([100, 8191, 8192, 8193, 20480, 20481, 30000], dtype=np.int64)
+    xi_off = np.concatenate([[0], np.cumsum(T)]).astype(np.int64)
+    P, total = len(T), int(xi_off[-1])
+    w = _random_weights(xi_off, 17)
+    budget = 600.0
+    print(f"[design paths] T = {T.tolist()} variant={variant}", flush=True)
+    err = torch.zeros(1, dtype=torch.int32, device="cuda")
+    tw, toff = _cuda(w, torch.float64), _cuda(xi_off, torch.int64)
+    xi = pspo.design_cutoffs(tw, toff, P, total, budget, variant, err_flag=err)
+    out = torch.full((total,), float("nan"), dtype=torch.float64, device="cuda")
+    xi_na = pspo.design_cutoffs_noalloc(tw, toff, P, total, budget, out, variant=variant, err_flag=err)
+    torch.cuda.synchronize()
+    assert int(err.item()) == 0
+    assert torch.equal(xi, xi_na)
+    np.testing.assert_allclose(xi.cpu().numpy(), cd.design_tables(w, xi_off, budget, variant), rtol=1e-12)
