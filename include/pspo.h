@@ -404,9 +404,9 @@ int pspo_timing_start(int32_t max_records);
  * of records, then destroys the events.
  *  ms     host, float64 [PSPO_TIMED_KINDS], written.
  *  count  host, int32 [PSPO_TIMED_KINDS], written.
- * Errors: PSPO_ERR_INVALID_ARG if timing is not started on this thread or a
- * pointer is NULL; PSPO_ERR_HIP if an event wait fails (the events are
- * destroyed and timing stops either way).
+ * Errors: PSPO_ERR_INVALID_ARG if timing is not started on this thread, or
+ * if a pointer is NULL; PSPO_ERR_HIP if an event wait fails.  Once timing was
+ * started, the call ends it whatever it returns (the events are destroyed).
  */
 int pspo_timing_stop(double* ms, int32_t* count);
 
