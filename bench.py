@@ -58,6 +58,7 @@ sys.path.insert(0, ROOT)
 PEAK_BF16_TFLOPS = 2516.6     # MI355X dense bf16 MFMA (256 CUs x 2.4 GHz x 4096 flop/clk)
 GOLDEN = os.path.join(ROOT, "tests", "golden")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "loss_fwd_bwd_qwen7b_traffic.json")
+XI_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "computing_xi_qwen7b_traffic.json")
 
 
 def source_hash():
@@ -271,6 +272,19 @@ def bench_proxy(args):
     flops = 2.0 * N * cfg.V * cfg.d
     achieved = flops / (pms * 1e-3) / 1e12
     prod_achieved = flops / (prod_ms * 1e-3) / 1e12
+    # memory-side bytes per launch of the score-proxy product from the committed counter
+    # runs, only while the kernels are the ones they were taken on
+    traffic, counters = None, None
+    if os.path.exists(XI_TRAFFIC_FILE):
+        with open(XI_TRAFFIC_FILE) as f:
+            t = json.load(f)
+        if t.get("N") == N and t.get("workload") == args.workload and t.get("source_hash") == source_hash():
+            traffic = t["bytes_per_launch"]
+            counters = {"source": os.path.relpath(XI_TRAFFIC_FILE, ROOT) + " (rocprofv3 --pmc runs of the same "
+                                                                           "kernel on this batch, not re-measured here)",
+                        "mfma_busy_pct": t.get("mfma_busy_pct"), "clock_ghz": t.get("clock_ghz"),
+                        "memory_read_GBps": t["fetch_bytes_per_launch"] / (prod_ms * 1e-3) / 1e9,
+                        "memory_write_GBps": t["write_bytes_per_launch"] / (prod_ms * 1e-3) / 1e9}
     result = {
         "metric": "completion tokens/sec for computing xi (score proxy on the matrix cores + cutoff design); "
                   "% of bf16 MFMA peak",
@@ -285,12 +299,14 @@ def bench_proxy(args):
                                "epilogue), timed live with HIP events the library records around it",
                      "flops": "2 N V d per launch", "launch_ms": prod_ms, "achieved": prod_achieved,
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": prod_achieved / PEAK_BF16_TFLOPS,
-                     "traffic": None},
+                     "traffic": traffic},
         "score_proxy_call": {"what": "the whole pspo_score_proxy call (operand copies, the product, row norms, "
                                      "finalize): 2 N V d flops / its mean duration",
                              "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                              "frac": achieved / PEAK_BF16_TFLOPS},
     }
+    if counters is not None:
+        result["counters"] = counters
     if not args.no_cpu_baseline:
         from threadpoolctl import threadpool_info
         from oracle import cutoff_design as ocd
